@@ -1,0 +1,199 @@
+"""Pins of the oracle's replay buffer, sampling rules and gather."""
+
+import json
+import os
+
+import numpy as np
+import pytest
+from scipy import stats
+
+from oracle import buffer as ob
+from oracle import philox
+
+
+def test_fifo_push_evicts_oldest_and_sampling_keeps_records():
+    # App. B "BufferStructure": push evicts the oldest once full
+    b = ob.FifoBuffer(3)
+    for r in range(5):
+        b.push(r)
+    assert b.records == [2, 3, 4]
+    rewards = [1.0, 0.0, 1.0]
+    ob.sample_indices(rewards, ob.RB_UNIFORM, seed=1, step=0, n_draw=10)
+    assert b.records == [2, 3, 4]
+
+
+def test_paper_worked_example_positive_bias(golden_dir):
+    with open(os.path.join(golden_dir, "pos_retain_example.json")) as f:
+        ex = json.load(f)
+    rewards = [1.0 if c else 0.0 for c in ex["correct"]]
+    n_fresh, n_pos_keep = ob.retain_split(ex["N"], ex["delta"])
+    kept = ob.retained_set(rewards, n_fresh, n_pos_keep)
+    assert [ex["names"][s] for s in kept] == ex["expected_buffer"]
+    assert len(kept) == ex["N"]
+
+
+def test_worked_example_at_printed_delta_differs():
+    # reading R8: at delta = 0.75 the stated rule does not give the printed set
+    correct = [False, True, True, False, True, True, False, True, False, False]
+    rewards = [1.0 if c else 0.0 for c in correct]
+    kept = ob.retained_set(rewards, *ob.retain_split(8, 0.75))
+    assert 6 not in kept  # z_{t-3} dropped
+    assert len(kept) == 7  # a sixth correct rollout would have to be older
+
+
+def test_retain_delta_zero_is_plain_fifo_window():
+    rng = np.random.default_rng(0)
+    rewards = (rng.random(50) < 0.3).astype(float)
+    kept = ob.retained_set(rewards, *ob.retain_split(20, 0.0))
+    assert kept == list(range(30, 50))
+
+
+def test_retain_brute_force_definition():
+    # freshest n_fresh + freshest n_pos_keep positives among the rest, by
+    # scanning from the newest record backwards
+    rng = np.random.default_rng(1)
+    for trial in range(200):
+        n = int(rng.integers(1, 40))
+        rewards = (rng.random(n) < rng.random()).astype(float)
+        nf = int(rng.integers(0, n + 3))
+        npk = int(rng.integers(0, n + 3))
+        want = set()
+        for s in range(n - 1, -1, -1):
+            if n - s <= nf:
+                want.add(s)
+        pos_taken = 0
+        for s in range(n - 1, -1, -1):
+            if s in want:
+                continue
+            if rewards[s] > 0 and pos_taken < npk:
+                want.add(s)
+                pos_taken += 1
+        assert ob.retained_set(rewards, nf, npk) == sorted(want)
+
+
+def test_uniform_chi_square():
+    n_live, n_draw = 97, 200000
+    rewards = [0.0] * n_live
+    idx = ob.sample_indices(rewards, ob.RB_UNIFORM, seed=11, step=4, n_draw=n_draw)
+    counts = np.bincount(idx, minlength=n_live)
+    chi2 = stats.chisquare(counts)
+    assert chi2.pvalue > 1e-4
+
+
+def test_uniform_draw_depends_only_on_seed_step_j():
+    rewards = [0.0] * 1000
+    a = ob.sample_indices(rewards, ob.RB_UNIFORM, seed=5, step=9, n_draw=64)
+    b = ob.sample_indices(rewards, ob.RB_UNIFORM, seed=5, step=9, n_draw=128)
+    assert a == b[:64]  # a prefix of a longer call: draws are independent
+    c = ob.sample_indices(rewards, ob.RB_UNIFORM, seed=5, step=10, n_draw=64)
+    assert a != c
+    for j in (0, 17, 63):
+        x0 = philox.draw_block(5, 9, j)[0]
+        assert a[j] == (x0 * 1000) >> 64
+
+
+def test_pos_mix_p0_equals_uniform_and_p1_only_positives():
+    rng = np.random.default_rng(3)
+    rewards = (rng.random(500) < 0.3).astype(float)
+    u = ob.sample_indices(rewards, ob.RB_UNIFORM, seed=2, step=1, n_draw=400)
+    m0 = ob.sample_indices(rewards, ob.RB_POS_MIX, seed=2, step=1, n_draw=400, p_q32=0)
+    assert u == m0
+    m1 = ob.sample_indices(rewards, ob.RB_POS_MIX, seed=2, step=1, n_draw=400,
+                           p_q32=philox.p_to_q32(1.0))
+    assert all(rewards[i] > 0 for i in m1)
+    pos = ob.positive_slots(rewards)
+    counts = np.bincount([pos.index(i) for i in m1], minlength=len(pos))
+    assert stats.chisquare(counts).pvalue > 1e-4
+
+
+def test_pos_mix_fraction_chi_square():
+    # expected positive fraction p + (1 - p) f_pos (reading R9)
+    rng = np.random.default_rng(4)
+    rewards = (rng.random(1000) < 0.3).astype(float)
+    f_pos = rewards.mean()
+    p = 0.7
+    n_draw = 50000
+    idx = ob.sample_indices(rewards, ob.RB_POS_MIX, seed=8, step=2, n_draw=n_draw,
+                            p_q32=philox.p_to_q32(p))
+    n_pos = sum(rewards[i] > 0 for i in idx)
+    expect = p + (1 - p) * f_pos
+    z = (n_pos - n_draw * expect) / np.sqrt(n_draw * expect * (1 - expect))
+    assert abs(z) < 4.5
+
+
+def test_pos_mix_no_positives_falls_back_to_uniform():
+    rewards = [0.0] * 64
+    u = ob.sample_indices(rewards, ob.RB_UNIFORM, seed=1, step=0, n_draw=32)
+    m = ob.sample_indices(rewards, ob.RB_POS_MIX, seed=1, step=0, n_draw=32,
+                          p_q32=philox.p_to_q32(1.0))
+    assert u == m
+
+
+def test_pos_retain_draws_cover_retained_set_uniformly():
+    rng = np.random.default_rng(5)
+    rewards = (rng.random(300) < 0.4).astype(float)
+    nf, npk = ob.retain_split(100, 0.5)
+    kept = ob.retained_set(rewards, nf, npk)
+    idx = ob.sample_indices(rewards, ob.RB_POS_RETAIN, seed=3, step=7,
+                            n_draw=50000, n_fresh=nf, n_pos_keep=npk)
+    assert set(idx) <= set(kept)
+    counts = np.bincount([kept.index(i) for i in idx], minlength=len(kept))
+    assert stats.chisquare(counts).pvalue > 1e-4
+    # delta = 0 over the whole table is uniform sampling, draw for draw
+    u = ob.sample_indices(rewards, ob.RB_UNIFORM, seed=3, step=7, n_draw=100)
+    r0 = ob.sample_indices(rewards, ob.RB_POS_RETAIN, seed=3, step=7, n_draw=100,
+                           n_fresh=300, n_pos_keep=0)
+    assert u == r0
+
+
+def _table(rng, n, max_len):
+    lens = rng.integers(1, max_len + 1, n)
+    off = np.zeros(n, dtype=np.int64)
+    off[1:] = np.cumsum(lens)[:-1]
+    total = int(lens.sum())
+    toks = rng.integers(0, 1000, total).astype(np.int32)
+    old = rng.standard_normal(total).astype(np.float32)
+    return off, lens, toks, old
+
+
+def test_gather_packed_windows_tile_the_stream():
+    rng = np.random.default_rng(6)
+    off, lens, toks, old = _table(rng, 40, 30)
+    adv = rng.standard_normal(40).astype(np.float32)
+    ver = rng.integers(0, 5, 40)
+    idx = [3, 3, 17, 0, 39, 22]
+    total = int(sum(lens[i] for i in idx))
+    win = 16
+    pieces = []
+    for wb in range(0, total + win, win):
+        g = ob.gather(idx, off, lens, adv, ver, toks, old, cur_version=7,
+                      layout=ob.LAYOUT_PACKED, max_tokens=win, token_begin=wb)
+        nv = g["n_tokens"]
+        assert nv == max(0, min(win, total - wb))
+        assert np.all(g["seq_of_token"][nv:] == -1)
+        pieces.append((g["tokens"][:nv], g["old_logp"][:nv], g["seq_of_token"][:nv]))
+        assert list(g["len"]) == [lens[i] for i in idx]
+        assert list(g["age"]) == [7 - ver[i] for i in idx]
+    stream_tok = np.concatenate([p[0] for p in pieces])
+    stream_seq = np.concatenate([p[2] for p in pieces])
+    want_tok = np.concatenate([toks[off[i]:off[i] + lens[i]] for i in idx])
+    want_seq = np.concatenate([[j] * lens[i] for j, i in enumerate(idx)])
+    assert np.array_equal(stream_tok, want_tok)
+    assert np.array_equal(stream_seq, want_seq)
+    assert g["cu_seqlens"][-1] == total
+    assert np.all(np.diff(g["cu_seqlens"]) == [lens[i] for i in idx])
+
+
+def test_gather_padded_rows():
+    rng = np.random.default_rng(7)
+    off, lens, toks, old = _table(rng, 10, 20)
+    adv = np.zeros(10, dtype=np.float32)
+    ver = np.zeros(10, dtype=np.int64)
+    idx = [9, 1, 1]
+    g = ob.gather(idx, off, lens, adv, ver, toks, old, 0, ob.LAYOUT_PADDED, l_max=12)
+    for j, i in enumerate(idx):
+        k = min(lens[i], 12)
+        assert np.array_equal(g["tokens"][j, :k], toks[off[i]:off[i] + k])
+        assert np.all(g["seq_of_token"][j, :k] == j)
+        assert np.all(g["seq_of_token"][j, k:] == -1)
+    assert g["n_tokens"] == sum(min(lens[i], 12) for i in idx)
