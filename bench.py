@@ -1,0 +1,254 @@
+"""Replayed-token throughput of the replay hot path on one MI355X.
+
+One step = the whole trainer-side path over one replay micro-batch:
+  rb_group_advantage  (advantages of the buffer's groups, as at insert)
+  rb_sample_gather    (uniform draws from a 1024-record FIFO buffer, packed
+                       into a 16384-token micro-batch)
+  policy_logprob_fwd  (hidden [16384, 3584] x W [152064, 3584], bf16 MFMA,
+                       online log-sum-exp)
+  policy_loss_fwd_bwd (clipped GRPO, token ratios, group advantages)
+  policy_logprob_bwd  (dhidden and dW, dW accumulated as over micro-batches)
+Inputs are synthetic (seeded), shaped like Qwen2.5-7B's LM head and the
+paper's rollout length mix; hidden states stand in for the model trunk's
+output.  All inputs are resident in HBM before timing starts.
+
+Prints one JSON line (metric: replayed tokens/s; also the fraction of the
+MI355X dense bf16 MFMA peak, a roofline record for the dominant kernel, and
+the CPU oracle timed on a bounded sample).
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+PEAK_BF16 = 2.5e15        # MI355X dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12         # MI355X HBM3E, B/s
+ROOT = os.path.dirname(os.path.abspath(__file__))
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="head7b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=256,
+                    help="tokens of the bounded sample the CPU oracle is timed on")
+    return ap.parse_args()
+
+
+def setup(wl, seed=0):
+    import torch
+
+    import paper_2604_08706_amd as rbp
+    from paper_2604_08706_amd import workloads as wlm
+
+    dev = "cuda"
+    T = wl.max_tokens
+    tab = wlm.record_table(wl, seed)
+    total = int(tab.length.sum())
+    S = {}
+    S["rewards"] = torch.from_numpy(tab.reward).to(dev)
+    S["group_off"] = torch.from_numpy(tab.group_off).to(dev)
+    S["adv_rec"] = torch.zeros(len(tab.length), dtype=torch.float32, device=dev)
+    S["len_rec"] = torch.from_numpy(tab.length.astype(np.int32)).to(dev)
+    S["off_rec"] = torch.from_numpy(tab.arena_off).to(dev)
+    S["ver_rec"] = torch.from_numpy(tab.version).to(dev)
+    S["arena_tok"] = wlm.arena_tokens(total, wl.V, seed, device=dev)
+    S["arena_old"] = torch.zeros(total, dtype=torch.float32, device=dev)
+    S["rec"] = rbp.make_records(len(tab.length), len(tab.length), 0, S["off_rec"], S["len_rec"],
+                                S["rewards"], S["adv_rec"], S["ver_rec"], S["arena_tok"],
+                                S["arena_old"])
+    hidden, W, _ = wlm.head(T, wl.d, wl.V, seed, device=dev)
+    S["hidden"], S["W"] = hidden, W
+    S["dW"] = torch.zeros((wl.V, wl.d), dtype=torch.float32, device=dev)
+    S["dh"] = torch.empty((T, wl.d), dtype=torch.float32, device=dev)
+    S["logp"] = torch.empty(T, device=dev)
+    S["lse"] = torch.empty(T, device=dev)
+    S["dlogp"] = torch.empty(T, device=dev)
+    S["loss"] = torch.zeros(1, device=dev)
+    S["stats"] = torch.zeros(4, device=dev)
+    S["ws_sample"] = rbp.workspace(rbp.RBP_OP_SAMPLE_GATHER, len(tab.length))
+    S["ws_fwd"] = rbp.workspace(rbp.RBP_OP_LOGPROB_FWD, T, wl.d, wl.V)
+    S["ws_loss"] = rbp.workspace(rbp.RBP_OP_LOSS, T)
+    S["ws_bwd"] = rbp.workspace(rbp.RBP_OP_LOGPROB_BWD, T, wl.d, wl.V)
+    S["T"] = T
+    S["tab"] = tab
+    return S
+
+
+def cfg_for(rbp, wl, step, seed=0):
+    return rbp.make_sample_cfg(rbp.RB_UNIFORM, rbp.RB_LAYOUT_PACKED, seed, step, wl.n_draw,
+                               cur_version=10, max_tokens=wl.max_tokens, token_begin=0)
+
+
+def align_old_logp(rbp, wl, S, steps, noise_sd, seed=0):
+    """Untimed: store behaviour log-probs for the tokens each step will draw,
+    as the current policy's log-probs plus staleness noise (a replayed,
+    slightly stale rollout)."""
+    import torch
+
+    from paper_2604_08706_amd import workloads as wlm
+
+    for k in steps:
+        cfg = cfg_for(rbp, wl, k, seed)
+        out = rbp.alloc_batch(cfg)
+        rbp.rb_sample_gather(S["rec"], cfg, out, S["ws_sample"])
+        rbp.policy_logprob_fwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"],
+                               S["logp"], S["lse"], S["ws_fwd"])
+        seq = out["seq_of_token"].long()
+        ok = seq >= 0
+        pos = torch.arange(S["T"], device="cuda")
+        start = out["cu_seqlens"].long()[seq.clamp(min=0)]
+        src = S["off_rec"][out["idx"].long()[seq.clamp(min=0)]] + (pos - start)
+        noise = wlm.normal(S["T"], noise_sd, 1000 + k, device="cuda")
+        S["arena_old"][src[ok]] = (S["logp"] + noise)[ok]
+    torch.cuda.synchronize()
+
+
+def run_step(rbp, wl, S, step, out, ev=None):
+    rbp.rb_group_advantage(S["rewards"], S["group_off"], S["adv_rec"])
+    rbp.rb_sample_gather(S["rec"], cfg_for(rbp, wl, step), out, S["ws_sample"])
+    if ev is not None:
+        ev[0].record()
+    rbp.policy_logprob_fwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"], S["logp"],
+                           S["lse"], S["ws_fwd"])
+    if ev is not None:
+        ev[1].record()
+    rbp.policy_loss_fwd_bwd(S["logp"], out["old_logp"], out["seq_of_token"], out["adv"],
+                            out["len"], wl.n_draw, S["loss"], S["dlogp"], S["stats"],
+                            S["ws_loss"])
+    if ev is not None:
+        ev[2].record()
+    rbp.policy_logprob_bwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"], S["lse"],
+                           S["dlogp"], S["dh"], S["dW"], S["ws_bwd"], accumulate_dW=True)
+    if ev is not None:
+        ev[3].record()
+
+
+def cpu_baseline(wl, n_tokens, seed=0):
+    """The oracle (fp64 numpy) timed on a bounded sample of the same workload:
+    the buffer draw and gather, then log-probs, loss and backward over the
+    first n_tokens tokens of the micro-batch at full d and V."""
+    import torch
+
+    from oracle import buffer as ob
+    from oracle.advantage import group_advantage
+    from oracle.grad import logprob_backward
+    from oracle.logprob import logprob
+    from oracle.loss import grpo_loss
+    from paper_2604_08706_amd import workloads as wlm
+
+    tab = wlm.record_table(wl, seed)
+    total = int(tab.length.sum())
+    tok = wlm.arena_tokens(total, wl.V, seed).numpy()
+    hidden, W, _ = wlm.head(n_tokens, wl.d, wl.V, seed)
+    h64 = hidden.to(torch.float64).numpy()
+    W64 = W.to(torch.float64).numpy()
+    t0 = time.perf_counter()
+    adv = group_advantage(tab.reward, tab.group_off)
+    idx = ob.sample_indices(tab.reward, ob.RB_UNIFORM, seed, 0, wl.n_draw)
+    old_arena = np.zeros(total, dtype=np.float32)
+    g = ob.gather(idx, tab.arena_off, tab.length, adv, tab.version, tok, old_arena, 10,
+                  ob.LAYOUT_PACKED, max_tokens=n_tokens)
+    y, seq = g["tokens"], g["seq_of_token"]
+    logp, lse = logprob(h64, W64, y, seq)
+    loss, dlogp, _ = grpo_loss(logp, logp + 0.1, seq, g["adv"], g["len"], wl.n_draw)
+    logprob_backward(h64, W64, y, lse, dlogp, seq)
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": n_tokens / dt, "unit": "replayed tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{n_tokens} tokens of one {wl.max_tokens}-token micro-batch at "
+                      f"d={wl.d}, V={wl.V} (sample+gather, advantages, log-probs, loss, "
+                      f"backward in fp64 numpy); {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
+              "data-parallel path is a design note, not part of this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2604_08706_amd as rbp
+    from paper_2604_08706_amd import workloads as wlm
+
+    wl = wlm.WORKLOADS[args.workload]
+    if wl.layout != "packed":
+        raise SystemExit("bench workload must use the packed layout")
+    S = setup(wl)
+    T = S["T"]
+    steps = list(range(args.warmup + args.steps))
+    align_old_logp(rbp, wl, S, steps, wl.noise_sd)
+    cfg0 = cfg_for(rbp, wl, 0)
+    out = rbp.alloc_batch(cfg0)
+    for k in range(args.warmup):
+        run_step(rbp, wl, S, k, out)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record()
+    for i in range(args.steps):
+        run_step(rbp, wl, S, args.warmup + i, out, evs[i])
+    stop.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / args.steps
+    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    loss_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    n_valid = int(out["n_tokens"].item())
+    tok_s = n_valid * args.steps / (ms_total / 1e3)
+    dV = wl.d * wl.V
+    frac = tok_s * 6 * dV / PEAK_BF16
+    fwd_flops = 2.0 * T * dV
+    rec = {
+        "metric": "replayed tokens/sec (fwd+bwd logprob+loss) at 7B shape; % bf16 MFMA peak",
+        "value": round(tok_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; Qwen2.5-7B-shaped LM head, log-normal rollout lengths)",
+        "config": {"workload": f"{wl.name}: packed micro-batch of {T} replayed tokens, "
+                               f"d={wl.d}, V={wl.V}, buffer {wl.n_records} records",
+                   "tokens_per_step": n_valid, "d": wl.d, "V": wl.V},
+        "mfma_peak_frac_6dV": round(frac, 4),
+        "mfma_peak_frac_8dV_executed": round(tok_s * 8 * dV / PEAK_BF16, 4),
+        "phase_ms": {"fwd": round(fwd_ms, 3), "loss": round(loss_ms, 3),
+                     "bwd": round(bwd_ms, 3),
+                     "sample+adv+rest": round(ms_step - fwd_ms - loss_ms - bwd_ms, 3)},
+        "roofline": {
+            "kernel": "policy_logprob_fwd (logits_lse_partial_kernel + lse_merge_kernel)",
+            "bound": "mfma",
+            "achieved": round(fwd_flops / (fwd_ms / 1e3) / 1e12, 2),
+            "peak": PEAK_BF16 / 1e12,
+            "unit": "TFLOP/s",
+            "frac": round(fwd_flops / (fwd_ms / 1e3) / PEAK_BF16, 4),
+            "traffic": None,
+        },
+        "wall_s_timed": round(t_wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,258 @@
+/*
+ * rbpolicy.h -- C ABI of librbpolicy.so, the MI355X (gfx950) replay-buffer
+ * policy-gradient hot path.
+ *
+ * Method: arXiv 2604.08706, "Efficient RL Training for LLMs with Experience
+ * Replay".  A trainer draws stored rollouts from a FIFO replay buffer (Sec. 3.1;
+ * App. B "BufferStructure"), re-scores every token under the current policy and
+ * trains on it with the clipped, importance-weighted GRPO objective whose old
+ * probabilities and group advantages were recorded when the rollout was
+ * generated (App. D.2).  This library is that trainer-side path for the LM head:
+ *
+ *   rb_group_advantage   advantages of a freshly generated group     (App. D.2)
+ *   rb_sample_gather     draw records and gather their tokens         (Sec. 3.1, 5; App. B, D.3)
+ *   policy_logprob_fwd   log pi(y_t) from hidden states and W         (App. D.2)
+ *   policy_loss_fwd_bwd  clipped GRPO loss and d loss / d logp        (App. D.2)
+ *   policy_logprob_bwd   d loss / d hidden and d loss / d W           (chain rule of the above)
+ *
+ * Conventions shared by every entry point:
+ *   - Pointers marked "device" are HIP device pointers (or managed memory); the
+ *     structs themselves and every scalar argument live on the host.
+ *   - Tensors are dense, row-major and contiguous.  bf16 tensors are passed as
+ *     uint16_t bit patterns (IEEE binary32 truncated to its upper 16 bits).
+ *   - The caller owns and allocates every buffer, workspace included; the
+ *     library never allocates, frees or synchronises.  Size the workspace with
+ *     rbp_workspace_bytes().  Workspace contents are scratch between calls.
+ *   - All device work is enqueued on `stream` (a hipStream_t; NULL = the null
+ *     stream) and is asynchronous to the host.
+ *   - Return value: RBP_OK (0) or a negative RBP_E* code.  Arguments are checked
+ *     on the host before anything is enqueued; on an error nothing is enqueued,
+ *     except RBP_EHIP, which reports a failed launch (outputs then undefined).
+ *     rbp_last_error() gives a thread-local description of the last failure.
+ *   - Results are bitwise reproducible for identical inputs (no floating-point
+ *     atomics; every reduction runs in a fixed order).
+ *   - No exception crosses this interface.  The library holds no mutable global
+ *     state except the thread-local error text.
+ */
+#ifndef RBPOLICY_H
+#define RBPOLICY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes --------------------------------------------------------- */
+enum {
+  RBP_OK = 0,
+  RBP_EINVAL = -1,       /* a null pointer, a size out of range, a bad enum     */
+  RBP_EUNSUPPORTED = -2, /* a shape this build does not handle (e.g. d % 8)     */
+  RBP_EWORKSPACE = -3,   /* workspace too small (see rbp_workspace_bytes)       */
+  RBP_EHIP = -4          /* a HIP launch failed                                 */
+};
+
+/* ---- sampling rules (rb_sample_cfg.mode) ----------------------------------- */
+enum {
+  RB_UNIFORM = 0,    /* i.i.d. uniform over the live records, with replacement
+                        (Sec. 4 analysis; App. C.1)                             */
+  RB_POS_MIX = 1,    /* per draw, a coin with probability p_pos picks a uniform
+                        positive record (reward > 0), else a uniform live record;
+                        no positives -> uniform.  Not in the paper.             */
+  RB_POS_RETAIN = 2  /* positive-bias sampling (Sec. 5; App. D.3): uniform over
+                        the freshest n_fresh records plus the freshest
+                        n_pos_keep positive records older than those            */
+};
+
+/* ---- batch layouts (rb_sample_cfg.layout) ---------------------------------- */
+enum {
+  RB_LAYOUT_PACKED = 0, /* drawn sequences concatenated; one window of the stream */
+  RB_LAYOUT_PADDED = 1  /* one row of l_max tokens per draw                        */
+};
+
+/* ---- operations for rbp_workspace_bytes ------------------------------------ */
+enum {
+  RBP_OP_SAMPLE_GATHER = 1, /* n = capacity of the record table              */
+  RBP_OP_LOGPROB_FWD = 2,   /* n = T                                          */
+  RBP_OP_LOSS = 3,          /* n = T                                          */
+  RBP_OP_LOGPROB_BWD = 4    /* n = tokens per backward chunk (T for one chunk) */
+};
+
+/*
+ * Record table of the replay buffer (App. B "BufferStructure"), as a ring:
+ * logical slot s (0 = oldest live record, n_live-1 = newest) is physical row
+ * (head + s) % capacity of every per-record array.  A record's tokens and the
+ * behaviour log-probabilities recorded at generation (App. D.2) are
+ * arena_tokens / arena_old_logp[arena_off .. arena_off + length).
+ */
+typedef struct rb_records {
+  int64_t n_live;                /* live records, 1 <= n_live <= capacity          */
+  int64_t capacity;              /* rows of the per-record arrays                  */
+  int64_t head;                  /* physical row of slot 0, 0 <= head < capacity   */
+  const int64_t* arena_off;      /* device [capacity]                              */
+  const int32_t* length;         /* device [capacity], tokens per record (>= 1)    */
+  const float* reward;           /* device [capacity]; > 0 means positive/correct  */
+  const float* advantage;        /* device [capacity], group advantage at insert   */
+  const int32_t* version;        /* device [capacity], policy version at generation*/
+  const int32_t* arena_tokens;   /* device [arena_size]                            */
+  const float* arena_old_logp;   /* device [arena_size]                            */
+  int64_t arena_size;            /* every record must lie inside [0, arena_size)   */
+} rb_records;
+
+/*
+ * Sampling configuration.  Draw j of a call reads the Philox4x64-10 block with
+ * counter (j, step, 0, 0) and key (seed, 0) (Salmon et al., SC'11); its first
+ * word x0 maps to an index in [0, n) as floor(x0 * n / 2^64), the high half of
+ * its second word x1 decides the stratum coin: (x1 >> 32) < p_pos_q32.  A call
+ * therefore depends only on (seed, step) and the record table: re-running a
+ * step after a restart reproduces it bit for bit.
+ */
+typedef struct rb_sample_cfg {
+  int32_t mode;          /* RB_UNIFORM / RB_POS_MIX / RB_POS_RETAIN                */
+  int32_t layout;        /* RB_LAYOUT_PACKED / RB_LAYOUT_PADDED                    */
+  uint64_t seed;
+  uint64_t step;
+  int64_t n_draw;        /* draws (sequences) in the batch, 1 .. 2^20              */
+  uint64_t p_pos_q32;    /* RB_POS_MIX: floor(p_pos * 2^32), 0 .. 2^32             */
+  int64_t n_fresh;       /* RB_POS_RETAIN: (1 - delta) N                           */
+  int64_t n_pos_keep;    /* RB_POS_RETAIN: floor(delta N)                          */
+  int32_t cur_version;   /* current policy version; age = cur_version - version    */
+  int32_t pad_;
+  int64_t max_tokens;    /* packed: window length (token capacity of the outputs)  */
+  int64_t token_begin;   /* packed: window start within the concatenated stream   */
+  int64_t l_max;         /* padded: row length                                     */
+} rb_sample_cfg;
+
+/*
+ * Outputs of rb_sample_gather, all caller-allocated device buffers.
+ * Packed: tokens / old_logp / seq_of_token have max_tokens entries; position t
+ *   holds stream position token_begin + t; past the end of the stream the
+ *   padding is token 0, old_logp 0, seq_of_token -1.  cu_seqlens[j] is the
+ *   stream position where draw j starts (prefix sums of full lengths).
+ * Padded: those arrays are [n_draw, l_max]; row j holds the first
+ *   min(len_j, l_max) tokens of draw j, then padding; cu_seqlens[j] = j * l_max.
+ * Per draw j: idx = slot drawn, adv = its advantage, len = its full length,
+ *   age = cur_version - its version.  n_tokens = valid output positions.
+ */
+typedef struct rb_batch {
+  int32_t* idx;          /* device [n_draw]                                        */
+  float* adv;            /* device [n_draw]                                        */
+  int32_t* len;          /* device [n_draw]                                        */
+  int32_t* age;          /* device [n_draw]                                        */
+  int32_t* cu_seqlens;   /* device [n_draw + 1]                                    */
+  int32_t* tokens;       /* device, see above                                      */
+  float* old_logp;       /* device, see above                                      */
+  int32_t* seq_of_token; /* device, see above; -1 marks padding                    */
+  int64_t* n_tokens;     /* device [1]                                             */
+} rb_batch;
+
+/*
+ * Draw a training batch from the replay buffer and gather it (Sec. 3.1:
+ * sampling does not remove records; Sec. 4: draws are uniform with
+ * replacement; Sec. 5 and App. D.3: positive-bias retention).  Draws are
+ * kept in draw order, duplicates included.
+ * Errors: RBP_EINVAL for null pointers, n_live outside [1, capacity], n_draw
+ *   outside [1, 2^20], an unknown mode/layout, p_pos_q32 > 2^32, negative
+ *   n_fresh/n_pos_keep, max_tokens < 1 (packed) or l_max < 1 (padded);
+ *   RBP_EWORKSPACE if ws_bytes < rbp_workspace_bytes(RBP_OP_SAMPLE_GATHER,
+ *   capacity, 0, 0).  Record offsets and lengths are trusted: the caller
+ *   guarantees each record lies inside the arena and the stream fits in
+ *   int32 positions.  RB_POS_RETAIN with an empty retained set draws slot 0.
+ */
+int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
+                     const rb_batch* out, void* ws, size_t ws_bytes,
+                     void* stream);
+
+/*
+ * Group-normalised advantage at insert time (App. D.2):
+ * A_i = (r_i - mean_g) / (std_g + eps) over group g = [group_off[g],
+ * group_off[g+1]); std uses `ddof` (1 = sample estimate); a group whose rewards
+ * are all equal (or has no degrees of freedom) gets A = 0.  fp32 arithmetic.
+ * reward, group_off, adv: device.  Groups must be non-overlapping, ascending.
+ * Errors: RBP_EINVAL for null pointers, n_groups < 0, ddof not 0 or 1, eps < 0.
+ */
+int rb_group_advantage(const float* reward, const int32_t* group_off,
+                       int32_t n_groups, int32_t ddof, float eps, float* adv,
+                       void* stream);
+
+/*
+ * Per-token log-probability of the sampled tokens under the current policy
+ * (App. D.2, temperature 1): z_t = W h_t, lse_t = log sum_v exp(z_{t,v}),
+ * logp_t = z_{t,y_t} - lse_t.  bf16 MFMA products with fp32 accumulation; the
+ * T x V logits are never written to memory (online log-sum-exp per tile).
+ * hidden  device bf16 [T, d];  W device bf16 [V, d];  tokens device int32 [T]
+ *         (each in [0, V) where not masked);
+ * seq_of_token device int32 [T] or NULL; a negative entry masks the token
+ *         (logp = 0, lse = 0);
+ * logp, lse device fp32 [T] (lse is what policy_logprob_bwd needs);
+ * ws      device, >= rbp_workspace_bytes(RBP_OP_LOGPROB_FWD, T, d, V).
+ * Errors: RBP_EINVAL (null pointers, T < 0, d < 1, V < 1);
+ *         RBP_EUNSUPPORTED (d % 8 != 0); RBP_EWORKSPACE.
+ */
+int policy_logprob_fwd(const uint16_t* hidden, const uint16_t* W,
+                       const int32_t* tokens, const int32_t* seq_of_token,
+                       int64_t T, int32_t d, int32_t V, float* logp, float* lse,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Clipped, importance-weighted GRPO objective on replayed tokens and its
+ * gradient (App. D.2), token-level ratio with per-sequence token means:
+ *   rho_t   = exp(logp_t - old_logp_t)
+ *   l_t     = min(rho_t A_i, clip(rho_t, 1 - eps_low, 1 + eps_high) A_i)
+ *   loss    = -sum_t l_t / (n_seq_total * seq_len_i)      (i = seq_of_token[t])
+ *   dlogp_t = -A_i rho_t act_t / (n_seq_total * seq_len_i), act_t = 0 iff
+ *             (A_i > 0 and rho_t > 1 + eps_high) or (A_i < 0 and rho_t < 1 - eps_low).
+ * logp, old_logp, seq_of_token device [T]; adv device fp32 [B]; seq_len device
+ * int32 [B] (full lengths, >= 1); tokens with seq_of_token < 0 are masked
+ * (dlogp = 0).  seq_of_token entries must be < B.
+ * loss_accum device fp32 [1] and stats device fp32 [4] are ACCUMULATED (+=):
+ *   stats = {sum rho, tokens clipped with zero gradient, valid tokens, sum l_t}.
+ * dlogp device fp32 [T] is overwritten.
+ * ws device, >= rbp_workspace_bytes(RBP_OP_LOSS, T, 0, 0).
+ * Errors: RBP_EINVAL (null pointers, T < 0, B < 1, n_seq_total < 1, eps < 0);
+ *         RBP_EWORKSPACE.
+ */
+int policy_loss_fwd_bwd(const float* logp, const float* old_logp,
+                        const int32_t* seq_of_token, const float* adv,
+                        const int32_t* seq_len, int64_t T, int32_t B,
+                        int64_t n_seq_total, float eps_low, float eps_high,
+                        float* loss_accum, float* dlogp, float* stats,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Backward of policy_logprob_fwd: with p_t = exp(z_t - lse_t) and
+ * dz_t = dlogp_t (e_{y_t} - p_t):  dhidden_t = W^T dz_t,  dW (+)= sum_t dz_t h_t^T.
+ * The logits are recomputed tile by tile (bf16 MFMA, fp32 accumulation); dz is
+ * rounded to bf16 for the two products.  Masked tokens get a zero dhidden row
+ * and add nothing to dW.
+ * hidden, W, tokens, seq_of_token as in policy_logprob_fwd; lse, dlogp device
+ * fp32 [T]; dhidden device fp32 [T, d] (overwritten); dW device fp32 [V, d]
+ * (overwritten, or accumulated into when accumulate_dW != 0).
+ * ws device: the tokens are processed in chunks of Tc tokens, with Tc the
+ * largest multiple of 256 (at most T rounded up to 256) whose
+ * rbp_workspace_bytes(RBP_OP_LOGPROB_BWD, Tc, d, V) fits in ws_bytes.
+ * Errors: RBP_EINVAL; RBP_EUNSUPPORTED (d % 8 != 0); RBP_EWORKSPACE (not even
+ * a 256-token chunk fits).
+ */
+int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
+                       const int32_t* tokens, const int32_t* seq_of_token,
+                       const float* lse, const float* dlogp, int64_t T,
+                       int32_t d, int32_t V, float* dhidden, float* dW,
+                       int accumulate_dW, void* ws, size_t ws_bytes,
+                       void* stream);
+
+/* Workspace bytes an operation needs (see RBP_OP_*); 0 for an invalid op. */
+size_t rbp_workspace_bytes(int op, int64_t n, int32_t d, int32_t V);
+
+/* Static text for a status code. */
+const char* rbp_status_string(int status);
+
+/* Thread-local description of the last failure in this thread ("" if none). */
+const char* rbp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RBPOLICY_H */

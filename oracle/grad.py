@@ -48,31 +48,32 @@ def logprob_backward(hidden, W, tokens, lse, dlogp, seq_of_token=None,
     return dhidden, dW
 
 
-def dhidden_rows(hidden, W, tokens, lse, dlogp, rows):
-    """dhidden of selected rows only, one row at a time (spot checks)."""
+def dz_rows(hidden, W, tokens, lse, dlogp, rows):
+    """dz_t = dlogp_t (e_{y_t} - softmax(W h_t)) for selected rows only,
+    [len(rows), V] (for spot checks at sizes where a full pass is too slow)."""
     W = np.asarray(W, dtype=np.float64)
-    out = []
-    for t in rows:
-        z = W @ np.asarray(hidden[t], dtype=np.float64)
-        dz = -float(dlogp[t]) * np.exp(z - float(lse[t]))
-        dz[int(tokens[t])] += float(dlogp[t])
-        out.append(dz @ W)
-    return np.array(out)
+    rows = list(rows)
+    H = np.asarray([np.asarray(hidden[t], dtype=np.float64) for t in rows])
+    z = H @ W.T
+    dl = np.array([float(dlogp[t]) for t in rows])
+    ls = np.array([float(lse[t]) for t in rows])
+    dz = -dl[:, None] * np.exp(z - ls[:, None])
+    dz[np.arange(len(rows)), [int(tokens[t]) for t in rows]] += dl
+    return dz
 
 
-def dW_from_rows(hidden, W, tokens, lse, dlogp, rows, v_lo=0, v_hi=None):
+def dhidden_rows(hidden, W, tokens, lse, dlogp, rows, dz=None):
+    """dhidden of selected rows only: W^T dz_t."""
+    if dz is None:
+        dz = dz_rows(hidden, W, tokens, lse, dlogp, rows)
+    return dz @ np.asarray(W, dtype=np.float64)
+
+
+def dW_from_rows(hidden, W, tokens, lse, dlogp, rows, v_lo=0, v_hi=None, dz=None):
     """Rows [v_lo, v_hi) of dW = sum over the given token rows of dz_t h_t^T
-    (exact dW when every other token has dlogp = 0)."""
-    W = np.asarray(W, dtype=np.float64)
-    v_hi = W.shape[0] if v_hi is None else v_hi
-    Wb = W[v_lo:v_hi]
-    acc = np.zeros_like(Wb)
-    for t in rows:
-        h = np.asarray(hidden[t], dtype=np.float64)
-        z = W @ h
-        dz = -float(dlogp[t]) * np.exp(z[v_lo:v_hi] - float(lse[t]))
-        y = int(tokens[t])
-        if v_lo <= y < v_hi:
-            dz[y - v_lo] += float(dlogp[t])
-        acc += np.outer(dz, h)
-    return acc
+    (the exact dW when every other token has dlogp = 0)."""
+    if dz is None:
+        dz = dz_rows(hidden, W, tokens, lse, dlogp, rows)
+    v_hi = dz.shape[1] if v_hi is None else v_hi
+    H = np.asarray([np.asarray(hidden[t], dtype=np.float64) for t in rows])
+    return dz[:, v_lo:v_hi].T @ H

@@ -1,0 +1,369 @@
+// Replay-buffer sampling and batch gather (rb_sample_gather).
+//
+// Paper: the buffer is a FIFO list whose sampling does not remove records
+// (Sec. 3.1; App. B "BufferStructure"); draws are uniform with replacement
+// (Sec. 4); positive-bias retention keeps the freshest (1-delta)N rollouts
+// plus the freshest delta*N correct rollouts older than those (Sec. 5;
+// App. D.3).  The positive-prioritised mixture is an addition (see header).
+//
+// Device pipeline (one stream):
+//   [mix/retain only] pos_count -> pos_scan -> pos_compact : ascending list of
+//       positive slots (slot = FIFO position, 0 = oldest) in the workspace;
+//   draw     : one thread per draw; Philox4x64-10 block -> slot; per-draw
+//              outputs; block scan of lengths -> cu_seqlens, n_tokens;
+//   gather   : one thread per output position; coalesced copies from the
+//              token arena.
+// Everything is integer work or a bit-exact copy of stored floats.
+
+#include "rbp_internal.h"
+
+namespace {
+
+constexpr int kSlotsPerBlock = 1024;  // compaction granule
+constexpr int kCountThreads = 256;    // 4 slots per thread
+constexpr int kDrawThreads = 1024;
+
+// ---- Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11) ----------------------
+struct Block4 {
+  uint64_t x0, x1, x2, x3;
+};
+
+__device__ __forceinline__ Block4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2,
+                                                uint64_t c3, uint64_t k0, uint64_t k1) {
+  const uint64_t kMul0 = 0xD2E7470EE14C6C93ull, kMul1 = 0xCA5A826395121157ull;
+  const uint64_t kWeyl0 = 0x9E3779B97F4A7C15ull, kWeyl1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += kWeyl0;
+      k1 += kWeyl1;
+    }
+    const uint64_t hi0 = __umul64hi(kMul0, c0), lo0 = kMul0 * c0;
+    const uint64_t hi1 = __umul64hi(kMul1, c2), lo1 = kMul1 * c2;
+    const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  return {c0, c1, c2, c3};
+}
+
+__device__ __forceinline__ int64_t phys_row(int64_t slot, int64_t head, int64_t cap) {
+  int64_t r = head + slot;
+  return r >= cap ? r - cap : r;
+}
+
+// Block-wide exclusive scan of one int64 per thread (fixed order).
+template <int NT>
+__device__ int64_t block_exclusive_scan(int64_t v, int64_t* total, int64_t* lds_waves) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int64_t incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int64_t o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
+  }
+  if (lane == 63) lds_waves[wave] = incl;
+  __syncthreads();
+  int64_t wave_base = 0, sum = 0;
+  for (int w = 0; w < NT / 64; ++w) {
+    if (w < wave) wave_base += lds_waves[w];
+    sum += lds_waves[w];
+  }
+  __syncthreads();
+  *total = sum;
+  return wave_base + incl - v;
+}
+
+__global__ void __launch_bounds__(kCountThreads) pos_count_kernel(
+    const float* __restrict__ reward, int64_t head, int64_t cap, int64_t n_range,
+    int32_t* __restrict__ counts) {
+  __shared__ int64_t lds[kCountThreads / 64];
+  const int64_t s0 = (int64_t)blockIdx.x * kSlotsPerBlock + threadIdx.x * 4;
+  int64_t c = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t s = s0 + i;
+    if (s < n_range && reward[phys_row(s, head, cap)] > 0.0f) ++c;
+  }
+  int64_t total;
+  block_exclusive_scan<kCountThreads>(c, &total, lds);
+  if (threadIdx.x == 0) counts[blockIdx.x] = (int32_t)total;
+}
+
+__global__ void __launch_bounds__(1024) pos_scan_kernel(const int32_t* __restrict__ counts,
+                                                        int32_t* __restrict__ offsets,
+                                                        int64_t nb, int64_t* __restrict__ meta) {
+  __shared__ int64_t lds[1024 / 64];
+  int64_t carry = 0;
+  for (int64_t base = 0; base < nb; base += 1024) {
+    const int64_t i = base + threadIdx.x;
+    const int64_t v = i < nb ? counts[i] : 0;
+    int64_t total;
+    const int64_t ex = block_exclusive_scan<1024>(v, &total, lds);
+    if (i < nb) offsets[i] = (int32_t)(carry + ex);
+    carry += total;
+  }
+  if (threadIdx.x == 0) meta[0] = carry;
+}
+
+__global__ void __launch_bounds__(kCountThreads) pos_compact_kernel(
+    const float* __restrict__ reward, int64_t head, int64_t cap, int64_t n_range,
+    const int32_t* __restrict__ offsets, int32_t* __restrict__ pos_list) {
+  __shared__ int64_t lds[kCountThreads / 64];
+  const int64_t s0 = (int64_t)blockIdx.x * kSlotsPerBlock + threadIdx.x * 4;
+  bool f[4];
+  int64_t c = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t s = s0 + i;
+    f[i] = s < n_range && reward[phys_row(s, head, cap)] > 0.0f;
+    c += f[i];
+  }
+  int64_t total;
+  int64_t at = offsets[blockIdx.x] + block_exclusive_scan<kCountThreads>(c, &total, lds);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (f[i]) pos_list[at++] = (int32_t)(s0 + i);
+}
+
+struct DrawParams {
+  int32_t mode, layout;
+  uint64_t seed, step, p_q32;
+  int64_t n_draw, n_live, head, cap;
+  int64_t first_fresh, n_pos_keep;
+  int32_t cur_version;
+  int64_t max_tokens, token_begin, l_max;
+};
+
+__global__ void __launch_bounds__(kDrawThreads) draw_kernel(
+    DrawParams p, const int64_t* __restrict__ meta, const int32_t* __restrict__ pos_list,
+    const int32_t* __restrict__ length, const float* __restrict__ advantage,
+    const int32_t* __restrict__ version, int32_t* __restrict__ out_idx,
+    float* __restrict__ out_adv, int32_t* __restrict__ out_len, int32_t* __restrict__ out_age,
+    int32_t* __restrict__ cu_seqlens, int64_t* __restrict__ n_tokens,
+    int64_t* __restrict__ stream_total) {
+  __shared__ int64_t lds[kDrawThreads / 64];
+  const int64_t n_pos = (p.mode == RB_UNIFORM) ? 0 : meta[0];
+  // retained set: the newest `keep` positives older than the fresh part, then
+  // the fresh part [first_fresh, n_live)
+  const int64_t keep = n_pos < p.n_pos_keep ? n_pos : p.n_pos_keep;
+  const int64_t n_set = keep + (p.n_live - p.first_fresh);
+  int64_t carry = 0, valid = 0;
+  if (threadIdx.x == 0) cu_seqlens[0] = 0;
+  for (int64_t base = 0; base < p.n_draw; base += kDrawThreads) {
+    const int64_t j = base + threadIdx.x;
+    int64_t len = 0;
+    if (j < p.n_draw) {
+      const Block4 b = philox4x64_10((uint64_t)j, p.step, 0, 0, p.seed, 0);
+      int64_t slot;
+      if (p.mode == RB_UNIFORM) {
+        slot = (int64_t)__umul64hi(b.x0, (uint64_t)p.n_live);
+      } else if (p.mode == RB_POS_MIX) {
+        if (n_pos > 0 && (b.x1 >> 32) < p.p_q32)
+          slot = pos_list[__umul64hi(b.x0, (uint64_t)n_pos)];
+        else
+          slot = (int64_t)__umul64hi(b.x0, (uint64_t)p.n_live);
+      } else {
+        if (n_set <= 0) {
+          slot = 0;
+        } else {
+          const int64_t i = (int64_t)__umul64hi(b.x0, (uint64_t)n_set);
+          slot = i < keep ? pos_list[n_pos - keep + i] : p.first_fresh + (i - keep);
+        }
+      }
+      const int64_t r = phys_row(slot, p.head, p.cap);
+      len = length[r];
+      out_idx[j] = (int32_t)slot;
+      out_adv[j] = advantage[r];
+      out_len[j] = (int32_t)len;
+      out_age[j] = p.cur_version - version[r];
+    }
+    int64_t total;
+    if (p.layout == RB_LAYOUT_PACKED) {
+      const int64_t ex = block_exclusive_scan<kDrawThreads>(len, &total, lds);
+      if (j < p.n_draw) cu_seqlens[j + 1] = (int32_t)(carry + ex + len);
+      carry += total;
+    } else {
+      const int64_t v = len < p.l_max ? len : p.l_max;
+      block_exclusive_scan<kDrawThreads>(v, &total, lds);
+      if (j < p.n_draw) cu_seqlens[j + 1] = (int32_t)((j + 1) * p.l_max);
+      valid += total;
+    }
+  }
+  if (threadIdx.x == 0) {
+    if (p.layout == RB_LAYOUT_PACKED) {
+      int64_t v = carry - p.token_begin;
+      v = v < 0 ? 0 : (v > p.max_tokens ? p.max_tokens : v);
+      *n_tokens = v;
+      *stream_total = carry;
+    } else {
+      *n_tokens = valid;
+      *stream_total = valid;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) gather_packed_kernel(
+    int64_t n_draw, int64_t head, int64_t cap, int64_t token_begin, int64_t max_tokens,
+    const int64_t* __restrict__ stream_total, const int32_t* __restrict__ cu_seqlens,
+    const int32_t* __restrict__ idx, const int64_t* __restrict__ arena_off,
+    const int32_t* __restrict__ arena_tokens, const float* __restrict__ arena_old,
+    int32_t* __restrict__ tokens, float* __restrict__ old_logp, int32_t* __restrict__ seq) {
+  const int64_t total = *stream_total;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < max_tokens;
+       t += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t pos = token_begin + t;
+    if (pos < total) {
+      // largest j with cu_seqlens[j] <= pos (lengths are >= 1)
+      int64_t lo = 0, hi = n_draw;  // invariant: cu[lo] <= pos < cu[hi]
+      while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (cu_seqlens[mid] <= pos) lo = mid; else hi = mid;
+      }
+      const int64_t src = arena_off[phys_row(idx[lo], head, cap)] + (pos - cu_seqlens[lo]);
+      tokens[t] = arena_tokens[src];
+      old_logp[t] = arena_old[src];
+      seq[t] = (int32_t)lo;
+    } else {
+      tokens[t] = 0;
+      old_logp[t] = 0.0f;
+      seq[t] = -1;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) gather_padded_kernel(
+    int64_t l_max, int64_t head, int64_t cap, const int32_t* __restrict__ idx,
+    const int32_t* __restrict__ len, const int64_t* __restrict__ arena_off,
+    const int32_t* __restrict__ arena_tokens, const float* __restrict__ arena_old,
+    int32_t* __restrict__ tokens, float* __restrict__ old_logp, int32_t* __restrict__ seq) {
+  const int64_t j = blockIdx.x;
+  const int64_t n = len[j] < l_max ? len[j] : l_max;
+  const int64_t off = arena_off[phys_row(idx[j], head, cap)];
+  int32_t* tok_row = tokens + j * l_max;
+  float* old_row = old_logp + j * l_max;
+  int32_t* seq_row = seq + j * l_max;
+  for (int64_t p = (int64_t)blockIdx.y * blockDim.x + threadIdx.x; p < l_max;
+       p += (int64_t)gridDim.y * blockDim.x) {
+    if (p < n) {
+      tok_row[p] = arena_tokens[off + p];
+      old_row[p] = arena_old[off + p];
+      seq_row[p] = (int32_t)j;
+    } else {
+      tok_row[p] = 0;
+      old_row[p] = 0.0f;
+      seq_row[p] = -1;
+    }
+  }
+}
+
+}  // namespace
+
+size_t rbp::sample_gather_ws(int64_t capacity) {
+  const int64_t nb = ceil_div(capacity < 1 ? 1 : capacity, kSlotsPerBlock);
+  WsCarver c(nullptr);
+  c.take<int32_t>(nb);
+  c.take<int32_t>(nb);
+  c.take<int32_t>(capacity < 1 ? 1 : capacity);
+  c.take<int64_t>(4);
+  return align_up(c.used, 256);
+}
+
+extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
+                                const rb_batch* out, void* ws, size_t ws_bytes,
+                                void* stream) {
+  rbp::clear_error();
+  RBP_REQUIRE(rec && cfg && out, RBP_EINVAL, "rb_sample_gather: null struct pointer");
+  RBP_REQUIRE(rec->capacity >= 1 && rec->n_live >= 1 && rec->n_live <= rec->capacity,
+              RBP_EINVAL, "rb_sample_gather: need 1 <= n_live <= capacity (got %lld, %lld)",
+              (long long)rec->n_live, (long long)rec->capacity);
+  RBP_REQUIRE(rec->capacity <= INT32_MAX, RBP_EINVAL,
+              "rb_sample_gather: capacity above 2^31-1");
+  RBP_REQUIRE(rec->head >= 0 && rec->head < rec->capacity, RBP_EINVAL,
+              "rb_sample_gather: head outside [0, capacity)");
+  RBP_REQUIRE(rec->arena_off && rec->length && rec->reward && rec->advantage &&
+                  rec->version && rec->arena_tokens && rec->arena_old_logp,
+              RBP_EINVAL, "rb_sample_gather: null record array");
+  RBP_REQUIRE(cfg->mode == RB_UNIFORM || cfg->mode == RB_POS_MIX || cfg->mode == RB_POS_RETAIN,
+              RBP_EINVAL, "rb_sample_gather: unknown mode %d", cfg->mode);
+  RBP_REQUIRE(cfg->layout == RB_LAYOUT_PACKED || cfg->layout == RB_LAYOUT_PADDED, RBP_EINVAL,
+              "rb_sample_gather: unknown layout %d", cfg->layout);
+  RBP_REQUIRE(cfg->n_draw >= 1 && cfg->n_draw <= (1 << 20), RBP_EINVAL,
+              "rb_sample_gather: n_draw %lld outside [1, 2^20]", (long long)cfg->n_draw);
+  RBP_REQUIRE(cfg->p_pos_q32 <= (1ull << 32), RBP_EINVAL,
+              "rb_sample_gather: p_pos_q32 above 2^32");
+  RBP_REQUIRE(cfg->n_fresh >= 0 && cfg->n_pos_keep >= 0, RBP_EINVAL,
+              "rb_sample_gather: negative n_fresh / n_pos_keep");
+  if (cfg->layout == RB_LAYOUT_PACKED) {
+    RBP_REQUIRE(cfg->max_tokens >= 1 && cfg->token_begin >= 0, RBP_EINVAL,
+                "rb_sample_gather: packed layout needs max_tokens >= 1, token_begin >= 0");
+  } else {
+    RBP_REQUIRE(cfg->l_max >= 1 && cfg->n_draw * cfg->l_max <= INT32_MAX, RBP_EINVAL,
+                "rb_sample_gather: padded layout needs l_max >= 1 and n_draw * l_max < 2^31");
+  }
+  RBP_REQUIRE(out->idx && out->adv && out->len && out->age && out->cu_seqlens && out->tokens &&
+                  out->old_logp && out->seq_of_token && out->n_tokens,
+              RBP_EINVAL, "rb_sample_gather: null output array");
+  const size_t need = rbp::sample_gather_ws(rec->capacity);
+  RBP_REQUIRE(ws && ws_bytes >= need, RBP_EWORKSPACE,
+              "rb_sample_gather: workspace needs %zu bytes, got %zu", need, ws_bytes);
+
+  hipStream_t s = rbp::as_stream(stream);
+  const int64_t nb_cap = rbp::ceil_div(rec->capacity, kSlotsPerBlock);
+  rbp::WsCarver c(ws);
+  int32_t* counts = c.take<int32_t>(nb_cap);
+  int32_t* offsets = c.take<int32_t>(nb_cap);
+  int32_t* pos_list = c.take<int32_t>(rec->capacity);
+  int64_t* meta = c.take<int64_t>(4);
+
+  DrawParams p{};
+  p.mode = cfg->mode;
+  p.layout = cfg->layout;
+  p.seed = cfg->seed;
+  p.step = cfg->step;
+  p.p_q32 = cfg->p_pos_q32;
+  p.n_draw = cfg->n_draw;
+  p.n_live = rec->n_live;
+  p.head = rec->head;
+  p.cap = rec->capacity;
+  p.first_fresh = rec->n_live - cfg->n_fresh;
+  if (p.first_fresh < 0) p.first_fresh = 0;
+  p.n_pos_keep = cfg->n_pos_keep;
+  p.cur_version = cfg->cur_version;
+  p.max_tokens = cfg->max_tokens;
+  p.token_begin = cfg->token_begin;
+  p.l_max = cfg->l_max;
+
+  if (cfg->mode != RB_UNIFORM) {
+    // positives over all live slots (mixture) or over the non-fresh ones (retention)
+    const int64_t n_range = cfg->mode == RB_POS_MIX ? rec->n_live : p.first_fresh;
+    const int64_t nb = rbp::ceil_div(n_range > 0 ? n_range : 1, kSlotsPerBlock);
+    hipLaunchKernelGGL(pos_count_kernel, dim3(nb), dim3(kCountThreads), 0, s, rec->reward,
+                       rec->head, rec->capacity, n_range, counts);
+    hipLaunchKernelGGL(pos_scan_kernel, dim3(1), dim3(1024), 0, s, counts, offsets, nb, meta);
+    hipLaunchKernelGGL(pos_compact_kernel, dim3(nb), dim3(kCountThreads), 0, s, rec->reward,
+                       rec->head, rec->capacity, n_range, offsets, pos_list);
+  }
+  hipLaunchKernelGGL(draw_kernel, dim3(1), dim3(kDrawThreads), 0, s, p, meta, pos_list,
+                     rec->length, rec->advantage, rec->version, out->idx, out->adv, out->len,
+                     out->age, out->cu_seqlens, out->n_tokens, meta + 1);
+  if (cfg->layout == RB_LAYOUT_PACKED) {
+    int64_t blocks = rbp::ceil_div(cfg->max_tokens, 256);
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(gather_packed_kernel, dim3(blocks), dim3(256), 0, s, cfg->n_draw,
+                       rec->head, rec->capacity, cfg->token_begin, cfg->max_tokens, meta + 1,
+                       out->cu_seqlens, out->idx, rec->arena_off, rec->arena_tokens,
+                       rec->arena_old_logp, out->tokens, out->old_logp, out->seq_of_token);
+  } else {
+    int64_t by = rbp::ceil_div(cfg->l_max, 256);
+    if (by > 64) by = 64;
+    hipLaunchKernelGGL(gather_padded_kernel, dim3(cfg->n_draw, by), dim3(256), 0, s, cfg->l_max,
+                       rec->head, rec->capacity, out->idx, out->len, rec->arena_off,
+                       rec->arena_tokens, rec->arena_old_logp, out->tokens, out->old_logp,
+                       out->seq_of_token);
+  }
+  RBP_CHECK_LAUNCH("rb_sample_gather");
+  return RBP_OK;
+}

@@ -1,0 +1,187 @@
+"""GPU parity of policy_logprob_fwd / policy_logprob_bwd against the oracle.
+
+Tolerances: log-probabilities within 2e-3 absolute; dhidden and dW within 1e-2
+relative L2, also restricted to the non-target rows of dW and on peaked logits
+(so that errors in the softmax part cannot hide behind the one-hot term)."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.grad import dW_from_rows, dhidden_rows, dz_rows, logprob_backward
+from oracle.logprob import logprob, logprob_rows
+from paper_2604_08706_amd import workloads as wlm
+
+from gpu_util import bf16_to_f64, rel_l2, require_gpu, to_np
+
+pytestmark = pytest.mark.gpu
+
+LOGP_ATOL = 2e-3
+GRAD_RTOL = 1e-2
+
+
+def _mask(T, seed, frac=0.1):
+    rng = np.random.default_rng(seed)
+    seq = np.zeros(T, dtype=np.int32)
+    seq[rng.random(T) < frac] = -1
+    return seq
+
+
+def _fwd(rbp, hidden, W, tokens, seq):
+    T, d = hidden.shape
+    V = W.shape[0]
+    logp = torch.empty(T, device="cuda")
+    lse = torch.empty(T, device="cuda")
+    ws = rbp.workspace(rbp.RBP_OP_LOGPROB_FWD, T, d, V)
+    rbp.policy_logprob_fwd(hidden, W, tokens, seq, logp, lse, ws)
+    torch.cuda.synchronize()
+    return logp, lse
+
+
+def _bwd(rbp, hidden, W, tokens, seq, lse, dlogp, ws_tokens=None, dW0=None):
+    T, d = hidden.shape
+    V = W.shape[0]
+    dh = torch.empty((T, d), device="cuda")
+    dW = torch.empty((V, d), device="cuda") if dW0 is None else dW0.clone()
+    ws = rbp.workspace(rbp.RBP_OP_LOGPROB_BWD, T if ws_tokens is None else ws_tokens, d, V)
+    rbp.policy_logprob_bwd(hidden, W, tokens, seq, lse, dlogp, dh, dW, ws,
+                           accumulate_dW=dW0 is not None)
+    torch.cuda.synchronize()
+    return dh, dW
+
+
+def _check_grads(dh, dW, want_dh, want_dW, tokens, seq):
+    assert rel_l2(dh, want_dh) < GRAD_RTOL
+    assert rel_l2(dW, want_dW) < GRAD_RTOL
+    target = np.zeros(want_dW.shape[0], dtype=bool)
+    target[np.asarray(tokens)[np.asarray(seq) >= 0]] = True
+    if (~target).any():
+        assert rel_l2(dW[~target], want_dW[~target]) < GRAD_RTOL
+    assert np.all(dh[np.asarray(seq) < 0] == 0)
+
+
+SHAPES = [  # T, d, V -- tile tails in every dimension
+    (1, 8, 1), (37, 8, 300), (256, 64, 1024), (300, 72, 1000), (513, 136, 2049),
+    (257, 64, 256), (1000, 264, 4097),
+]
+
+
+@pytest.mark.parametrize("T,d,V", SHAPES)
+@pytest.mark.parametrize("w_sd", [0.02, 1.0])
+def test_small_shapes_fwd_bwd(T, d, V, w_sd):
+    rbp = require_gpu()
+    print(f"[logprob] T={T} d={d} V={V} w_sd={w_sd}", flush=True)
+    hidden, W, tokens = wlm.head(T, d, V, seed=T + d + V, w_sd=w_sd)
+    seq = _mask(T, T)
+    h64, W64, y = bf16_to_f64(hidden), bf16_to_f64(W), to_np(tokens)
+    want_logp, want_lse = logprob(h64, W64, y, seq)
+    hc, Wc, tc, sc = hidden.cuda(), W.cuda(), tokens.cuda(), torch.from_numpy(seq).cuda()
+    logp, lse = _fwd(rbp, hc, Wc, tc, sc)
+    assert np.abs(to_np(logp) - want_logp).max() < LOGP_ATOL
+    assert np.abs(to_np(lse) - want_lse).max() < LOGP_ATOL
+    dlogp = wlm.normal(T, 1.0, T + 1).numpy()
+    dlogp[seq < 0] = 0.0
+    want_dh, want_dW = logprob_backward(h64, W64, y, want_lse, dlogp, seq)
+    dh, dW = _bwd(rbp, hc, Wc, tc, sc, lse, torch.from_numpy(dlogp).cuda())
+    _check_grads(to_np(dh), to_np(dW), want_dh, want_dW, y, seq)
+
+
+@pytest.mark.parametrize("name,T", [("head05b", 700), ("head15b", 300)])
+def test_real_vocab_full_oracle(name, T):
+    """Real vocabulary (151936 = 593.5 tiles: a V tail), several token tiles."""
+    rbp = require_gpu()
+    wl = wlm.WORKLOADS[name]
+    print(f"[logprob] {name} T={T}", flush=True)
+    hidden, W, tokens = wlm.head(T, wl.d, wl.V, seed=11, device="cuda")
+    seq = _mask(T, 5)
+    sc = torch.from_numpy(seq).cuda()
+    h64, W64, y = bf16_to_f64(hidden), bf16_to_f64(W), to_np(tokens)
+    want_logp, want_lse = logprob(h64, W64, y, seq)
+    logp, lse = _fwd(rbp, hidden, W, tokens, sc)
+    assert np.abs(to_np(logp) - want_logp).max() < LOGP_ATOL
+    dlogp = wlm.normal(T, 1e-3, 6).numpy()
+    dlogp[seq < 0] = 0.0
+    want_dh, want_dW = logprob_backward(h64, W64, y, want_lse, dlogp, seq)
+    dh, dW = _bwd(rbp, hidden, W, tokens, sc, lse, torch.from_numpy(dlogp).cuda())
+    _check_grads(to_np(dh), to_np(dW), want_dh, want_dW, y, seq)
+    # several token chunks (workspace for 256 tokens) with dW accumulation
+    dW0 = wlm.normal((wl.V, wl.d), 1e-4, 7, device="cuda")
+    dh2, dW2 = _bwd(rbp, hidden, W, tokens, sc, lse, torch.from_numpy(dlogp).cuda(),
+                    ws_tokens=256, dW0=dW0)
+    _check_grads(to_np(dh2), to_np(dW2), want_dh, want_dW + to_np(dW0).astype(np.float64), y,
+                 seq)
+
+
+def test_head7b_full_size_sampled_rows():
+    """The benchmark's launch configuration (T = 16384, d = 3584, V = 152064,
+    one backward chunk) checked on sampled rows the oracle computes one by one."""
+    rbp = require_gpu()
+    wl = wlm.WORKLOADS["head7b"]
+    T = 16384
+    print("[logprob] head7b full size", flush=True)
+    hidden, W, tokens = wlm.head(T, wl.d, wl.V, seed=0, device="cuda")
+    logp, lse = _fwd(rbp, hidden, W, tokens, None)
+    rng = np.random.default_rng(0)
+    rows = np.sort(rng.choice(T, 24, replace=False))
+    rows = np.concatenate([[0, 255, 256, T - 1], rows])
+    h64 = hidden[torch.from_numpy(rows).cuda()].cpu().to(torch.float64).numpy()
+    W64 = bf16_to_f64(W)
+    y = to_np(tokens)[rows]
+    want_logp, want_lse = logprob_rows(h64, W64, y, range(len(rows)))
+    assert np.abs(to_np(logp)[rows] - want_logp).max() < LOGP_ATOL
+    assert np.abs(to_np(lse)[rows] - want_lse).max() < LOGP_ATOL
+    # backward with the upstream gradient nonzero on the sampled rows only:
+    # dW is then exactly the sum over those rows
+    dlogp = np.zeros(T, dtype=np.float32)
+    dlogp[rows] = wlm.normal(len(rows), 1e-3, 1).numpy()
+    lse_in = np.zeros(T, dtype=np.float32)
+    lse_in[rows] = want_lse.astype(np.float32)
+    dh, dW = _bwd(rbp, hidden, W, tokens, None, torch.from_numpy(lse_in).cuda(),
+                  torch.from_numpy(dlogp).cuda())
+    dh_np = to_np(dh)
+    others = np.ones(T, dtype=bool)
+    others[rows] = False
+    assert np.all(dh_np[others] == 0)
+    dz = dz_rows(h64, W64, y, want_lse, dlogp[rows], range(len(rows)))
+    want_dh = dhidden_rows(h64, W64, y, want_lse, dlogp[rows], range(len(rows)), dz=dz)
+    assert rel_l2(dh_np[rows], want_dh) < GRAD_RTOL
+    num = den = num_nt = den_nt = 0.0
+    target = set(y.tolist())
+    for v0 in range(0, wl.V, 16384):
+        v1 = min(v0 + 16384, wl.V)
+        want = dW_from_rows(h64, W64, y, want_lse, dlogp[rows], range(len(rows)), v0, v1,
+                            dz=dz)
+        got = dW[v0:v1].cpu().numpy().astype(np.float64)
+        num += ((got - want) ** 2).sum()
+        den += (want ** 2).sum()
+        nt = np.array([v not in target for v in range(v0, v1)])
+        num_nt += ((got[nt] - want[nt]) ** 2).sum()
+        den_nt += (want[nt] ** 2).sum()
+    assert np.sqrt(num / den) < GRAD_RTOL
+    assert np.sqrt(num_nt / den_nt) < GRAD_RTOL
+    del hidden, W, dW
+    torch.cuda.empty_cache()
+
+
+def test_bitwise_reproducible_and_bad_args():
+    rbp = require_gpu()
+    T, d, V = 600, 128, 3000
+    hidden, W, tokens = wlm.head(T, d, V, seed=3, device="cuda")
+    a = _fwd(rbp, hidden, W, tokens, None)
+    b = _fwd(rbp, hidden, W, tokens, None)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    dlogp = wlm.normal(T, 1.0, 2, device="cuda")
+    g1 = _bwd(rbp, hidden, W, tokens, None, a[1], dlogp)
+    g2 = _bwd(rbp, hidden, W, tokens, None, a[1], dlogp)
+    assert torch.equal(g1[0], g2[0]) and torch.equal(g1[1], g2[1])
+    h12 = torch.zeros((4, 12), dtype=torch.bfloat16, device="cuda")
+    W12 = torch.zeros((5, 12), dtype=torch.bfloat16, device="cuda")
+    t4 = torch.zeros(4, dtype=torch.int32, device="cuda")
+    with pytest.raises(rbp.RbpError) as e:
+        _fwd(rbp, h12, W12, t4, None)
+    assert e.value.status == rbp.RBP_EUNSUPPORTED
+    with pytest.raises(rbp.RbpError) as e:
+        rbp.policy_logprob_fwd(hidden, W, tokens, None, torch.empty(T, device="cuda"),
+                               torch.empty(T, device="cuda"),
+                               torch.empty(16, dtype=torch.uint8, device="cuda"))
+    assert e.value.status == rbp.RBP_EWORKSPACE

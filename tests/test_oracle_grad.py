@@ -3,7 +3,7 @@
 import numpy as np
 import pytest
 
-from oracle.grad import dW_from_rows, dhidden_rows, logprob_backward
+from oracle.grad import dW_from_rows, dhidden_rows, dz_rows, logprob_backward
 from oracle.logprob import logprob
 from oracle.loss import grpo_loss
 
@@ -106,4 +106,8 @@ def test_row_helpers_match_full_backward():
     assert np.allclose(dhidden_rows(h, W, y, lse, dlogp, rows), dh[rows], atol=1e-13)
     assert np.allclose(dW_from_rows(h, W, y, lse, dlogp, rows), dW, atol=1e-13)
     assert np.allclose(dW_from_rows(h, W, y, lse, dlogp, rows, 10, 30), dW[10:30],
+                       atol=1e-13)
+    dz = dz_rows(h, W, y, lse, dlogp, rows)
+    assert np.allclose(dz.sum(axis=1), 0.0, atol=1e-14)
+    assert np.allclose(dW_from_rows(h, W, y, lse, dlogp, rows, 5, 9, dz=dz), dW[5:9],
                        atol=1e-13)
