@@ -171,8 +171,12 @@ def rb_group_advantage(reward, group_off, adv, ddof=1, eps=1e-6, stream=None):
 
 def make_records(n_live, capacity, head, arena_off, length, reward, advantage, version,
                  arena_tokens, arena_old_logp):
-    """Build the host-side rb_records struct from device tensors."""
+    """Build the host-side rb_records struct from device tensors.
+
+    The struct keeps references to the tensors, so their memory stays
+    allocated for as long as the struct is alive."""
     rec = RbRecords()
+    rec._keep = (arena_off, length, reward, advantage, version, arena_tokens, arena_old_logp)
     rec.n_live, rec.capacity, rec.head = int(n_live), int(capacity), int(head)
     rec.arena_off = _dev(arena_off, torch.int64, "arena_off", capacity).value
     rec.length = _dev(length, torch.int32, "length", capacity).value

@@ -24,6 +24,7 @@
 #include <cmath>
 
 #include "gemm_core.h"
+#include "gemm_dma.h"
 #include "rbp_internal.h"
 
 namespace {
@@ -33,6 +34,7 @@ using rbp::gemm::acc_n;
 using rbp::gemm::f32x16;
 using rbp::gemm::kLdsBytes;
 using rbp::gemm::mainloop;
+using rbp::gemm::mainloop_dma;
 using rbp::gemm::map_tile;
 using rbp::gemm::Operand;
 
@@ -42,6 +44,13 @@ constexpr int kGroupGrad = 4;
 
 #define RBP_GEMM_KERNEL \
   __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+
+// Logit products (K-major operands, direct HBM -> LDS loads): 8 waves, two per
+// SIMD, so that enough waves keep loads in flight to feed 256 x 256 tiles.
+using GL = rbp::gemm::Grid8;
+#define RBP_LOGITS_KERNEL                                                        \
+  __global__ __attribute__((amdgpu_flat_work_group_size(GL::kThreads, GL::kThreads), \
+                            amdgpu_waves_per_eu(GL::kWaves / 4, GL::kWaves / 4)))
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float((uint32_t)b << 16);
@@ -53,53 +62,59 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // Forward tile: partial (max, sum exp) of each token column over 256 vocab rows.
-RBP_GEMM_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
-                                               const uint16_t* __restrict__ H, int64_t T,
-                                               int32_t d, int32_t V, int64_t tiles_m,
-                                               int64_t tiles_n, float2* __restrict__ part,
-                                               int64_t ld_part) {
+RBP_LOGITS_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
+                                                 const uint16_t* __restrict__ H, int64_t T,
+                                                 int32_t d, int32_t V, int64_t tiles_m,
+                                                 int64_t tiles_n, float2* __restrict__ part,
+                                                 int64_t ld_part) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   int64_t tm, tn;
   map_tile(blockIdx.x, tiles_m, tiles_n, kGroupLogits, tm, tn);
   const int64_t m0 = tm * 256, n0 = tn * 256;
   const Operand A{W, d, V, d};
   const Operand B{H, d, T, d};
-  f32x16 acc[4][4];
-  mainloop<true, true>(A, B, m0, n0, 0, d, smem, acc);
+  f32x16 acc[GL::MI][GL::NI];
+  mainloop_dma<GL>(A, B, m0, n0, 0, d, smem, acc);
 
   float2* lds_ms = reinterpret_cast<float2*>(smem);  // [wm][256 columns]
-  const int lane = threadIdx.x & 63, wm = (threadIdx.x >> 6) >> 1;
+  const int lane = threadIdx.x & 63;
   const int64_t vlim = (int64_t)V - m0;
 #pragma unroll
-  for (int ni = 0; ni < 4; ++ni) {
+  for (int ni = 0; ni < GL::NI; ++ni) {
     float mx = -INFINITY;
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < GL::MI; ++mi)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        if (acc_m(mi, r) < vlim) mx = fmaxf(mx, acc[mi][ni][r]);
+        if (GL::row(mi, r) < vlim) mx = fmaxf(mx, acc[mi][ni][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    float s = 0.0f;
+    float sum = 0.0f;
     if (mx != -INFINITY) {
       const float mb = mx * kLog2e;
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
+      for (int mi = 0; mi < GL::MI; ++mi)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          if (acc_m(mi, r) < vlim) s += exp2f(fmaf(acc[mi][ni][r], kLog2e, -mb));
+          if (GL::row(mi, r) < vlim) sum += exp2f(fmaf(acc[mi][ni][r], kLog2e, -mb));
     }
-    s += __shfl_xor(s, 32, 64);
-    if (lane < 32) lds_ms[wm * 256 + acc_n(ni)] = make_float2(mx, s);
+    sum += __shfl_xor(sum, 32, 64);
+    if (lane < 32) lds_ms[GL::wm() * 256 + GL::col(ni)] = make_float2(mx, sum);
   }
   __syncthreads();
-  const int col = threadIdx.x;
-  const float2 a = lds_ms[col], b = lds_ms[256 + col];
-  const float M = fmaxf(a.x, b.x);
-  float S = 0.0f;
-  if (a.x != -INFINITY) S += a.y * exp2f((a.x - M) * kLog2e);
-  if (b.x != -INFINITY) S += b.y * exp2f((b.x - M) * kLog2e);
-  const int64_t t = n0 + col;
-  if (t < T) part[t * ld_part + tm] = make_float2(M, S);
+  if (threadIdx.x < 256) {
+    const int col = threadIdx.x;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < GL::WM; ++w) M = fmaxf(M, lds_ms[w * 256 + col].x);
+    float S = 0.0f;
+#pragma unroll
+    for (int w = 0; w < GL::WM; ++w) {
+      const float2 q = lds_ms[w * 256 + col];
+      if (q.x != -INFINITY) S += q.y * exp2f((q.x - M) * kLog2e);
+    }
+    const int64_t t = n0 + col;
+    if (t < T) part[t * ld_part + tm] = make_float2(M, S);
+  }
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -163,27 +178,27 @@ __global__ void __launch_bounds__(256) lse_merge_kernel(
 }
 
 // Backward step 1: recompute the tile, write dz = dlogp (onehot - p) as bf16.
-RBP_GEMM_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
-                                        const uint16_t* __restrict__ Hc, int64_t Tn, int32_t d,
-                                        int32_t V, const int32_t* __restrict__ tokens,
-                                        const int32_t* __restrict__ seq,
-                                        const float* __restrict__ lse,
-                                        const float* __restrict__ dlogp,
-                                        uint16_t* __restrict__ G, int64_t ldG, int64_t tiles_m,
-                                        int64_t tiles_n) {
+RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
+                                          const uint16_t* __restrict__ Hc, int64_t Tn,
+                                          int32_t d, int32_t V, const int32_t* __restrict__ tokens,
+                                          const int32_t* __restrict__ seq,
+                                          const float* __restrict__ lse,
+                                          const float* __restrict__ dlogp,
+                                          uint16_t* __restrict__ G, int64_t ldG, int64_t tiles_m,
+                                          int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   int64_t tm, tn;
   map_tile(blockIdx.x, tiles_m, tiles_n, kGroupLogits, tm, tn);
   const int64_t m0 = tm * 256, n0 = tn * 256;
   const Operand A{W, d, V, d};
   const Operand B{Hc, d, Tn, d};
-  f32x16 acc[4][4];
-  mainloop<true, true>(A, B, m0, n0, 0, d, smem, acc);
+  f32x16 acc[GL::MI][GL::NI];
+  mainloop_dma<GL>(A, B, m0, n0, 0, d, smem, acc);
 
   const int64_t vlim = (int64_t)V - m0;
 #pragma unroll
-  for (int ni = 0; ni < 4; ++ni) {
-    const int64_t t = n0 + acc_n(ni);
+  for (int ni = 0; ni < GL::NI; ++ni) {
+    const int64_t t = n0 + GL::col(ni);
     float ls = 0.0f, dl = 0.0f;
     int64_t y = -1;
     if (t < Tn && (seq == nullptr || seq[t] >= 0)) {
@@ -194,13 +209,13 @@ RBP_GEMM_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
     const float lsb = ls * kLog2e;
     uint16_t* grow = G + t * ldG + m0;
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < GL::MI; ++mi)
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
         float g[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int v = acc_m(mi, rg * 4 + i);
+          const int v = GL::row(mi, rg * 4 + i);
           const float p = exp2f(fmaf(acc[mi][ni][rg * 4 + i], kLog2e, -lsb));
           const float oh = (v == y) ? 1.0f : 0.0f;
           g[i] = (v < vlim) ? dl * (oh - p) : 0.0f;
@@ -208,7 +223,7 @@ RBP_GEMM_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
         uint2 pk;
         pk.x = pack_bf16x2(g[0], g[1]);
         pk.y = pack_bf16x2(g[2], g[3]);
-        *reinterpret_cast<uint2*>(grow + acc_m(mi, rg * 4)) = pk;
+        *reinterpret_cast<uint2*>(grow + GL::row(mi, rg * 4)) = pk;
       }
   }
 }
@@ -319,7 +334,7 @@ extern "C" int policy_logprob_fwd(const uint16_t* hidden, const uint16_t* W,
   hipStream_t s = rbp::as_stream(stream);
   const int64_t tiles_m = rbp::ceil_div(V, 256), tiles_n = rbp::ceil_div(T, 256);
   float2* part = static_cast<float2*>(ws);
-  hipLaunchKernelGGL(logits_lse_partial_kernel, dim3(tiles_m * tiles_n), dim3(256), 0, s, W,
+  hipLaunchKernelGGL(logits_lse_partial_kernel, dim3(tiles_m * tiles_n), dim3(GL::kThreads), 0, s, W,
                      hidden, T, d, V, tiles_m, tiles_n, part, tiles_m);
   hipLaunchKernelGGL(lse_merge_kernel, dim3(rbp::ceil_div(T, 4)), dim3(256), 0, s, part, tiles_m,
                      tiles_m, hidden, W, tokens, seq_of_token, T, d, V, logp, lse);
@@ -363,7 +378,7 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
     const int64_t Tn = (T - t0) < Tc ? (T - t0) : Tc;
     const int64_t tiles_t = rbp::ceil_div(Tn, 256);
     const uint16_t* Hc = hidden + t0 * d;
-    hipLaunchKernelGGL(grad_logits_kernel, dim3(tiles_v * tiles_t), dim3(256), 0, s, W, Hc, Tn,
+    hipLaunchKernelGGL(grad_logits_kernel, dim3(tiles_v * tiles_t), dim3(GL::kThreads), 0, s, W, Hc, Tn,
                        d, V, tokens + t0, seq_of_token ? seq_of_token + t0 : nullptr, lse + t0,
                        dlogp + t0, G, Vp, tiles_v, tiles_t);
     hipLaunchKernelGGL(dhidden_kernel, dim3(tiles_d * tiles_t), dim3(256), 0, s, W, G, Tn, d, V,
