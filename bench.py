@@ -37,7 +37,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="head7b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=256,
+    ap.add_argument("--cpu-tokens", type=int, default=128,
                     help="tokens of the bounded sample the CPU oracle is timed on")
     return ap.parse_args()
 
@@ -161,7 +161,16 @@ def cpu_baseline(wl, n_tokens, seed=0):
     loss, dlogp, _ = grpo_loss(logp, logp + 0.1, seq, g["adv"], g["len"], wl.n_draw)
     logprob_backward(h64, W64, y, lse, dlogp, seq)
     dt = time.perf_counter() - t0
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = os.cpu_count() or 1
+    try:
+        import threadpoolctl
+
+        blas = [p["num_threads"] for p in threadpoolctl.threadpool_info()
+                if p.get("user_api") == "blas"]
+        if blas:
+            threads = max(blas)
+    except ImportError:
+        pass
     return {"value": n_tokens / dt, "unit": "replayed tokens/s", "cores": threads,
             "kind": "oracle",
             "sample": f"{n_tokens} tokens of one {wl.max_tokens}-token micro-batch at "

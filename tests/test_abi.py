@@ -1,0 +1,113 @@
+"""The C ABI: the library loads without a GPU, exports every function the
+header declares, and rejects invalid arguments on the host (no launch)."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "rbpolicy.h")
+
+
+def _lib_path():
+    from paper_2604_08706_amd import _binding
+
+    if not os.path.exists(_binding.LIB_PATH):
+        from paper_2604_08706_amd import build
+
+        build.build(verbose=False)
+    return _binding.LIB_PATH
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[\w]+\s*\**\s*(\w+)\s*\([^;]*\)\s*;", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for n in ("rb_sample_gather", "rb_group_advantage", "policy_logprob_fwd",
+              "policy_loss_fwd_bwd", "policy_logprob_bwd", "rbp_workspace_bytes",
+              "rbp_status_string", "rbp_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    path = _lib_path()
+    out = subprocess.run(["nm", "-D", "--defined-only", path], capture_output=True, text=True,
+                         check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    missing = [n for n in _declared_functions() if n not in exported]
+    assert not missing, missing
+    lib = ctypes.CDLL(path)
+    for n in _declared_functions():
+        assert getattr(lib, n) is not None
+
+
+def test_binding_names_match_header():
+    from paper_2604_08706_amd import _binding
+
+    assert sorted(_binding.EXPORTED) == _declared_functions()
+
+
+def test_status_strings_and_workspace_sizes():
+    from paper_2604_08706_amd import _binding as b
+
+    lib = b.load_library(_lib_path())
+    assert lib.rbp_status_string(0) == b"ok"
+    assert lib.rbp_status_string(-3) == b"workspace too small"
+    assert lib.rbp_status_string(12345) == b"unknown status"
+    assert lib.rbp_workspace_bytes(99, 10, 8, 8) == 0
+    # backward workspace: one bf16 [Tc, V rounded to 256] chunk
+    assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_BWD, 16384, 3584, 152064) == \
+        16384 * 152064 * 2
+    assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_BWD, 1, 64, 1000) == 256 * 1024 * 2
+    # forward workspace: one (max, sum) pair per token and 256-wide vocab tile
+    assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_FWD, 100, 64, 513) == \
+        ((100 * 3 * 8 + 255) // 256) * 256
+    assert lib.rbp_workspace_bytes(b.RBP_OP_LOSS, 10, 0, 0) > 0
+    assert lib.rbp_workspace_bytes(b.RBP_OP_SAMPLE_GATHER, 1_000_000, 0, 0) >= 4_000_000
+
+
+def test_invalid_arguments_fail_on_the_host():
+    from paper_2604_08706_amd import _binding as b
+
+    lib = b.load_library(_lib_path())
+    null = ctypes.c_void_p(0)
+    assert lib.rb_sample_gather(None, None, None, null, 0, null) == b.RBP_EINVAL
+    assert b"null" in lib.rbp_last_error()
+    rec = b.RbRecords()
+    rec.n_live, rec.capacity, rec.head = 5, 4, 0  # n_live > capacity
+    cfg = b.RbSampleCfg()
+    out = b.RbBatch()
+    assert lib.rb_sample_gather(ctypes.byref(rec), ctypes.byref(cfg), ctypes.byref(out), null, 0,
+                                null) == b.RBP_EINVAL
+    assert lib.policy_logprob_fwd(null, null, null, null, -1, 64, 10, null, null, null, 0,
+                                  null) == b.RBP_EINVAL
+    assert lib.policy_logprob_fwd(null, null, null, null, 4, 12, 10, null, null, null, 0,
+                                  null) == b.RBP_EUNSUPPORTED
+    assert lib.policy_logprob_bwd(null, null, null, null, null, null, 4, 12, 10, null, null, 0,
+                                  null, 0, null) == b.RBP_EUNSUPPORTED
+    assert lib.policy_loss_fwd_bwd(null, null, null, null, null, 4, 0, 1, 0.2, 0.2, null, null,
+                                   null, null, 0, null) == b.RBP_EINVAL
+    assert lib.rb_group_advantage(null, null, 3, 1, 1e-6, null, null) == b.RBP_EINVAL
+    assert lib.rb_group_advantage(ctypes.c_void_p(8), ctypes.c_void_p(8), 3, 2, 1e-6,
+                                  ctypes.c_void_p(8), null) == b.RBP_EINVAL
+    lib.rbp_status_string(0)
+    # a successful call clears the thread's error text
+    assert lib.rb_group_advantage(ctypes.c_void_p(8), ctypes.c_void_p(8), 0, 1, 1e-6,
+                                  ctypes.c_void_p(8), null) == b.RBP_OK
+    assert lib.rbp_last_error() == b""
+
+
+def test_product_path_fails_loudly_without_the_library(tmp_path):
+    from paper_2604_08706_amd import _binding as b
+
+    with pytest.raises(ImportError):
+        b.load_library(str(tmp_path / "missing.so"))
