@@ -1,25 +1,25 @@
-// bf16 MFMA mainloop for two K-major operands with HBM -> LDS direct loads
-// (gfx950 buffer_load_dwordx4 ... lds), used where both operands are stored
-// with k contiguous.  Same workgroup tile, wave grid, MFMA and accumulator
-// layout as gemm_core.h, so the epilogues work on either mainloop.
+// The K loop of every bf16 product: operands streamed HBM -> LDS with direct
+// loads (gfx950 buffer_load_dwordx4 ... lds), K step 64, two LDS stages.
 //
-// K step 32, four LDS stages of 32 KiB (A then B, each [256 rows][32 k] bf16 =
-// 64-byte rows).  The loads of step s + 3 are issued two iterations before
-// step s + 3 is multiplied, straight into LDS: no staging registers, no
-// ds_write instructions, and ~2000 MFMA cycles of latency cover.
-//
-// The loads are issued with inline assembly and their completion is tracked by
-// hand (s_waitcnt vmcnt): the compiler's own tracking of LDS-DMA would wait for
-// every outstanding load before each LDS read and serialize the pipeline.
-// Nothing else in these kernels touches M0 or issues vector memory loads inside
-// the loop, and the loop ends with vmcnt(0).
-//
-// A DMA instruction writes 64 lanes x 16 bytes to LDS at M0 + 16 * lane, i.e.
-// 16 consecutive 64-byte rows.  The bank swizzle is applied on the HBM side:
-// the lane that lands on physical chunk p of row `row` fetches logical chunk
-// p ^ f(row) with f(row) = ((row >> 1) ^ (row >> 2)) & 3, which makes every
-// fragment read (32 consecutive rows, one chunk) hit distinct banks whether the
-// LDS serves 8 or 16 lanes of a 16-byte read per cycle.
+// * Direct loads need no staging registers and no ds_write instructions.  A
+//   load instruction writes 64 lanes x 16 bytes to LDS at M0 + 16 * lane, i.e.
+//   8 consecutive 128-byte rows; the bank swizzle (gemm_core.h) is applied on
+//   the HBM side -- the lane that lands on physical chunk p of row `row`
+//   fetches logical chunk p ^ swz(row).
+// * 128-byte rows make every row segment a whole cache line: measured L2 ->
+//   CU rate ~28 TB/s for 128-byte segments against ~16 TB/s for 64-byte ones.
+// * The loads of step s + 1 are issued right after the barrier that frees
+//   their stage -- one full step ahead -- half during the last K slice of one
+//   step and half during the first slice of the next, spread between MFMAs so
+//   the wave's MFMA issue never waits behind a burst of loads.
+// * Fragments are read one K slice (16) ahead of the MFMAs that use them; the
+//   first slice of step s + 1 is read right after the barrier, while the last
+//   slice of step s (already in registers) multiplies.
+// * The loads are issued with inline assembly and their completion is tracked
+//   by hand (s_waitcnt vmcnt): the compiler's own tracking of LDS-DMA waits for
+//   every outstanding load before each LDS read and would serialize the
+//   pipeline.  Nothing else in these kernels touches M0 or issues vector memory
+//   loads inside the loop, and the loop ends with vmcnt(0).
 #pragma once
 
 #include "gemm_core.h"
@@ -27,12 +27,9 @@
 namespace rbp {
 namespace gemm {
 
-constexpr int kDmaBK = 32;
-constexpr int kDmaStages = 4;
-constexpr int kDmaTile = 256 * kDmaBK * 2;   // 16 KiB
-constexpr int kDmaStage = 2 * kDmaTile;      // A + B
-constexpr int kDmaLds = kDmaStages * kDmaStage;
-static_assert(kDmaLds <= kLdsBytes, "DMA stages must fit the shared LDS allocation");
+constexpr int kBK = 64;
+constexpr int kStageBytes = 2 * kTileBytes;  // A + B
+static_assert(2 * kStageBytes <= kLdsBytes, "two stages must fit the LDS allocation");
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
@@ -68,102 +65,6 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Wave grid of a DMA workgroup: WM x WN waves over the 256 x 256 tile, each
-// wave owning (256 / WM) x (256 / WN) outputs = MI x NI MFMA tiles of 32 x 32.
-template <int WM_, int WN_>
-struct Grid {
-  static constexpr int WM = WM_, WN = WN_;
-  static constexpr int kWaves = WM * WN;
-  static constexpr int kThreads = 64 * kWaves;
-  static constexpr int MI = 256 / 32 / WM;
-  static constexpr int NI = 256 / 32 / WN;
-  static constexpr int kLoadsPerOperand = 16 / kWaves;  // 1 KiB blocks per wave per step
-  static __device__ __forceinline__ int wave() { return threadIdx.x >> 6; }
-  static __device__ __forceinline__ int wm() { return wave() / WN; }
-  static __device__ __forceinline__ int wn() { return wave() % WN; }
-  // row (m) / column (n) of accumulator r of MFMA tile (mi, ni), tile-relative
-  static __device__ __forceinline__ int row(int mi, int r) {
-    return wm() * (256 / WM) + mi * 32 + (r >> 2) * 8 + ((threadIdx.x & 63) >> 5) * 4 + (r & 3);
-  }
-  static __device__ __forceinline__ int col(int ni) {
-    return wn() * (256 / WN) + ni * 32 + (threadIdx.x & 31);
-  }
-};
-using Grid4 = Grid<2, 2>;  // 4 waves, 128 x 128 per wave
-using Grid8 = Grid<2, 4>;  // 8 waves (two per SIMD), 128 x 64 per wave
-
-// Per-thread load plan of one K-major operand tile (256 rows x 32 k).
-template <class G>
-struct DmaOperand {
-  i32x4 rsrc;
-  uint32_t voff0;      // byte offset of this lane's chunk for j = 0 at k = 0
-  uint32_t row_step;   // bytes between the row blocks of j and j + 1
-  int kc;              // first k of this lane's chunk within the step
-  int64_t k_extent;
-
-  __device__ __forceinline__ void init(const Operand& op, int64_t mn0) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int64_t rows = op.mn_extent - mn0;
-    rows = rows < 0 ? 0 : (rows > 256 ? 256 : rows);
-    rsrc = rsrc_words(op.ptr + mn0 * op.ld, (uint32_t)(rows * op.ld * 2));
-    // block j * kWaves + wave holds 16 rows; lane -> row + lane/4, physical
-    // chunk lane % 4, logical chunk (lane % 4) ^ f(row), f(row) the same for
-    // every block because blocks start at multiples of 16 rows
-    const int row = wave * 16 + (lane >> 2);
-    const int f = ((lane >> 3) ^ (lane >> 4)) & 3;
-    const int c = (lane & 3) ^ f;
-    kc = c * 8;
-    voff0 = (uint32_t)((row * op.ld + kc) * 2);
-    row_step = (uint32_t)(G::kWaves * 16 * op.ld * 2);
-    k_extent = op.k_extent;
-  }
-  // Issue load j of this wave's loads of one step into the tile at LDS byte
-  // address `tile` (step K offset k0).
-  __device__ __forceinline__ void issue_one(uint32_t tile, int64_t k0, int j) const {
-    const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const bool ok = k0 + kc < k_extent;
-    dma16(tile + (uint32_t)(j * G::kWaves + wave) * 1024u,
-          ok ? voff0 + j * row_step + (uint32_t)(k0 * 2) : kOutOfRange, rsrc);
-  }
-  __device__ __forceinline__ void issue(uint32_t tile, int64_t k0) const {
-#pragma unroll
-    for (int j = 0; j < G::kLoadsPerOperand; ++j) issue_one(tile, k0, j);
-  }
-};
-
-// Per-lane fragment bases for 64-byte rows: slice ks reads physical chunk
-// (2 ks) ^ t with t = (lane / 32) ^ f(lane % 32) (fragment row blocks start at
-// multiples of 32 rows, which leave f unchanged).
-struct DmaFrag {
-  uint32_t a[2], b[2];
-};
-
-template <class G>
-__device__ __forceinline__ DmaFrag dma_frag_bases() {
-  const int lane = threadIdx.x & 63;
-  const int r = lane & 31;
-  const int t = (lane >> 5) ^ (((r >> 1) ^ (r >> 2)) & 3);
-  DmaFrag f;
-#pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
-    const uint32_t off = (uint32_t)(r * 64 + (((2 * ks) ^ t) << 4));
-    f.a[ks] = (uint32_t)(G::wm() * (256 / G::WM) * 64) + off;
-    f.b[ks] = (uint32_t)(kDmaTile + G::wn() * (256 / G::WN) * 64) + off;
-  }
-  return f;
-}
-
-template <class G>
-__device__ __forceinline__ void dma_frags(const uint8_t* stage, const DmaFrag& f, int ks,
-                                          bf16x8 (&a)[G::MI], bf16x8 (&b)[G::NI]) {
-#pragma unroll
-  for (int i = 0; i < G::MI; ++i)
-    a[i] = *reinterpret_cast<const bf16x8*>(stage + f.a[ks] + 2048 * i);
-#pragma unroll
-  for (int i = 0; i < G::NI; ++i)
-    b[i] = *reinterpret_cast<const bf16x8*>(stage + f.b[ks] + 2048 * i);
-}
-
 template <class G>
 __device__ __forceinline__ void mfma_tiles(const bf16x8 (&a)[G::MI], const bf16x8 (&b)[G::NI],
                                            f32x16 (&acc)[G::MI][G::NI]) {
@@ -196,91 +97,155 @@ __device__ __forceinline__ void mfma_tiles_interleaved(const bf16x8 (&a)[G::MI],
   }
 }
 
-// vmcnt wait allowing `steps` later K steps (`per` loads each) to stay in flight.
-template <int per>
-__device__ __forceinline__ void wait_steps(int steps) {
-  static_assert(kDmaStages <= 5, "extend the cases below");
-  switch (steps) {
-    case 0: wait_vmcnt<0>(); break;
-    case 1: wait_vmcnt<per>(); break;
-    case 2: wait_vmcnt<2 * per>(); break;
-    default: wait_vmcnt<3 * per>(); break;
+template <class G>
+struct DmaOperand {
+  static constexpr int kLoads = 32 / G::kWaves;  // 1 KiB blocks per wave per step
+  i32x4 rsrc;
+  uint32_t voff[kLoads];
+  int kc[kLoads];
+  int64_t k_extent;
+
+  __device__ __forceinline__ void init(const Operand& op, int64_t mn0) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int64_t rows = op.mn_extent - mn0;
+    rows = rows < 0 ? 0 : (rows > 256 ? 256 : rows);
+    rsrc = rsrc_words(op.ptr + mn0 * op.ld, (uint32_t)(rows * op.ld * 2));
+    // block b = j * kWaves + wave holds rows 8 b .. 8 b + 7; lane -> row
+    // 8 b + lane / 8, physical chunk lane % 8, logical chunk
+    // (lane % 8) ^ swz(row), swz(row) = (row ^ (row >> 3)) & 7 = (lane / 8) ^ (b & 7)
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int b = j * G::kWaves + wave;
+      const int row = b * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ (lane >> 3) ^ (b & 7);
+      kc[j] = c * 8;
+      voff[j] = (uint32_t)((row * op.ld + c * 8) * 2);
+    }
+    k_extent = op.k_extent;
   }
+  __device__ __forceinline__ void issue_one(uint32_t tile, int64_t k0, int j) const {
+    const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const bool ok = k0 + kc[j] < k_extent;
+    dma16(tile + (uint32_t)(j * G::kWaves + wave) * 1024u,
+          ok ? voff[j] + (uint32_t)(k0 * 2) : kOutOfRange, rsrc);
+  }
+};
+
+// Fragment bases for 128-byte rows (gemm_core.h swizzle): slice ks, row block i
+// reads base[((2 ks) ^ (4 (i & 1))) / 2] + 4096 i.
+struct FragBase {
+  uint32_t a[4], b[4];
+};
+
+template <class G>
+__device__ __forceinline__ FragBase frag_bases() {
+  const int lane = threadIdx.x & 63;
+  const int r = lane & 31;
+  const int t = (lane >> 5) ^ (r & 7) ^ (r >> 3);
+  FragBase f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t off = (uint32_t)(r * 128 + (((2 * j) ^ t) << 4));
+    f.a[j] = (uint32_t)(G::wm() * (256 / G::WM) * 128) + off;
+    f.b[j] = (uint32_t)(kTileBytes + G::wn() * (256 / G::WN) * 128) + off;
+  }
+  return f;
+}
+
+template <class G>
+__device__ __forceinline__ void read_frags(const uint8_t* stage, const FragBase& f, int ks,
+                                        bf16x8 (&a)[G::MI], bf16x8 (&b)[G::NI]) {
+#pragma unroll
+  for (int i = 0; i < G::MI; ++i)
+    a[i] = *reinterpret_cast<const bf16x8*>(stage + f.a[((2 * ks) ^ (4 * (i & 1))) >> 1] +
+                                            4096 * i);
+#pragma unroll
+  for (int i = 0; i < G::NI; ++i)
+    b[i] = *reinterpret_cast<const bf16x8*>(stage + f.b[((2 * ks) ^ (4 * (i & 1))) >> 1] +
+                                            4096 * i);
 }
 
 // Full K loop over [k_begin, k_end) for the tile at (m0, n0), both operands
-// K-major (k_extent % 8 == 0).  Step s lives in stage s % kDmaStages.  Per
-// iteration s:
-//   read slice 1 fragments; MFMAs of slice 0;
-//   wait for step s + 1's loads, barrier (step s + 1 now visible, stage of
-//   step s - 1 free); issue step s + kDmaStages - 1 into that stage;
-//   read step s + 1's slice 0 fragments; MFMAs of slice 1.
+// K-major (k_extent % 8 == 0), K step 64, two LDS stages.  Per step s (stage
+// s % 2), with slice 0's fragments already in registers:
+//   slices 0..2: read the next slice's fragments, then this slice's MFMAs
+//     (slice 0 also issues step s + 1's B loads, deferred from step s - 1);
+//   wait for step s + 1's loads and for this wave's LDS reads; barrier
+//     (step s + 1 visible; stage s % 2 no longer read by anyone);
+//   read step s + 1's slice 0 fragments; slice 3's MFMAs, issuing step s + 2's
+//     A loads into stage s % 2.
 // Ends with a barrier, so the caller may reuse `smem` right away.
 template <class G>
-__device__ __forceinline__ void mainloop_dma(const Operand& A, const Operand& B, int64_t m0,
-                                             int64_t n0, int64_t k_begin, int64_t k_end,
-                                             uint8_t* smem, f32x16 (&acc)[G::MI][G::NI]) {
+__device__ __forceinline__ void mainloop(const Operand& A, const Operand& B, int64_t m0,
+                                         int64_t n0, int64_t k_begin, int64_t k_end,
+                                         uint8_t* smem, f32x16 (&acc)[G::MI][G::NI]) {
 #pragma unroll
   for (int mi = 0; mi < G::MI; ++mi)
 #pragma unroll
     for (int ni = 0; ni < G::NI; ++ni)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.0f;
-  const int64_t nk = (k_end - k_begin + kDmaBK - 1) / kDmaBK;
+  const int64_t nk = (k_end - k_begin + kBK - 1) / kBK;
   if (nk <= 0) return;
-  constexpr int kPer = 2 * G::kLoadsPerOperand;  // loads per thread per step
+  constexpr int L = DmaOperand<G>::kLoads;
   DmaOperand<G> la, lb;
   la.init(A, m0);
   lb.init(B, n0);
-  const DmaFrag f = dma_frag_bases<G>();
+  const FragBase f = frag_bases<G>();
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
-  auto issue = [&](int64_t step, int stage) {
-    const uint32_t st = lds0 + (uint32_t)stage * kDmaStage;
-    la.issue(st, k_begin + step * kDmaBK);
-    lb.issue(st + kDmaTile, k_begin + step * kDmaBK);
-  };
-  // prologue: steps 0 .. kDmaStages - 2 in flight, wait for step 0
-  const int64_t pre = nk < kDmaStages - 1 ? nk : kDmaStages - 1;
+  auto stage_lds = [&](int64_t step) { return lds0 + (uint32_t)(step & 1) * kStageBytes; };
+  auto kof = [&](int64_t step) { return k_begin + step * kBK; };
+  // prologue: step 0 landed, step 1 in flight
 #pragma unroll
-  for (int s = 0; s < kDmaStages - 1; ++s)
-    if (s < pre) issue(s, s);
-  wait_steps<kPer>((int)pre - 1);
+  for (int j = 0; j < L; ++j) la.issue_one(stage_lds(0), kof(0), j);
+#pragma unroll
+  for (int j = 0; j < L; ++j) lb.issue_one(stage_lds(0) + kTileBytes, kof(0), j);
+  wait_vmcnt<0>();
   lds_barrier();
+  if (nk > 1) {
+#pragma unroll
+    for (int j = 0; j < L; ++j) la.issue_one(stage_lds(1), kof(1), j);
+#pragma unroll
+    for (int j = 0; j < L; ++j) lb.issue_one(stage_lds(1) + kTileBytes, kof(1), j);
+  }
   bf16x8 a0[G::MI], b0[G::NI], a1[G::MI], b1[G::NI];
-  dma_frags<G>(smem, f, 0, a0, b0);
-  int cur = 0;                     // stage of step it
-  int ahead = kDmaStages - 1;      // stage of step it + kDmaStages - 1
+  read_frags<G>(smem, f, 0, a0, b0);
   for (int64_t it = 0; it < nk; ++it) {
-    const int nxt = cur + 1 == kDmaStages ? 0 : cur + 1;
-    dma_frags<G>(smem + cur * kDmaStage, f, 1, a1, b1);
+    const uint8_t* cur = smem + (it & 1) * kStageBytes;
+    const uint8_t* nxt = smem + ((it + 1) & 1) * kStageBytes;
+    // B loads of step it + 1, deferred from the previous step's last slice
+    const bool b_due = it >= 1 && it + 1 < nk;
+    const uint32_t st1 = stage_lds(it + 1) + kTileBytes;
+    const int64_t k1 = kof(it + 1);
+    read_frags<G>(cur, f, 1, a1, b1);
+    RBP_FENCE();
+    mfma_tiles_interleaved<G>(a0, b0, acc, L, [&](int l) {
+      if (b_due) lb.issue_one(st1, k1, l);
+    });
+    RBP_FENCE();
+    read_frags<G>(cur, f, 2, a0, b0);
+    RBP_FENCE();
+    mfma_tiles<G>(a1, b1, acc);
+    RBP_FENCE();
+    read_frags<G>(cur, f, 3, a1, b1);
     RBP_FENCE();
     mfma_tiles<G>(a0, b0, acc);
     RBP_FENCE();
-    // steps issued so far: 0 .. min(nk, it + kDmaStages - 1) - 1; step it + 1 must be in
-    const int64_t issued = nk < it + kDmaStages - 1 ? nk : it + kDmaStages - 1;
-    const int64_t later = issued - (it + 2);
-    wait_steps<kPer>(later < 0 ? 0 : (int)later);
+    // step it + 1 landed (only its loads are outstanding); this wave's reads
+    // of stage it % 2 done, so after the barrier the stage may be refilled
+    __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) lgkmcnt(0)
     lds_barrier();
-    // unconditional (the last iteration re-reads a stale stage): a read under
-    // a branch would make the compiler wait for it before the MFMAs below
-    dma_frags<G>(smem + nxt * kDmaStage, f, 0, a0, b0);
+    // unconditional (the last step re-reads a stale stage): a read under a
+    // branch would make the compiler wait for it before the MFMAs below
+    read_frags<G>(nxt, f, 0, a0, b0);
     RBP_FENCE();
-    // step it + kDmaStages - 1 goes into the stage of step it - 1, now free;
-    // its loads are spread over this slice's MFMAs
-    const bool more = it + kDmaStages - 1 < nk;
-    const uint32_t st = lds0 + (uint32_t)ahead * kDmaStage;
-    const int64_t kn = k_begin + (it + kDmaStages - 1) * kDmaBK;
-    mfma_tiles_interleaved<G>(a1, b1, acc, kPer, [&](int l) {
-      if (more) {
-        if (l < G::kLoadsPerOperand)
-          la.issue_one(st, kn, l);
-        else
-          lb.issue_one(st + kDmaTile, kn, l - G::kLoadsPerOperand);
-      }
+    const bool a_due = it + 2 < nk;
+    const uint32_t st2 = stage_lds(it + 2);
+    const int64_t k2 = kof(it + 2);
+    mfma_tiles_interleaved<G>(a1, b1, acc, L, [&](int l) {
+      if (a_due) la.issue_one(st2, k2, l);
     });
     RBP_FENCE();
-    cur = nxt;
-    ahead = ahead + 1 == kDmaStages ? 0 : ahead + 1;
   }
   wait_vmcnt<0>();
   __syncthreads();

@@ -29,24 +29,17 @@
 
 namespace {
 
-using rbp::gemm::acc_m;
-using rbp::gemm::acc_n;
 using rbp::gemm::f32x16;
 using rbp::gemm::kLdsBytes;
 using rbp::gemm::mainloop;
-using rbp::gemm::mainloop_dma;
 using rbp::gemm::map_tile;
 using rbp::gemm::Operand;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kGroupLogits = 4;
-constexpr int kGroupGrad = 4;
+constexpr int kGroupGrad = 8;
 
-#define RBP_GEMM_KERNEL \
-  __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
-
-// Logit products (K-major operands, direct HBM -> LDS loads): 8 waves, two per
-// SIMD, so that enough waves keep loads in flight to feed 256 x 256 tiles.
+// Every product runs on the 8-wave grid (two waves per SIMD).
 using GL = rbp::gemm::Grid8;
 #define RBP_LOGITS_KERNEL                                                        \
   __global__ __attribute__((amdgpu_flat_work_group_size(GL::kThreads, GL::kThreads), \
@@ -74,7 +67,7 @@ RBP_LOGITS_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
   const Operand A{W, d, V, d};
   const Operand B{H, d, T, d};
   f32x16 acc[GL::MI][GL::NI];
-  mainloop_dma<GL>(A, B, m0, n0, 0, d, smem, acc);
+  mainloop<GL>(A, B, m0, n0, 0, d, smem, acc);
 
   float2* lds_ms = reinterpret_cast<float2*>(smem);  // [wm][256 columns]
   const int lane = threadIdx.x & 63;
@@ -177,15 +170,21 @@ __global__ void __launch_bounds__(256) lse_merge_kernel(
   }
 }
 
-// Backward step 1: recompute the tile, write dz = dlogp (onehot - p) as bf16.
+// Backward step 1: recompute the tile, write dz = dlogp (onehot - p) as bf16,
+// both vocabulary-contiguous (G [Tc][Vp], for dhidden) and token-contiguous
+// (Gt [Vp][Tc], for dW).  The transposed copy is staged through LDS in two
+// 128-row halves: lanes holding adjacent tokens swap values so each writes
+// 32-bit token pairs, with a 544-byte row pitch that keeps those writes on
+// distinct banks; rows then leave as 16-byte stores.
 RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
                                           const uint16_t* __restrict__ Hc, int64_t Tn,
                                           int32_t d, int32_t V, const int32_t* __restrict__ tokens,
                                           const int32_t* __restrict__ seq,
                                           const float* __restrict__ lse,
                                           const float* __restrict__ dlogp,
-                                          uint16_t* __restrict__ G, int64_t ldG, int64_t tiles_m,
-                                          int64_t tiles_n) {
+                                          uint16_t* __restrict__ G, int64_t ldG,
+                                          uint16_t* __restrict__ Gt, int64_t ldGt,
+                                          int64_t tiles_m, int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   int64_t tm, tn;
   map_tile(blockIdx.x, tiles_m, tiles_n, kGroupLogits, tm, tn);
@@ -193,94 +192,181 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
   const Operand A{W, d, V, d};
   const Operand B{Hc, d, Tn, d};
   f32x16 acc[GL::MI][GL::NI];
-  mainloop_dma<GL>(A, B, m0, n0, 0, d, smem, acc);
+  mainloop<GL>(A, B, m0, n0, 0, d, smem, acc);
 
+  constexpr int kPitch = 544;                 // bytes per staged vocabulary row
+  static_assert(128 * kPitch <= kLdsBytes, "staging half must fit LDS");
+  const int lane = threadIdx.x & 63;
+  const bool odd = lane & 1;
   const int64_t vlim = (int64_t)V - m0;
+  float ls[GL::NI], dl[GL::NI];
+  int64_t yrow[GL::NI];
 #pragma unroll
   for (int ni = 0; ni < GL::NI; ++ni) {
     const int64_t t = n0 + GL::col(ni);
-    float ls = 0.0f, dl = 0.0f;
-    int64_t y = -1;
+    ls[ni] = 0.0f;
+    dl[ni] = 0.0f;
+    yrow[ni] = -1;
     if (t < Tn && (seq == nullptr || seq[t] >= 0)) {
-      ls = lse[t];
-      dl = dlogp[t];
-      y = (int64_t)tokens[t] - m0;  // target row within this tile
+      ls[ni] = lse[t] * kLog2e;
+      dl[ni] = dlogp[t];
+      yrow[ni] = (int64_t)tokens[t] - m0;  // target row within this tile
     }
-    const float lsb = ls * kLog2e;
-    uint16_t* grow = G + t * ldG + m0;
+  }
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+#pragma unroll
+    for (int mh = 0; mh < GL::MI / 2; ++mh) {
+      const int mi = half * (GL::MI / 2) + mh;
+#pragma unroll
+      for (int ni = 0; ni < GL::NI; ++ni) {
+        const int64_t t = n0 + GL::col(ni);
+        uint16_t* grow = G + t * ldG + m0;
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          float g[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int v = GL::row(mi, rg * 4 + i);
+            const float p = exp2f(fmaf(acc[mi][ni][rg * 4 + i], kLog2e, -ls[ni]));
+            const float oh = (v == yrow[ni]) ? 1.0f : 0.0f;
+            g[i] = (v < vlim) ? dl[ni] * (oh - p) : 0.0f;
+          }
+          const uint32_t p01 = pack_bf16x2(g[0], g[1]), p23 = pack_bf16x2(g[2], g[3]);
+          uint2 pk;
+          pk.x = p01;
+          pk.y = p23;
+          *reinterpret_cast<uint2*>(grow + GL::row(mi, rg * 4)) = pk;
+          // token-pair exchange: the even lane keeps rows 0,1 of the run, the
+          // odd lane rows 2,3; each gets its neighbour's value of those rows
+          const uint32_t give = odd ? p01 : p23;
+          const uint32_t got = (uint32_t)__shfl_xor((int)give, 1, 64);
+          const uint32_t mine = odd ? p23 : p01;
+          // rows r, r+1 (even lane: mine = rows 0,1) as (t_even, t_odd) pairs
+          const uint32_t lo_even = odd ? (got & 0xffffu) : (mine & 0xffffu);
+          const uint32_t lo_odd = odd ? (mine & 0xffffu) : (got & 0xffffu);
+          const uint32_t hi_even = odd ? (got >> 16) : (mine >> 16);
+          const uint32_t hi_odd = odd ? (mine >> 16) : (got >> 16);
+          const int lrow = GL::row(mi, rg * 4) - GL::wm() * (256 / GL::WM) - half * 64 +
+                           GL::wm() * 64 + (odd ? 2 : 0);
+          const int tcol = GL::col(ni) & ~1;
+          uint8_t* dst = smem + lrow * kPitch + tcol * 2;
+          *reinterpret_cast<uint32_t*>(dst) = lo_even | (lo_odd << 16);
+          *reinterpret_cast<uint32_t*>(dst + kPitch) = hi_even | (hi_odd << 16);
+        }
+      }
+    }
+    __syncthreads();
+    // 128 staged rows x 512 bytes -> Gt rows m0 + wm*128 + half*64 + r
+#pragma unroll
+    for (int q = 0; q < 128 * 32 / GL::kThreads; ++q) {
+      const int c = threadIdx.x + q * GL::kThreads;
+      const int lrow = c >> 5, chunk = c & 31;
+      const int wm = lrow >> 6;
+      const int64_t v = m0 + wm * (256 / GL::WM) + half * 64 + (lrow & 63);
+      const uint4 val = *reinterpret_cast<const uint4*>(smem + lrow * kPitch + chunk * 16);
+      *reinterpret_cast<uint4*>(Gt + v * ldGt + n0 + chunk * 8) = val;
+    }
+    __syncthreads();
+  }
+}
+
+// dst[c][r] = src[r][c] for r < R, zero for R <= r < ld_dst (bf16; C % 8 == 0).
+// 64 x 64 tiles staged through LDS; 16-byte loads and stores.
+__global__ void __launch_bounds__(256) transpose_bf16_kernel(const uint16_t* __restrict__ src,
+                                                             int64_t R, int64_t C,
+                                                             uint16_t* __restrict__ dst,
+                                                             int64_t ld_dst) {
+  __shared__ uint16_t tile[64][64 + 8];
+  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
+  const int tr = threadIdx.x >> 3, tc = (threadIdx.x & 7) * 8;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int64_t r = r0 + tr + 32 * i, c = c0 + tc;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (r < R && c < C) v = *reinterpret_cast<const uint4*>(src + r * C + c);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      tile[tr + 32 * i][tc + 2 * q] = (uint16_t)(w[q] & 0xffff);
+      tile[tr + 32 * i][tc + 2 * q + 1] = (uint16_t)(w[q] >> 16);
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int64_t c = c0 + tr + 32 * i, r = r0 + tc;
+    if (c >= C || r >= ld_dst) continue;
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      w[q] = (uint32_t)tile[tc + 2 * q][tr + 32 * i] |
+             ((uint32_t)tile[tc + 2 * q + 1][tr + 32 * i] << 16);
+    *reinterpret_cast<uint4*>(dst + c * ld_dst + r) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// Backward step 2 (direct-load engine): one K half of dH[t][m] = sum_v W[v][m]
+// dz[t][v], reading W transposed ([d][Vp]) so both operands are k-contiguous.
+// Split s writes out + s * split_stride; the halves are added afterwards.
+RBP_LOGITS_KERNEL void dhidden_dma_kernel(const uint16_t* __restrict__ Wt,
+                                          const uint16_t* __restrict__ G, int64_t Tn, int32_t d,
+                                          int64_t ldG, int64_t k_split, float* __restrict__ out0,
+                                          float* __restrict__ out1, int64_t tiles_m,
+                                          int64_t tiles_n) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
+  const int64_t per_split = tiles_m * tiles_n;
+  const int64_t split = blockIdx.x / per_split;
+  int64_t tm, tn;
+  map_tile(blockIdx.x - split * per_split, tiles_m, tiles_n, kGroupGrad, tm, tn);
+  const int64_t m0 = tm * 256, n0 = tn * 256;
+  const Operand A{Wt, ldG, d, ldG};   // (m = hidden unit, k = vocab)
+  const Operand B{G, ldG, Tn, ldG};   // (n = token, k = vocab)
+  const int64_t k_begin = split * k_split;
+  const int64_t k_end = (k_begin + k_split) < ldG ? (k_begin + k_split) : ldG;
+  f32x16 acc[GL::MI][GL::NI];
+  mainloop<GL>(A, B, m0, n0, k_begin, k_end, smem, acc);
+  float* __restrict__ dH = split == 0 ? out0 : out1;
+#pragma unroll
+  for (int ni = 0; ni < GL::NI; ++ni) {
+    const int64_t t = n0 + GL::col(ni);
+    if (t >= Tn) continue;
 #pragma unroll
     for (int mi = 0; mi < GL::MI; ++mi)
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        float g[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int v = GL::row(mi, rg * 4 + i);
-          const float p = exp2f(fmaf(acc[mi][ni][rg * 4 + i], kLog2e, -lsb));
-          const float oh = (v == y) ? 1.0f : 0.0f;
-          g[i] = (v < vlim) ? dl * (oh - p) : 0.0f;
-        }
-        uint2 pk;
-        pk.x = pack_bf16x2(g[0], g[1]);
-        pk.y = pack_bf16x2(g[2], g[3]);
-        *reinterpret_cast<uint2*>(grow + GL::row(mi, rg * 4)) = pk;
+        const int64_t m = m0 + GL::row(mi, rg * 4);
+        if (m < d)
+          *reinterpret_cast<float4*>(dH + t * d + m) =
+              make_float4(acc[mi][ni][rg * 4 + 0], acc[mi][ni][rg * 4 + 1],
+                          acc[mi][ni][rg * 4 + 2], acc[mi][ni][rg * 4 + 3]);
       }
   }
 }
 
-// Backward step 2: dH[t][m] = sum_v W[v][m] dz[t][v].
-RBP_GEMM_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
-                                    const uint16_t* __restrict__ G, int64_t Tn, int32_t d,
-                                    int32_t V, int64_t ldG, float* __restrict__ dH,
-                                    int64_t tiles_m, int64_t tiles_n) {
+// Backward step 3 (direct-load engine): dW[v][m] (+)= sum_t H[t][m] dz[t][v],
+// reading both operands transposed (H^T [d][Tc], dz^T [Vp][Tc], k = token).
+RBP_LOGITS_KERNEL void dweight_dma_kernel(const uint16_t* __restrict__ Ht,
+                                          const uint16_t* __restrict__ Gt, int64_t Tn, int32_t d,
+                                          int32_t V, int64_t ldT, float* __restrict__ dW,
+                                          int accumulate, int64_t tiles_m, int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   int64_t tm, tn;
   map_tile(blockIdx.x, tiles_m, tiles_n, kGroupGrad, tm, tn);
   const int64_t m0 = tm * 256, n0 = tn * 256;
-  const Operand A{W, d, d, V};      // (m = hidden unit, k = vocab): W[k * d + m]
-  const Operand B{G, ldG, Tn, ldG}; // (n = token, k = vocab): G[n * ldG + k]
-  f32x16 acc[4][4];
-  mainloop<false, true>(A, B, m0, n0, 0, ldG, smem, acc);
+  const Operand A{Ht, ldT, d, ldT};   // (m = hidden unit, k = token)
+  const Operand B{Gt, ldT, V, ldT};   // (n = vocab, k = token)
+  f32x16 acc[GL::MI][GL::NI];
+  mainloop<GL>(A, B, m0, n0, 0, Tn, smem, acc);
 #pragma unroll
-  for (int ni = 0; ni < 4; ++ni) {
-    const int64_t t = n0 + acc_n(ni);
-    if (t >= Tn) continue;
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int64_t m = m0 + acc_m(mi, rg * 4);
-        if (m < d) {
-          float4 v = make_float4(acc[mi][ni][rg * 4 + 0], acc[mi][ni][rg * 4 + 1],
-                                 acc[mi][ni][rg * 4 + 2], acc[mi][ni][rg * 4 + 3]);
-          *reinterpret_cast<float4*>(dH + t * d + m) = v;
-        }
-      }
-  }
-}
-
-// Backward step 3: dW[v][m] (+)= sum_t H[t][m] dz[t][v].
-RBP_GEMM_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
-                                    const uint16_t* __restrict__ G, int64_t Tn, int32_t d,
-                                    int32_t V, int64_t ldG, float* __restrict__ dW,
-                                    int accumulate, int64_t tiles_m, int64_t tiles_n) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
-  int64_t tm, tn;
-  map_tile(blockIdx.x, tiles_m, tiles_n, kGroupGrad, tm, tn);
-  const int64_t m0 = tm * 256, n0 = tn * 256;
-  const Operand A{Hc, d, d, Tn};     // (m = hidden unit, k = token): H[k * d + m]
-  const Operand B{G, ldG, ldG, Tn};  // (n = vocab, k = token): G[k * ldG + n]
-  f32x16 acc[4][4];
-  mainloop<false, false>(A, B, m0, n0, 0, Tn, smem, acc);
-#pragma unroll
-  for (int ni = 0; ni < 4; ++ni) {
-    const int64_t v = n0 + acc_n(ni);
+  for (int ni = 0; ni < GL::NI; ++ni) {
+    const int64_t v = n0 + GL::col(ni);
     if (v >= V) continue;
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < GL::MI; ++mi)
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        const int64_t m = m0 + acc_m(mi, rg * 4);
+        const int64_t m = m0 + GL::row(mi, rg * 4);
         if (m < d) {
           float4* dst = reinterpret_cast<float4*>(dW + v * d + m);
           float4 val = make_float4(acc[mi][ni][rg * 4 + 0], acc[mi][ni][rg * 4 + 1],
@@ -298,6 +384,21 @@ RBP_GEMM_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
   }
 }
 
+// a[i] += b[i] (n % 4 == 0), fixed order per element.
+__global__ void __launch_bounds__(256) add_f32_kernel(float* __restrict__ a,
+                                                      const float* __restrict__ b, int64_t n4) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4;
+       i += (int64_t)gridDim.x * 256) {
+    float4 x = reinterpret_cast<float4*>(a)[i];
+    const float4 y = reinterpret_cast<const float4*>(b)[i];
+    x.x += y.x;
+    x.y += y.y;
+    x.z += y.z;
+    x.w += y.w;
+    reinterpret_cast<float4*>(a)[i] = x;
+  }
+}
+
 __global__ void __launch_bounds__(256) fill_zero_kernel(float* __restrict__ p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
     p[i] = 0.0f;
@@ -312,9 +413,33 @@ size_t rbp::logprob_fwd_ws(int64_t T, int32_t V) {
   return align_up(sizeof(float2) * (size_t)(T < 1 ? 1 : T) * (size_t)n_part, 256);
 }
 
-size_t rbp::logprob_bwd_ws(int64_t Tc, int32_t /*d*/, int32_t V) {
-  return align_up(sizeof(uint16_t) * (size_t)round256(Tc < 1 ? 1 : Tc) * (size_t)round256(V),
-                  256);
+namespace {
+// Backward workspace carving: dz [Tc][Vp] bf16, W^T [d][Vp] bf16, the second
+// dhidden K half [Tc][d] fp32, dz^T [Vp][Tc] bf16, H^T [d][Tc] bf16.
+struct BwdWs {
+  uint16_t* G;
+  uint16_t* Wt;
+  float* dh_half;
+  uint16_t* Gt;
+  uint16_t* Ht;
+  size_t bytes;
+};
+BwdWs carve_bwd(void* base, int64_t Tc, int32_t d, int32_t V) {
+  rbp::WsCarver c(base);
+  const int64_t T256 = round256(Tc < 1 ? 1 : Tc), Vp = round256(V);
+  BwdWs w;
+  w.G = c.take<uint16_t>((size_t)T256 * (size_t)Vp);
+  w.Wt = c.take<uint16_t>((size_t)d * (size_t)Vp);
+  w.dh_half = c.take<float>((size_t)T256 * (size_t)d);
+  w.Gt = c.take<uint16_t>((size_t)Vp * (size_t)T256);
+  w.Ht = c.take<uint16_t>((size_t)d * (size_t)T256);
+  w.bytes = rbp::align_up(c.used, 256);
+  return w;
+}
+}  // namespace
+
+size_t rbp::logprob_bwd_ws(int64_t Tc, int32_t d, int32_t V) {
+  return carve_bwd(nullptr, Tc, d < 1 ? 1 : d, V).bytes;
 }
 
 extern "C" int policy_logprob_fwd(const uint16_t* hidden, const uint16_t* W,
@@ -367,24 +492,54 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
     }
     return RBP_OK;
   }
-  // largest chunk (multiple of 256 tokens) whose dz workspace fits
-  int64_t Tc = ws ? (int64_t)(ws_bytes / (sizeof(uint16_t) * (size_t)Vp)) / 256 * 256 : 0;
-  if (Tc > round256(T)) Tc = round256(T);
+  // largest chunk (multiple of 256 tokens) whose workspace fits
+  int64_t Tc = 0;
+  if (ws) {
+    int64_t lo = 256, hi = round256(T);
+    if (rbp::logprob_bwd_ws(lo, d, V) <= ws_bytes) {
+      while (lo < hi) {  // largest multiple of 256 in [lo, hi] that fits
+        const int64_t mid = (lo + hi + 256) / 512 * 256;
+        if (rbp::logprob_bwd_ws(mid, d, V) <= ws_bytes) lo = mid; else hi = mid - 256;
+      }
+      Tc = lo;
+    }
+  }
   RBP_REQUIRE(Tc >= 256, RBP_EWORKSPACE,
               "policy_logprob_bwd: workspace of %zu bytes holds no 256-token chunk (needs %zu)",
               ws_bytes, rbp::logprob_bwd_ws(256, d, V));
-  uint16_t* G = static_cast<uint16_t*>(ws);
+  const BwdWs w = carve_bwd(ws, Tc, d, V);
+  // W^T for the dhidden product (both operands k-contiguous)
+  hipLaunchKernelGGL(transpose_bf16_kernel, dim3(Vp / 64, rbp::ceil_div(d, 64)), dim3(256), 0, s,
+                     W, (int64_t)V, (int64_t)d, w.Wt, Vp);
   for (int64_t t0 = 0; t0 < T; t0 += Tc) {
     const int64_t Tn = (T - t0) < Tc ? (T - t0) : Tc;
     const int64_t tiles_t = rbp::ceil_div(Tn, 256);
     const uint16_t* Hc = hidden + t0 * d;
-    hipLaunchKernelGGL(grad_logits_kernel, dim3(tiles_v * tiles_t), dim3(GL::kThreads), 0, s, W, Hc, Tn,
-                       d, V, tokens + t0, seq_of_token ? seq_of_token + t0 : nullptr, lse + t0,
-                       dlogp + t0, G, Vp, tiles_v, tiles_t);
-    hipLaunchKernelGGL(dhidden_kernel, dim3(tiles_d * tiles_t), dim3(256), 0, s, W, G, Tn, d, V,
-                       Vp, dhidden + t0 * d, tiles_d, tiles_t);
-    hipLaunchKernelGGL(dweight_kernel, dim3(tiles_d * tiles_v), dim3(256), 0, s, Hc, G, Tn, d, V,
-                       Vp, dW, (accumulate_dW || t0 > 0) ? 1 : 0, tiles_d, tiles_v);
+    hipLaunchKernelGGL(grad_logits_kernel, dim3(tiles_v * tiles_t), dim3(GL::kThreads), 0, s, W,
+                       Hc, Tn, d, V, tokens + t0, seq_of_token ? seq_of_token + t0 : nullptr,
+                       lse + t0, dlogp + t0, w.G, Vp, w.Gt, Tc, tiles_v, tiles_t);
+    // dhidden in two K halves when one pass would leave the last round of
+    // workgroups mostly empty
+    const int64_t tiles_dh = tiles_d * tiles_t;
+    const int splits = tiles_dh < 1024 && Vp >= 512 ? 2 : 1;
+    const int64_t k_split = splits == 2 ? Vp / 2 : Vp;
+    hipLaunchKernelGGL(dhidden_dma_kernel, dim3(tiles_dh * splits), dim3(GL::kThreads), 0, s,
+                       w.Wt, w.G, Tn, d, Vp, k_split, dhidden + t0 * d, w.dh_half, tiles_d,
+                       tiles_t);
+    if (splits == 2) {
+      const int64_t n4 = Tn * d / 4;
+      int64_t blocks = rbp::ceil_div(n4, 256);
+      if (blocks > 8192) blocks = 8192;
+      hipLaunchKernelGGL(add_f32_kernel, dim3(blocks), dim3(256), 0, s, dhidden + t0 * d,
+                         w.dh_half, n4);
+    }
+    // dW on the direct-load engine: token-contiguous copies of dz and H
+    const int64_t T256 = round256(Tn);
+    hipLaunchKernelGGL(transpose_bf16_kernel, dim3(T256 / 64, rbp::ceil_div(d, 64)), dim3(256), 0,
+                       s, Hc, Tn, (int64_t)d, w.Ht, Tc);
+    hipLaunchKernelGGL(dweight_dma_kernel, dim3(tiles_d * tiles_v), dim3(GL::kThreads), 0, s,
+                       w.Ht, w.Gt, Tn, d, V, Tc, dW, (accumulate_dW || t0 > 0) ? 1 : 0, tiles_d,
+                       tiles_v);
   }
   RBP_CHECK_LAUNCH("policy_logprob_bwd");
   return RBP_OK;
