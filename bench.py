@@ -29,6 +29,21 @@ PEAK_BF16 = 2.5e15        # MI355X dense bf16 MFMA, FLOP/s
 PEAK_HBM = 8.0e12         # MI355X HBM3E, B/s
 ROOT = os.path.dirname(os.path.abspath(__file__))
 
+# HBM traffic of one policy_logprob_fwd call at the 16384-token micro-batch
+# (d=3584, V=152064): FETCH_SIZE and WRITE_SIZE per dispatch from two
+# rocprofv3 --pmc passes over this script, scaled by what the same counters
+# read for a plain copy of known size (--copy-probe-mib: a 1 GiB copy reads
+# 524302 KiB of FETCH_SIZE, factor 2.0, and 1048576 KiB of WRITE_SIZE, factor
+# 1.0).  Only valid for the sources the counters were read on.
+TRAFFIC_SOURCES = ("logprob.hip", "gemm_core.h", "gemm_dma.h")
+TRAFFIC = {
+    "sources_sha256": "902b8192f7421d881a7ffe25ae987fad7e453efded898897a67da4674b1086af",
+    "fetch_bytes": {"logits_lse_partial_kernel": 27359900081,   # 13359692 KiB x 2.0
+                    "lse_merge_kernel": 373312410},             # 182294 KiB x 2.0
+    "write_bytes": {"logits_lse_partial_kernel": 116963904,     # 114223 KiB
+                    "lse_merge_kernel": 264704},                # 258.5 KiB
+}
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -37,9 +52,44 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="head7b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=128,
+    ap.add_argument("--cpu-tokens", type=int, default=3072,
                     help="tokens of the bounded sample the CPU oracle is timed on")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB three "
+                         "times (calibrates the HBM byte counters) and exit")
     return ap.parse_args()
+
+
+def copy_probe(mib):
+    """A plain copy of known size, for scaling FETCH_SIZE / WRITE_SIZE."""
+    import torch
+
+    n = mib << 18  # float32 elements
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4}))
+
+
+def sources_sha256():
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, "paper_2604_08706_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_bytes():
+    """HBM bytes per forward call, or None once the kernel sources differ
+    from the ones the counters were read on."""
+    if TRAFFIC is None or TRAFFIC["sources_sha256"] != sources_sha256():
+        return None
+    return sum(TRAFFIC["fetch_bytes"].values()) + sum(TRAFFIC["write_bytes"].values())
 
 
 def setup(wl, seed=0):
@@ -180,6 +230,9 @@ def cpu_baseline(wl, n_tokens, seed=0):
 
 def main():
     args = parse()
+    if args.copy_probe_mib:
+        copy_probe(args.copy_probe_mib)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
               "data-parallel path is a design note, not part of this build", file=sys.stderr)
@@ -250,7 +303,7 @@ def main():
             "peak": PEAK_BF16 / 1e12,
             "unit": "TFLOP/s",
             "frac": round(fwd_flops / (fwd_ms / 1e3) / PEAK_BF16, 4),
-            "traffic": None,
+            "traffic": traffic_bytes(),
         },
         "wall_s_timed": round(t_wall, 3),
     }
