@@ -65,6 +65,10 @@ struct Grid {
   static __device__ __forceinline__ int row(int mi, int r) {
     return wm() * (256 / WM) + mi * 32 + (r >> 2) * 8 + ((threadIdx.x & 63) >> 5) * 4 + (r & 3);
   }
+  // row(mi, r) - row(0, 0): a compile-time constant for unrolled mi, r
+  static __device__ __forceinline__ constexpr int row_off(int mi, int r) {
+    return mi * 32 + (r >> 2) * 8 + (r & 3);
+  }
   static __device__ __forceinline__ int col(int ni) {
     return wn() * (256 / WN) + ni * 32 + (threadIdx.x & 31);
   }
@@ -78,20 +82,22 @@ using Grid8 = Grid<2, 4>;
 // tiles), then rastered in groups of `group_m` M-tiles per N-tile: the ~32
 // blocks an XCD runs at once form a compact group_m x (32 / group_m) patch
 // whose operand rows are shared through that XCD's L2.
-__device__ __forceinline__ void map_tile(int64_t bid, int64_t tiles_m, int64_t tiles_n,
-                                         int64_t group_m, int64_t& tm, int64_t& tn) {
-  const int64_t nblk = tiles_m * tiles_n;
-  const int64_t xcd = bid & 7, local = bid >> 3;
-  const int64_t per = nblk >> 3, rem = nblk & 7;
-  const int64_t L = xcd < rem ? xcd * (per + 1) + local
-                              : rem * (per + 1) + (xcd - rem) * per + local;
-  const int64_t group_size = group_m * tiles_n;
-  const int64_t g = L / group_size;
-  const int64_t first_m = g * group_m;
-  const int64_t gm = (tiles_m - first_m) < group_m ? (tiles_m - first_m) : group_m;
-  const int64_t in = L - g * group_size;
-  tm = first_m + in % gm;
-  tn = in / gm;
+__device__ __forceinline__ void map_tile(int32_t bid, int32_t tiles_m, int32_t tiles_n,
+                                         int32_t group_m, int32_t& tm, int32_t& tn) {
+  const uint32_t nblk = (uint32_t)tiles_m * (uint32_t)tiles_n;
+  const uint32_t xcd = (uint32_t)bid & 7u, local = (uint32_t)bid >> 3;
+  const uint32_t per = nblk >> 3, rem = nblk & 7u;
+  const uint32_t L = xcd < rem ? xcd * (per + 1) + local
+                               : rem * (per + 1) + (xcd - rem) * per + local;
+  const uint32_t group_size = (uint32_t)group_m * (uint32_t)tiles_n;
+  const uint32_t g = L / group_size;
+  const uint32_t first_m = g * (uint32_t)group_m;
+  const uint32_t gm = ((uint32_t)tiles_m - first_m) < (uint32_t)group_m
+                          ? ((uint32_t)tiles_m - first_m)
+                          : (uint32_t)group_m;
+  const uint32_t in = L - g * group_size;
+  tm = (int32_t)(first_m + in % gm);
+  tn = (int32_t)(in / gm);
 }
 
 }  // namespace gemm

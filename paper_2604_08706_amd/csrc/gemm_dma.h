@@ -97,19 +97,17 @@ __device__ __forceinline__ void mfma_tiles_interleaved(const bf16x8 (&a)[G::MI],
   }
 }
 
+// Each lane's share of one operand tile's loads.  Load j of a wave moves a
+// 1 KiB block (8 rows x 128 bytes) into LDS; the offsets are relative to the
+// first row of the tile, so they serve every tile of a launch.
 template <class G>
-struct DmaOperand {
+struct DmaLanes {
   static constexpr int kLoads = 32 / G::kWaves;  // 1 KiB blocks per wave per step
-  i32x4 rsrc;
   uint32_t voff[kLoads];
   int kc[kLoads];
-  int64_t k_extent;
 
-  __device__ __forceinline__ void init(const Operand& op, int64_t mn0) {
+  __device__ __forceinline__ void init(int64_t ld) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int64_t rows = op.mn_extent - mn0;
-    rows = rows < 0 ? 0 : (rows > 256 ? 256 : rows);
-    rsrc = rsrc_words(op.ptr + mn0 * op.ld, (uint32_t)(rows * op.ld * 2));
     // block b = j * kWaves + wave holds rows 8 b .. 8 b + 7; lane -> row
     // 8 b + lane / 8, physical chunk lane % 8, logical chunk
     // (lane % 8) ^ swz(row), swz(row) = (row ^ (row >> 3)) & 7 = (lane / 8) ^ (b & 7)
@@ -119,17 +117,27 @@ struct DmaOperand {
       const int row = b * 8 + (lane >> 3);
       const int c = (lane & 7) ^ (lane >> 3) ^ (b & 7);
       kc[j] = c * 8;
-      voff[j] = (uint32_t)((row * op.ld + c * 8) * 2);
+      voff[j] = (uint32_t)((row * ld + c * 8) * 2);
     }
-    k_extent = op.k_extent;
   }
-  __device__ __forceinline__ void issue_one(uint32_t tile, int64_t k0, int j) const {
+  // load j of K step k0 from the tile whose resource is `rsrc` into the LDS
+  // tile at byte address `tile`; columns at or past k_extent read as zero
+  __device__ __forceinline__ void issue(uint32_t tile, i32x4 rsrc, int32_t k0,
+                                        int32_t k_extent, int j) const {
     const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const bool ok = k0 + kc[j] < k_extent;
     dma16(tile + (uint32_t)(j * G::kWaves + wave) * 1024u,
           ok ? voff[j] + (uint32_t)(k0 * 2) : kOutOfRange, rsrc);
   }
 };
+
+// Buffer resource over the (at most 256) rows of `op` starting at mn0: rows
+// past the operand's end read as zero.
+__device__ __forceinline__ i32x4 tile_rsrc(const Operand& op, int64_t mn0) {
+  int64_t rows = op.mn_extent - mn0;
+  rows = rows < 0 ? 0 : (rows > 256 ? 256 : rows);
+  return rsrc_words(op.ptr + mn0 * op.ld, (uint32_t)(rows * op.ld * 2));
+}
 
 // Fragment bases for 128-byte rows (gemm_core.h swizzle): slice ks, row block i
 // reads base[((2 ks) ^ (4 (i & 1))) / 2] + 4096 i.
@@ -165,90 +173,166 @@ __device__ __forceinline__ void read_frags(const uint8_t* stage, const FragBase&
                                             4096 * i);
 }
 
-// Full K loop over [k_begin, k_end) for the tile at (m0, n0), both operands
-// K-major (k_extent % 8 == 0), K step 64, two LDS stages.  Per step s (stage
-// s % 2), with slice 0's fragments already in registers:
-//   slices 0..2: read the next slice's fragments, then this slice's MFMAs
-//     (slice 0 also issues step s + 1's B loads, deferred from step s - 1);
-//   wait for step s + 1's loads and for this wave's LDS reads; barrier
-//     (step s + 1 visible; stage s % 2 no longer read by anyone);
-//   read step s + 1's slice 0 fragments; slice 3's MFMAs, issuing step s + 2's
-//     A loads into stage s % 2.
-// Ends with a barrier, so the caller may reuse `smem` right away.
-template <class G>
-__device__ __forceinline__ void mainloop(const Operand& A, const Operand& B, int64_t m0,
-                                         int64_t n0, int64_t k_begin, int64_t k_end,
-                                         uint8_t* smem, f32x16 (&acc)[G::MI][G::NI]) {
+// One output tile: rows m0.. of A, rows n0.. of B, K range [k_begin, k_end)
+// (non-empty).  32-bit fields keep the loop's scalar state small.
+struct Tile {
+  int32_t m0, n0, k_begin, k_end;
+};
+
+__device__ __forceinline__ int32_t k_steps(const Tile& t) {
+  return (t.k_end - t.k_begin + kBK - 1) / kBK;
+}
+
+// Load-side view of a tile: buffer resources of its A and B rows and its
+// first K column.  A resource of range 0 (past the end of the stream) makes
+// every load read zeros.
+struct TileRes {
+  i32x4 ra, rb;
+  int32_t kb;
+};
+
+// Persistent tile loop.  This workgroup takes the virtual blocks blockIdx.x,
+// blockIdx.x + gridDim.x, ... below n_vid; tile_of(vid) gives each one's Tile
+// (every tile of a launch has the same number of K steps, nk >= 1) and
+// epi(vid, acc) consumes its finished fp32 accumulators.  Both operands are
+// K-major (k_extent % 8 == 0).
+//
+// The K steps of consecutive tiles form one stream through two 64-KiB LDS
+// stages (stream step g in stage g % 2), so the first steps of the next tile
+// load while the current tile's last steps multiply and its epilogue runs.
+// Per step g, with slice 0's fragments already in registers:
+//   slice 0: read slice 1; MFMAs; issue the B loads of step g + 1 (their A
+//            loads went out in step g - 1, or in the prologue);
+//   slices 1, 2: read the next slice; MFMAs;
+//   wait for step g + 1's loads and this wave's LDS reads; barrier (step g + 1
+//   visible to all; stage g % 2 no longer read);
+//   slice 3: read step g + 1's slice 0; MFMAs; issue step g + 2's A loads into
+//            stage g % 2;
+//   after the last step of a tile: epi(), which may use LDS only at byte
+//   offsets >= kLdsBytes (the stages are in use) and may contain barriers.
+// The load cursor runs two steps ahead of the MFMAs; it holds its tile's
+// resources (cur) and the following tile's (nxt), refreshed once per tile.
+template <class G, class TileFn, class EpiFn>
+__device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, int32_t n_vid,
+                                            uint8_t* smem, TileFn&& tile_of, EpiFn&& epi) {
+  const int32_t stride = (int32_t)gridDim.x;
+  const int32_t vid0 = (int32_t)blockIdx.x;
+  if (vid0 >= n_vid) return;
+  constexpr int L = DmaLanes<G>::kLoads;
+  DmaLanes<G> la, lb;
+  la.init(A.ld);
+  lb.init(B.ld);
+  const FragBase f = frag_bases<G>();
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
+  const int32_t nk = k_steps(tile_of(vid0));
+  const int32_t ka = (int32_t)A.k_extent, kbx = (int32_t)B.k_extent;
+
+  auto res_of = [&](int32_t vid) {
+    TileRes r;
+    if (vid < n_vid) {
+      const Tile t = tile_of(vid);
+      r.ra = tile_rsrc(A, t.m0);
+      r.rb = tile_rsrc(B, t.n0);
+      r.kb = t.k_begin;
+    } else {
+      r.ra = rsrc_words(A.ptr, 0u);
+      r.rb = rsrc_words(B.ptr, 0u);
+      r.kb = 0;
+    }
+    return r;
+  };
+  // load cursor: tile qvid (resources cur), K step qs; nxt = tile qvid + stride
+  int32_t qvid = vid0, qs = 0;
+  TileRes cur = res_of(vid0), nxt = res_of(vid0 + stride);
+  auto advance = [&]() {
+    if (++qs == nk) {
+      qs = 0;
+      qvid += stride;
+      cur = nxt;
+    }
+  };
+  auto issue_a = [&](uint32_t stage, int j) {
+    la.issue(stage, cur.ra, cur.kb + qs * kBK, ka, j);
+  };
+  auto issue_b = [&](uint32_t stage, int j) {
+    lb.issue(stage + kTileBytes, cur.rb, cur.kb + qs * kBK, kbx, j);
+  };
+
+  // prologue: step 0 landed, step 1's A loads in flight (its B loads are
+  // issued in step 0's first slice), cursor at step 1
+#pragma unroll
+  for (int j = 0; j < L; ++j) issue_a(lds0, j);
+#pragma unroll
+  for (int j = 0; j < L; ++j) issue_b(lds0, j);
+  wait_vmcnt<0>();
+  lds_barrier();
+  advance();
+  if (qs == 0) nxt = res_of(qvid + stride);
+#pragma unroll
+  for (int j = 0; j < L; ++j) issue_a(lds0 + kStageBytes, j);
+
+  int32_t mvid = vid0, mit = 0;
+  f32x16 acc[G::MI][G::NI];
 #pragma unroll
   for (int mi = 0; mi < G::MI; ++mi)
 #pragma unroll
     for (int ni = 0; ni < G::NI; ++ni)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.0f;
-  const int64_t nk = (k_end - k_begin + kBK - 1) / kBK;
-  if (nk <= 0) return;
-  constexpr int L = DmaOperand<G>::kLoads;
-  DmaOperand<G> la, lb;
-  la.init(A, m0);
-  lb.init(B, n0);
-  const FragBase f = frag_bases<G>();
-  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
-  auto stage_lds = [&](int64_t step) { return lds0 + (uint32_t)(step & 1) * kStageBytes; };
-  auto kof = [&](int64_t step) { return k_begin + step * kBK; };
-  // prologue: step 0 landed, step 1 in flight
-#pragma unroll
-  for (int j = 0; j < L; ++j) la.issue_one(stage_lds(0), kof(0), j);
-#pragma unroll
-  for (int j = 0; j < L; ++j) lb.issue_one(stage_lds(0) + kTileBytes, kof(0), j);
-  wait_vmcnt<0>();
-  lds_barrier();
-  if (nk > 1) {
-#pragma unroll
-    for (int j = 0; j < L; ++j) la.issue_one(stage_lds(1), kof(1), j);
-#pragma unroll
-    for (int j = 0; j < L; ++j) lb.issue_one(stage_lds(1) + kTileBytes, kof(1), j);
-  }
   bf16x8 a0[G::MI], b0[G::NI], a1[G::MI], b1[G::NI];
   read_frags<G>(smem, f, 0, a0, b0);
-  for (int64_t it = 0; it < nk; ++it) {
-    const uint8_t* cur = smem + (it & 1) * kStageBytes;
-    const uint8_t* nxt = smem + ((it + 1) & 1) * kStageBytes;
-    // B loads of step it + 1, deferred from the previous step's last slice
-    const bool b_due = it >= 1 && it + 1 < nk;
-    const uint32_t st1 = stage_lds(it + 1) + kTileBytes;
-    const int64_t k1 = kof(it + 1);
-    read_frags<G>(cur, f, 1, a1, b1);
+  for (uint32_t g = 0;; ++g) {
+    const uint8_t* cur_st = smem + (g & 1) * kStageBytes;
+    const uint8_t* nxt_st = smem + ((g + 1) & 1) * kStageBytes;
+    const uint32_t st_next = lds0 + ((g + 1) & 1) * kStageBytes;
+    const uint32_t st_cur = lds0 + (g & 1) * kStageBytes;
+    read_frags<G>(cur_st, f, 1, a1, b1);
     RBP_FENCE();
-    mfma_tiles_interleaved<G>(a0, b0, acc, L, [&](int l) {
-      if (b_due) lb.issue_one(st1, k1, l);
-    });
+    mfma_tiles_interleaved<G>(a0, b0, acc, L, [&](int l) { issue_b(st_next, l); });
     RBP_FENCE();
-    read_frags<G>(cur, f, 2, a0, b0);
+    advance();
+    read_frags<G>(cur_st, f, 2, a0, b0);
     RBP_FENCE();
     mfma_tiles<G>(a1, b1, acc);
     RBP_FENCE();
-    read_frags<G>(cur, f, 3, a1, b1);
+    read_frags<G>(cur_st, f, 3, a1, b1);
     RBP_FENCE();
     mfma_tiles<G>(a0, b0, acc);
     RBP_FENCE();
-    // step it + 1 landed (only its loads are outstanding); this wave's reads
-    // of stage it % 2 done, so after the barrier the stage may be refilled
+    // step g + 1 landed (only its loads are outstanding); this wave's reads
+    // of stage g % 2 done, so after the barrier the stage may be refilled
     __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) lgkmcnt(0)
     lds_barrier();
-    // unconditional (the last step re-reads a stale stage): a read under a
-    // branch would make the compiler wait for it before the MFMAs below
-    read_frags<G>(nxt, f, 0, a0, b0);
+    // unconditional (after the last step it reads a stale stage): a read under
+    // a branch would make the compiler wait for it before the MFMAs below
+    read_frags<G>(nxt_st, f, 0, a0, b0);
     RBP_FENCE();
-    const bool a_due = it + 2 < nk;
-    const uint32_t st2 = stage_lds(it + 2);
-    const int64_t k2 = kof(it + 2);
-    mfma_tiles_interleaved<G>(a1, b1, acc, L, [&](int l) {
-      if (a_due) la.issue_one(st2, k2, l);
-    });
+    mfma_tiles_interleaved<G>(a1, b1, acc, L, [&](int l) { issue_a(st_cur, l); });
     RBP_FENCE();
+    if (++mit == nk) {
+      epi(mvid, acc);
+#pragma unroll
+      for (int mi = 0; mi < G::MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < G::NI; ++ni)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.0f;
+      mvid += stride;
+      if (mvid >= n_vid) break;
+      mit = 0;
+      nxt = res_of(qvid + stride);
+    }
   }
   wait_vmcnt<0>();
-  __syncthreads();
+}
+
+// Workgroups for a persistent launch over n_tiles tiles on a device with
+// n_cu compute units (one 256 x 256 workgroup per CU): a multiple of 8, so a
+// virtual block keeps the XCD (block id mod 8) of the workgroup that runs it.
+inline int64_t stream_grid(int64_t n_tiles, int n_cu) {
+  int64_t g = n_cu < 8 ? 8 : (n_cu / 8) * 8;
+  const int64_t need = (n_tiles + 7) / 8 * 8;
+  return g < need ? g : need;
 }
 
 }  // namespace gemm

@@ -14,12 +14,14 @@
 //
 // Backward, per chunk of Tc tokens:
 //   1. the same product is recomputed; its epilogue turns the tile into
-//      dz = dlogp (onehot - exp(z - lse)), rounded to bf16, into a [Tc, Vp]
-//      workspace (Vp = V rounded up to 256; padding written as zeros);
-//   2. dH^T = W^T dz^T  (A = W read vocab-major, transposed in the loader);
-//   3. dW^T = H^T dz    (both operands token-major, transposed in the loader).
-// All three are MFMA-bound; no floating-point atomics are used, so results are
-// bitwise reproducible.
+//      dz = dlogp (onehot - exp(z - lse)), rounded to bf16, written both
+//      token-major (dz [Tc][Vp]) and vocabulary-major (dz^T [Vp][Tc]);
+//      Vp = V rounded up to 256, padding written as zeros;
+//   2. dH = dz W as sum_v W^T[m][v] dz[t][v], W^T transposed once per call;
+//   3. dW = dz^T H as sum_t H^T[m][t] dz^T[v][t], H^T transposed per chunk.
+// Every product keeps both operands k-contiguous and runs on the persistent
+// direct-load stream of gemm_dma.h (one 256 x 256 workgroup per CU).  No
+// floating-point atomics are used, so results are bitwise reproducible.
 
 #include <cmath>
 
@@ -31,7 +33,8 @@ namespace {
 
 using rbp::gemm::f32x16;
 using rbp::gemm::kLdsBytes;
-using rbp::gemm::mainloop;
+using rbp::gemm::Tile;
+using rbp::gemm::tile_stream;
 using rbp::gemm::map_tile;
 using rbp::gemm::Operand;
 
@@ -45,6 +48,11 @@ using GL = rbp::gemm::Grid8;
   __global__ __attribute__((amdgpu_flat_work_group_size(GL::kThreads, GL::kThreads), \
                             amdgpu_waves_per_eu(GL::kWaves / 4, GL::kWaves / 4)))
 
+// 2^x on the hardware unit (v_exp_f32, ~1 ulp).  Arguments here are
+// (z - max) * log2 e <= 0; below -126 the result flushes toward zero, which
+// only drops terms under 2^-126 of the largest one in a sum.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float((uint32_t)b << 16);
 }
@@ -54,60 +62,83 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
-// Forward tile: partial (max, sum exp) of each token column over 256 vocab rows.
+// Forward: per 256 x 256 tile, the partial (max, sum exp) of each token
+// column over the tile's 256 vocabulary rows.
 RBP_LOGITS_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
                                                  const uint16_t* __restrict__ H, int64_t T,
                                                  int32_t d, int32_t V, int64_t tiles_m,
                                                  int64_t tiles_n, float2* __restrict__ part,
                                                  int64_t ld_part) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
-  int64_t tm, tn;
-  map_tile(blockIdx.x, tiles_m, tiles_n, kGroupLogits, tm, tn);
-  const int64_t m0 = tm * 256, n0 = tn * 256;
+  // two operand stages, then the cross-wave (max, sum) exchange [WM][256]
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes + GL::WM * 256 * 8];
+  float2* lds_ms = reinterpret_cast<float2*>(smem + kLdsBytes);
   const Operand A{W, d, V, d};
   const Operand B{H, d, T, d};
-  f32x16 acc[GL::MI][GL::NI];
-  mainloop<GL>(A, B, m0, n0, 0, d, smem, acc);
-
-  float2* lds_ms = reinterpret_cast<float2*>(smem);  // [wm][256 columns]
   const int lane = threadIdx.x & 63;
-  const int64_t vlim = (int64_t)V - m0;
-#pragma unroll
-  for (int ni = 0; ni < GL::NI; ++ni) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int mi = 0; mi < GL::MI; ++mi)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        if (GL::row(mi, r) < vlim) mx = fmaxf(mx, acc[mi][ni][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    float sum = 0.0f;
-    if (mx != -INFINITY) {
-      const float mb = mx * kLog2e;
+  auto tile_of = [&](int32_t vid) {
+    int32_t tm, tn;
+    map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupLogits, tm, tn);
+    return Tile{tm * 256, tn * 256, 0, d};
+  };
+  auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
+    const Tile tile = tile_of(vid);
+    const int32_t vlim = V - tile.m0;
+    if (vlim < 256) {  // last vocabulary tile: rows past V take no part
+      const int32_t lim = vlim - GL::row(0, 0);  // row(mi, r) < V  <=>  row_off(mi, r) < lim
 #pragma unroll
       for (int mi = 0; mi < GL::MI; ++mi)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (GL::row(mi, r) < vlim) sum += exp2f(fmaf(acc[mi][ni][r], kLog2e, -mb));
-    }
-    sum += __shfl_xor(sum, 32, 64);
-    if (lane < 32) lds_ms[GL::wm() * 256 + GL::col(ni)] = make_float2(mx, sum);
-  }
-  __syncthreads();
-  if (threadIdx.x < 256) {
-    const int col = threadIdx.x;
-    float M = -INFINITY;
+        for (int ni = 0; ni < GL::NI; ++ni)
 #pragma unroll
-    for (int w = 0; w < GL::WM; ++w) M = fmaxf(M, lds_ms[w * 256 + col].x);
-    float S = 0.0f;
-#pragma unroll
-    for (int w = 0; w < GL::WM; ++w) {
-      const float2 q = lds_ms[w * 256 + col];
-      if (q.x != -INFINITY) S += q.y * exp2f((q.x - M) * kLog2e);
+          for (int r = 0; r < 16; ++r) {
+            // all ones where the row is real (mask arithmetic, not compares:
+            // 128 live compare masks would overflow the scalar registers)
+            const uint32_t keep = (uint32_t)((GL::row_off(mi, r) - lim) >> 31);
+            acc[mi][ni][r] = __uint_as_float((__float_as_uint(acc[mi][ni][r]) & keep) |
+                                             (0xff800000u & ~keep));
+          }
     }
-    const int64_t t = n0 + col;
-    if (t < T) part[t * ld_part + tm] = make_float2(M, S);
-  }
+#pragma unroll
+    for (int ni = 0; ni < GL::NI; ++ni) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mi = 0; mi < GL::MI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[mi][ni][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      float sum = 0.0f;
+      if (mx != -INFINITY) {
+        const float mb = mx * kLog2e;
+        float s4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int mi = 0; mi < GL::MI; ++mi)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            s4[r & 3] += exp2_hw(fmaf(acc[mi][ni][r], kLog2e, -mb));
+        sum = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+      }
+      sum += __shfl_xor(sum, 32, 64);
+      if (lane < 32) lds_ms[GL::wm() * 256 + GL::col(ni)] = make_float2(mx, sum);
+    }
+    __syncthreads();
+    if (threadIdx.x < 256) {
+      const int col = threadIdx.x;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < GL::WM; ++w) M = fmaxf(M, lds_ms[w * 256 + col].x);
+      float S = 0.0f;
+#pragma unroll
+      for (int w = 0; w < GL::WM; ++w) {
+        const float2 q = lds_ms[w * 256 + col];
+        if (q.x != -INFINITY) S += q.y * exp2_hw((q.x - M) * kLog2e);
+      }
+      const int64_t t = tile.n0 + col;
+      if (t < T) part[t * ld_part + tile.m0 / 256] = make_float2(M, S);
+    }
+    // lds_ms is next written in the next tile's epilogue, after at least one
+    // K step (and its barrier) of that tile
+  };
+  tile_stream<GL>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -170,12 +201,12 @@ __global__ void __launch_bounds__(256) lse_merge_kernel(
   }
 }
 
-// Backward step 1: recompute the tile, write dz = dlogp (onehot - p) as bf16,
-// both vocabulary-contiguous (G [Tc][Vp], for dhidden) and token-contiguous
-// (Gt [Vp][Tc], for dW).  The transposed copy is staged through LDS in two
-// 128-row halves: lanes holding adjacent tokens swap values so each writes
-// 32-bit token pairs, with a 544-byte row pitch that keeps those writes on
-// distinct banks; rows then leave as 16-byte stores.
+// Backward step 1: recompute the tile and write dz = dlogp (onehot - p) as
+// bf16, both token-major (G[t][v]) and vocabulary-major (Gt[v][t]).  Masked
+// and padding tokens get dz = 0 (p is evaluated against lse = +inf).  A lane
+// holds four consecutive vocabulary rows of one token: G takes them as one
+// 8-byte store; for Gt, lanes of adjacent tokens swap halves so that each
+// stores 32-bit (token, token + 1) pairs of two rows.
 RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
                                           const uint16_t* __restrict__ Hc, int64_t Tn,
                                           int32_t d, int32_t V, const int32_t* __restrict__ tokens,
@@ -186,89 +217,92 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
                                           uint16_t* __restrict__ Gt, int64_t ldGt,
                                           int64_t tiles_m, int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
-  int64_t tm, tn;
-  map_tile(blockIdx.x, tiles_m, tiles_n, kGroupLogits, tm, tn);
-  const int64_t m0 = tm * 256, n0 = tn * 256;
   const Operand A{W, d, V, d};
   const Operand B{Hc, d, Tn, d};
-  f32x16 acc[GL::MI][GL::NI];
-  mainloop<GL>(A, B, m0, n0, 0, d, smem, acc);
-
-  constexpr int kPitch = 544;                 // bytes per staged vocabulary row
-  static_assert(128 * kPitch <= kLdsBytes, "staging half must fit LDS");
   const int lane = threadIdx.x & 63;
   const bool odd = lane & 1;
-  const int64_t vlim = (int64_t)V - m0;
-  float ls[GL::NI], dl[GL::NI];
-  int64_t yrow[GL::NI];
+  auto tile_of = [&](int32_t vid) {
+    int32_t tm, tn;
+    map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupLogits, tm, tn);
+    return Tile{tm * 256, tn * 256, 0, d};
+  };
+  auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
+    const Tile tile = tile_of(vid);
+    const int64_t m0 = tile.m0, n0 = tile.n0;
+    const int32_t vlim = V - tile.m0;
+    const bool full = vlim >= 256;
+    const int32_t lim = vlim - GL::row(0, 0);  // as row_off(mi, r) < lim
+    float ls[GL::NI], dl[GL::NI];
+    int yrow[GL::NI];
+    bool hit[GL::NI];  // some token of this wave's column block has its target in the tile
 #pragma unroll
-  for (int ni = 0; ni < GL::NI; ++ni) {
-    const int64_t t = n0 + GL::col(ni);
-    ls[ni] = 0.0f;
-    dl[ni] = 0.0f;
-    yrow[ni] = -1;
-    if (t < Tn && (seq == nullptr || seq[t] >= 0)) {
-      ls[ni] = lse[t] * kLog2e;
-      dl[ni] = dlogp[t];
-      yrow[ni] = (int64_t)tokens[t] - m0;  // target row within this tile
+    for (int ni = 0; ni < GL::NI; ++ni) {
+      const int64_t t = n0 + GL::col(ni);
+      ls[ni] = INFINITY;
+      dl[ni] = 0.0f;
+      int64_t y = -1;
+      if (t < Tn && (seq == nullptr || seq[t] >= 0)) {
+        ls[ni] = lse[t] * kLog2e;
+        dl[ni] = dlogp[t];
+        y = (int64_t)tokens[t] - m0;
+      }
+      const bool in_tile = y >= 0 && y < 256;
+      yrow[ni] = in_tile ? (int)y - GL::row(0, 0) : -1000;  // relative to row(0, 0)
+      hit[ni] = __any(in_tile);
     }
-  }
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
-#pragma unroll
-    for (int mh = 0; mh < GL::MI / 2; ++mh) {
-      const int mi = half * (GL::MI / 2) + mh;
+    for (int mi = 0; mi < GL::MI; ++mi) {
 #pragma unroll
       for (int ni = 0; ni < GL::NI; ++ni) {
         const int64_t t = n0 + GL::col(ni);
+        float g[16];  // p, then dz
+#pragma unroll
+        for (int r = 0; r < 16; ++r) g[r] = exp2_hw(fmaf(acc[mi][ni][r], kLog2e, -ls[ni]));
+        if (hit[ni]) {  // wave-uniform: rare, only here is the one-hot term tested
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            // dl where the row is the target, else 0 (mask arithmetic rather
+            // than compares, which would pile up in scalar registers)
+            const int32_t diff = GL::row_off(mi, r) - yrow[ni];
+            const uint32_t is_y = ~(uint32_t)((diff | -diff) >> 31);
+            g[r] = fmaf(-dl[ni], g[r], __uint_as_float(__float_as_uint(dl[ni]) & is_y));
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) g[r] = -dl[ni] * g[r];
+        }
+        if (!full) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const uint32_t keep = (uint32_t)((GL::row_off(mi, r) - lim) >> 31);
+            g[r] = __uint_as_float(__float_as_uint(g[r]) & keep);
+          }
+        }
         uint16_t* grow = G + t * ldG + m0;
+        const int tcol = GL::col(ni) & ~1;
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
-          float g[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int v = GL::row(mi, rg * 4 + i);
-            const float p = exp2f(fmaf(acc[mi][ni][rg * 4 + i], kLog2e, -ls[ni]));
-            const float oh = (v == yrow[ni]) ? 1.0f : 0.0f;
-            g[i] = (v < vlim) ? dl[ni] * (oh - p) : 0.0f;
-          }
-          const uint32_t p01 = pack_bf16x2(g[0], g[1]), p23 = pack_bf16x2(g[2], g[3]);
-          uint2 pk;
-          pk.x = p01;
-          pk.y = p23;
-          *reinterpret_cast<uint2*>(grow + GL::row(mi, rg * 4)) = pk;
-          // token-pair exchange: the even lane keeps rows 0,1 of the run, the
-          // odd lane rows 2,3; each gets its neighbour's value of those rows
+          const int v0 = GL::row(mi, rg * 4);
+          const uint32_t p01 = pack_bf16x2(g[rg * 4 + 0], g[rg * 4 + 1]);
+          const uint32_t p23 = pack_bf16x2(g[rg * 4 + 2], g[rg * 4 + 3]);
+          *reinterpret_cast<uint2*>(grow + v0) = make_uint2(p01, p23);
+          // token-pair exchange: the even lane keeps rows v0, v0 + 1, the odd
+          // lane rows v0 + 2, v0 + 3; each gets its neighbour's value of those
           const uint32_t give = odd ? p01 : p23;
           const uint32_t got = (uint32_t)__shfl_xor((int)give, 1, 64);
           const uint32_t mine = odd ? p23 : p01;
-          // rows r, r+1 (even lane: mine = rows 0,1) as (t_even, t_odd) pairs
           const uint32_t lo_even = odd ? (got & 0xffffu) : (mine & 0xffffu);
           const uint32_t lo_odd = odd ? (mine & 0xffffu) : (got & 0xffffu);
           const uint32_t hi_even = odd ? (got >> 16) : (mine >> 16);
           const uint32_t hi_odd = odd ? (mine >> 16) : (got >> 16);
-          const int lrow = GL::row(mi, rg * 4) - GL::wm() * (256 / GL::WM) - half * 64 +
-                           GL::wm() * 64 + (odd ? 2 : 0);
-          const int tcol = GL::col(ni) & ~1;
-          uint8_t* dst = smem + lrow * kPitch + tcol * 2;
+          uint16_t* dst = Gt + (m0 + v0 + (odd ? 2 : 0)) * ldGt + n0 + tcol;
           *reinterpret_cast<uint32_t*>(dst) = lo_even | (lo_odd << 16);
-          *reinterpret_cast<uint32_t*>(dst + kPitch) = hi_even | (hi_odd << 16);
+          *reinterpret_cast<uint32_t*>(dst + ldGt) = hi_even | (hi_odd << 16);
         }
       }
     }
-    __syncthreads();
-    // 128 staged rows x 512 bytes -> Gt rows m0 + wm*128 + half*64 + r
-#pragma unroll
-    for (int q = 0; q < 128 * 32 / GL::kThreads; ++q) {
-      const int c = threadIdx.x + q * GL::kThreads;
-      const int lrow = c >> 5, chunk = c & 31;
-      const int wm = lrow >> 6;
-      const int64_t v = m0 + wm * (256 / GL::WM) + half * 64 + (lrow & 63);
-      const uint4 val = *reinterpret_cast<const uint4*>(smem + lrow * kPitch + chunk * 16);
-      *reinterpret_cast<uint4*>(Gt + v * ldGt + n0 + chunk * 8) = val;
-    }
-    __syncthreads();
-  }
+  };
+  tile_stream<GL>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
 }
 
 // dst[c][r] = src[r][c] for r < R, zero for R <= r < ld_dst (bf16; C % 8 == 0).
@@ -306,82 +340,90 @@ __global__ void __launch_bounds__(256) transpose_bf16_kernel(const uint16_t* __r
   }
 }
 
-// Backward step 2 (direct-load engine): one K half of dH[t][m] = sum_v W[v][m]
-// dz[t][v], reading W transposed ([d][Vp]) so both operands are k-contiguous.
-// Split s writes out + s * split_stride; the halves are added afterwards.
+// Backward step 2: one K half of dH[t][m] = sum_v W[v][m] dz[t][v], reading W
+// transposed ([d][Vp]) so both operands are k-contiguous.  Virtual blocks of
+// split s write out0 (s = 0) or out1 (s = 1); the halves are added afterwards.
 RBP_LOGITS_KERNEL void dhidden_dma_kernel(const uint16_t* __restrict__ Wt,
                                           const uint16_t* __restrict__ G, int64_t Tn, int32_t d,
-                                          int64_t ldG, int64_t k_split, float* __restrict__ out0,
-                                          float* __restrict__ out1, int64_t tiles_m,
-                                          int64_t tiles_n) {
+                                          int64_t ldG, int64_t k_split, int splits,
+                                          float* __restrict__ out0, float* __restrict__ out1,
+                                          int64_t tiles_m, int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
-  const int64_t per_split = tiles_m * tiles_n;
-  const int64_t split = blockIdx.x / per_split;
-  int64_t tm, tn;
-  map_tile(blockIdx.x - split * per_split, tiles_m, tiles_n, kGroupGrad, tm, tn);
-  const int64_t m0 = tm * 256, n0 = tn * 256;
-  const Operand A{Wt, ldG, d, ldG};   // (m = hidden unit, k = vocab)
-  const Operand B{G, ldG, Tn, ldG};   // (n = token, k = vocab)
-  const int64_t k_begin = split * k_split;
-  const int64_t k_end = (k_begin + k_split) < ldG ? (k_begin + k_split) : ldG;
-  f32x16 acc[GL::MI][GL::NI];
-  mainloop<GL>(A, B, m0, n0, k_begin, k_end, smem, acc);
-  float* __restrict__ dH = split == 0 ? out0 : out1;
+  const Operand A{Wt, ldG, d, ldG};  // (m = hidden unit, k = vocab)
+  const Operand B{G, ldG, Tn, ldG};  // (n = token, k = vocab)
+  const int32_t per_split = (int32_t)(tiles_m * tiles_n);
+  auto tile_of = [&](int32_t vid) {
+    const int32_t split = vid >= per_split ? 1 : 0;  // at most two K splits
+    int32_t tm, tn;
+    map_tile(vid - split * per_split, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+    const int32_t kb = split * (int32_t)k_split;
+    const int32_t ke = (kb + (int32_t)k_split) < (int32_t)ldG ? (kb + (int32_t)k_split) : (int32_t)ldG;
+    return Tile{tm * 256, tn * 256, kb, ke};
+  };
+  auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
+    const Tile tile = tile_of(vid);
+    float* __restrict__ dH = tile.k_begin == 0 ? out0 : out1;
 #pragma unroll
-  for (int ni = 0; ni < GL::NI; ++ni) {
-    const int64_t t = n0 + GL::col(ni);
-    if (t >= Tn) continue;
+    for (int ni = 0; ni < GL::NI; ++ni) {
+      const int64_t t = tile.n0 + GL::col(ni);
+      if (t >= Tn) continue;
 #pragma unroll
-    for (int mi = 0; mi < GL::MI; ++mi)
+      for (int mi = 0; mi < GL::MI; ++mi)
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int64_t m = m0 + GL::row(mi, rg * 4);
-        if (m < d)
-          *reinterpret_cast<float4*>(dH + t * d + m) =
-              make_float4(acc[mi][ni][rg * 4 + 0], acc[mi][ni][rg * 4 + 1],
-                          acc[mi][ni][rg * 4 + 2], acc[mi][ni][rg * 4 + 3]);
-      }
-  }
+        for (int rg = 0; rg < 4; ++rg) {
+          const int64_t m = tile.m0 + GL::row(mi, rg * 4);
+          if (m < d)
+            *reinterpret_cast<float4*>(dH + t * d + m) =
+                make_float4(acc[mi][ni][rg * 4 + 0], acc[mi][ni][rg * 4 + 1],
+                            acc[mi][ni][rg * 4 + 2], acc[mi][ni][rg * 4 + 3]);
+        }
+    }
+  };
+  tile_stream<GL>(A, B, (int32_t)(per_split * splits), smem, tile_of, epi);
 }
 
-// Backward step 3 (direct-load engine): dW[v][m] (+)= sum_t H[t][m] dz[t][v],
-// reading both operands transposed (H^T [d][Tc], dz^T [Vp][Tc], k = token).
+// Backward step 3: dW[v][m] (+)= sum_t H[t][m] dz[t][v], reading both operands
+// transposed (H^T [d][Tc], dz^T [Vp][Tc], k = token).
 RBP_LOGITS_KERNEL void dweight_dma_kernel(const uint16_t* __restrict__ Ht,
                                           const uint16_t* __restrict__ Gt, int64_t Tn, int32_t d,
                                           int32_t V, int64_t ldT, float* __restrict__ dW,
                                           int accumulate, int64_t tiles_m, int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
-  int64_t tm, tn;
-  map_tile(blockIdx.x, tiles_m, tiles_n, kGroupGrad, tm, tn);
-  const int64_t m0 = tm * 256, n0 = tn * 256;
-  const Operand A{Ht, ldT, d, ldT};   // (m = hidden unit, k = token)
-  const Operand B{Gt, ldT, V, ldT};   // (n = vocab, k = token)
-  f32x16 acc[GL::MI][GL::NI];
-  mainloop<GL>(A, B, m0, n0, 0, Tn, smem, acc);
+  const Operand A{Ht, ldT, d, ldT};  // (m = hidden unit, k = token)
+  const Operand B{Gt, ldT, V, ldT};  // (n = vocab, k = token)
+  auto tile_of = [&](int32_t vid) {
+    int32_t tm, tn;
+    map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+    return Tile{tm * 256, tn * 256, 0, (int32_t)Tn};
+  };
+  auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
+    const Tile tile = tile_of(vid);
 #pragma unroll
-  for (int ni = 0; ni < GL::NI; ++ni) {
-    const int64_t v = n0 + GL::col(ni);
-    if (v >= V) continue;
+    for (int ni = 0; ni < GL::NI; ++ni) {
+      const int64_t v = tile.n0 + GL::col(ni);
+      if (v >= V) continue;
 #pragma unroll
-    for (int mi = 0; mi < GL::MI; ++mi)
+      for (int mi = 0; mi < GL::MI; ++mi)
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int64_t m = m0 + GL::row(mi, rg * 4);
-        if (m < d) {
-          float4* dst = reinterpret_cast<float4*>(dW + v * d + m);
-          float4 val = make_float4(acc[mi][ni][rg * 4 + 0], acc[mi][ni][rg * 4 + 1],
-                                   acc[mi][ni][rg * 4 + 2], acc[mi][ni][rg * 4 + 3]);
-          if (accumulate) {
-            const float4 o = *dst;
-            val.x += o.x;
-            val.y += o.y;
-            val.z += o.z;
-            val.w += o.w;
+        for (int rg = 0; rg < 4; ++rg) {
+          const int64_t m = tile.m0 + GL::row(mi, rg * 4);
+          if (m < d) {
+            float4* dst = reinterpret_cast<float4*>(dW + v * d + m);
+            float4 val = make_float4(acc[mi][ni][rg * 4 + 0], acc[mi][ni][rg * 4 + 1],
+                                     acc[mi][ni][rg * 4 + 2], acc[mi][ni][rg * 4 + 3]);
+            if (accumulate) {
+              const float4 o = *dst;
+              val.x += o.x;
+              val.y += o.y;
+              val.z += o.z;
+              val.w += o.w;
+            }
+            *dst = val;
           }
-          *dst = val;
         }
-      }
-  }
+    }
+  };
+  tile_stream<GL>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
 }
 
 // a[i] += b[i] (n % 4 == 0), fixed order per element.
@@ -405,6 +447,16 @@ __global__ void __launch_bounds__(256) fill_zero_kernel(float* __restrict__ p, i
 }
 
 int64_t round256(int64_t x) { return (x + 255) / 256 * 256; }
+
+// Compute units of the current device (the persistent products launch one
+// workgroup per CU).
+int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+    n = 256;
+  return n;
+}
 
 }  // namespace
 
@@ -459,7 +511,8 @@ extern "C" int policy_logprob_fwd(const uint16_t* hidden, const uint16_t* W,
   hipStream_t s = rbp::as_stream(stream);
   const int64_t tiles_m = rbp::ceil_div(V, 256), tiles_n = rbp::ceil_div(T, 256);
   float2* part = static_cast<float2*>(ws);
-  hipLaunchKernelGGL(logits_lse_partial_kernel, dim3(tiles_m * tiles_n), dim3(GL::kThreads), 0, s, W,
+  const int64_t grid = rbp::gemm::stream_grid(tiles_m * tiles_n, device_cus());
+  hipLaunchKernelGGL(logits_lse_partial_kernel, dim3(grid), dim3(GL::kThreads), 0, s, W,
                      hidden, T, d, V, tiles_m, tiles_n, part, tiles_m);
   hipLaunchKernelGGL(lse_merge_kernel, dim3(rbp::ceil_div(T, 4)), dim3(256), 0, s, part, tiles_m,
                      tiles_m, hidden, W, tokens, seq_of_token, T, d, V, logp, lse);
@@ -511,21 +564,22 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
   // W^T for the dhidden product (both operands k-contiguous)
   hipLaunchKernelGGL(transpose_bf16_kernel, dim3(Vp / 64, rbp::ceil_div(d, 64)), dim3(256), 0, s,
                      W, (int64_t)V, (int64_t)d, w.Wt, Vp);
+  const int n_cu = device_cus();
   for (int64_t t0 = 0; t0 < T; t0 += Tc) {
     const int64_t Tn = (T - t0) < Tc ? (T - t0) : Tc;
     const int64_t tiles_t = rbp::ceil_div(Tn, 256);
     const uint16_t* Hc = hidden + t0 * d;
-    hipLaunchKernelGGL(grad_logits_kernel, dim3(tiles_v * tiles_t), dim3(GL::kThreads), 0, s, W,
-                       Hc, Tn, d, V, tokens + t0, seq_of_token ? seq_of_token + t0 : nullptr,
+    hipLaunchKernelGGL(grad_logits_kernel, dim3(rbp::gemm::stream_grid(tiles_v * tiles_t, n_cu)),
+                       dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, tokens + t0, seq_of_token ? seq_of_token + t0 : nullptr,
                        lse + t0, dlogp + t0, w.G, Vp, w.Gt, Tc, tiles_v, tiles_t);
-    // dhidden in two K halves when one pass would leave the last round of
-    // workgroups mostly empty
+    // dhidden in two K halves when one pass would give each CU only a few
+    // tiles (the last, partly empty round would then cost a large share)
     const int64_t tiles_dh = tiles_d * tiles_t;
-    const int splits = tiles_dh < 1024 && Vp >= 512 ? 2 : 1;
+    const int splits = tiles_dh < 4 * (int64_t)n_cu && Vp >= 512 ? 2 : 1;
     const int64_t k_split = splits == 2 ? Vp / 2 : Vp;
-    hipLaunchKernelGGL(dhidden_dma_kernel, dim3(tiles_dh * splits), dim3(GL::kThreads), 0, s,
-                       w.Wt, w.G, Tn, d, Vp, k_split, dhidden + t0 * d, w.dh_half, tiles_d,
-                       tiles_t);
+    hipLaunchKernelGGL(dhidden_dma_kernel, dim3(rbp::gemm::stream_grid(tiles_dh * splits, n_cu)),
+                       dim3(GL::kThreads), 0, s, w.Wt, w.G, Tn, d, Vp, k_split, splits,
+                       dhidden + t0 * d, w.dh_half, tiles_d, tiles_t);
     if (splits == 2) {
       const int64_t n4 = Tn * d / 4;
       int64_t blocks = rbp::ceil_div(n4, 256);
@@ -537,8 +591,8 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
     const int64_t T256 = round256(Tn);
     hipLaunchKernelGGL(transpose_bf16_kernel, dim3(T256 / 64, rbp::ceil_div(d, 64)), dim3(256), 0,
                        s, Hc, Tn, (int64_t)d, w.Ht, Tc);
-    hipLaunchKernelGGL(dweight_dma_kernel, dim3(tiles_d * tiles_v), dim3(GL::kThreads), 0, s,
-                       w.Ht, w.Gt, Tn, d, V, Tc, dW, (accumulate_dW || t0 > 0) ? 1 : 0, tiles_d,
+    hipLaunchKernelGGL(dweight_dma_kernel, dim3(rbp::gemm::stream_grid(tiles_d * tiles_v, n_cu)),
+                       dim3(GL::kThreads), 0, s, w.Ht, w.Gt, Tn, d, V, Tc, dW, (accumulate_dW || t0 > 0) ? 1 : 0, tiles_d,
                        tiles_v);
   }
   RBP_CHECK_LAUNCH("policy_logprob_bwd");
