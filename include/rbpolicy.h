@@ -232,9 +232,9 @@ int policy_loss_fwd_bwd(const float* logp, const float* old_logp,
  * ws device: the tokens are processed in chunks of Tc tokens, with Tc the
  * largest multiple of 256 (at most T rounded up to 256) whose
  * rbp_workspace_bytes(RBP_OP_LOGPROB_BWD, Tc, d, V) fits in ws_bytes.  With
- * Vp = V rounded up to 256 it holds dz and dz^T (bf16 [Tc, Vp] each), W^T (bf16
- * [d, Vp]), the chunk's hidden^T (bf16 [d, Tc]) and a split-K partial of
- * dhidden (fp32 [Tc, d]): 11.4 GB for Tc = 16384 at d = 3584, V = 152064.
+ * Vp = V rounded up to 256 it holds dz^T (bf16 [Vp, Tc]) and a split-K
+ * partial of dhidden (fp32 [Tc, d]): 5.2 GB for Tc = 16384 at d = 3584,
+ * V = 152064.
  * Errors: RBP_EINVAL; RBP_EUNSUPPORTED (d % 8 != 0); RBP_EWORKSPACE (not even
  * a 256-token chunk fits).
  */

@@ -15,12 +15,19 @@
 // * Fragments are read one K slice (16) ahead of the MFMAs that use them; the
 //   first slice of step s + 1 is read right after the barrier, while the last
 //   slice of step s (already in registers) multiplies.
+// * An operand is stored either K-major (k contiguous: tile = 256 rows of
+//   128 bytes per K step) or MN-major (m contiguous: tile = 64 K rows of 512
+//   bytes).  MN-major tiles are read with the gfx950 transpose load
+//   (ds_read_b64_tr_b16), which regroups 16-bit elements across lanes so the
+//   MFMA operand comes out k-contiguous per lane without any transpose pass.
 // * The loads are issued with inline assembly and their completion is tracked
 //   by hand (s_waitcnt vmcnt): the compiler's own tracking of LDS-DMA waits for
 //   every outstanding load before each LDS read and would serialize the
 //   pipeline.  Nothing else in these kernels touches M0 or issues vector memory
 //   loads inside the loop, and the loop ends with vmcnt(0).
 #pragma once
+
+#include <type_traits>
 
 #include "gemm_core.h"
 
@@ -43,6 +50,9 @@ __device__ __forceinline__ i32x4 rsrc_words(const void* base, uint32_t bytes) {
 #pragma clang diagnostic ignored "-Winline-asm"
 // 16 bytes per lane from buffer offset `voff` into LDS at lds + 16 * lane.
 __device__ __forceinline__ void dma16(uint32_t lds, uint32_t voff, i32x4 rsrc) {
+  // the resource is wave-uniform; say so where the compiler cannot prove it
+#pragma unroll
+  for (int i = 0; i < 4; ++i) rsrc[i] = __builtin_amdgcn_readfirstlane(rsrc[i]);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
                : "s"(lds), "v"(voff), "s"(rsrc)
@@ -97,11 +107,13 @@ __device__ __forceinline__ void mfma_tiles_interleaved(const bf16x8 (&a)[G::MI],
   }
 }
 
+// ---- K-major operand: LDS tile = 256 rows x 128 bytes (K step 64) ----------
+//
 // Each lane's share of one operand tile's loads.  Load j of a wave moves a
 // 1 KiB block (8 rows x 128 bytes) into LDS; the offsets are relative to the
 // first row of the tile, so they serve every tile of a launch.
 template <class G>
-struct DmaLanes {
+struct KLanes {
   static constexpr int kLoads = 32 / G::kWaves;  // 1 KiB blocks per wave per step
   uint32_t voff[kLoads];
   int kc[kLoads];
@@ -120,15 +132,6 @@ struct DmaLanes {
       voff[j] = (uint32_t)((row * ld + c * 8) * 2);
     }
   }
-  // load j of K step k0 from the tile whose resource is `rsrc` into the LDS
-  // tile at byte address `tile`; columns at or past k_extent read as zero
-  __device__ __forceinline__ void issue(uint32_t tile, i32x4 rsrc, int32_t k0,
-                                        int32_t k_extent, int j) const {
-    const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const bool ok = k0 + kc[j] < k_extent;
-    dma16(tile + (uint32_t)(j * G::kWaves + wave) * 1024u,
-          ok ? voff[j] + (uint32_t)(k0 * 2) : kOutOfRange, rsrc);
-  }
 };
 
 // Buffer resource over the (at most 256) rows of `op` starting at mn0: rows
@@ -139,39 +142,95 @@ __device__ __forceinline__ i32x4 tile_rsrc(const Operand& op, int64_t mn0) {
   return rsrc_words(op.ptr + mn0 * op.ld, (uint32_t)(rows * op.ld * 2));
 }
 
-// Fragment bases for 128-byte rows (gemm_core.h swizzle): slice ks, row block i
-// reads base[((2 ks) ^ (4 (i & 1))) / 2] + 4096 i.
-struct FragBase {
-  uint32_t a[4], b[4];
+// Fragment reads from a K-major tile (gemm_core.h swizzle): slice ks, row
+// block i reads base[((2 ks) ^ (4 (i & 1))) / 2] + 4096 i.
+template <int kCount>
+struct KFrags {
+  uint32_t base[4];
+  __device__ __forceinline__ void init(uint32_t tile_off, int wave_rows) {
+    const int lane = threadIdx.x & 63;
+    const int r = lane & 31;
+    const int t = (lane >> 5) ^ (r & 7) ^ (r >> 3);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      base[j] = tile_off + (uint32_t)(wave_rows * 128 + r * 128 + (((2 * j) ^ t) << 4));
+  }
+  __device__ __forceinline__ void read(const uint8_t* stage, int ks, bf16x8 (&v)[kCount]) const {
+#pragma unroll
+    for (int i = 0; i < kCount; ++i)
+      v[i] = *reinterpret_cast<const bf16x8*>(stage + base[((2 * ks) ^ (4 * (i & 1))) >> 1] +
+                                              4096 * i);
+  }
 };
 
+// ---- MN-major operand: LDS tile = 64 K rows x 512 bytes ---------------------
+//
+// Row r of the tile (K index k0 + r) holds the tile's 256 m as 32 chunks of
+// 16 bytes; logical chunk c sits at physical chunk c ^ (4 (r & 3)), i.e. the
+// four 64-byte quarters of each 256-byte half are rotated by row, so the
+// 8-byte transpose reads of one half-wave (4 K rows x 64 bytes) cover all
+// banks once.  Load j of a wave moves 2 rows (1 KiB); a lane fetches logical
+// chunk c ^ (4 (r & 3)) for physical chunk c = lane % 32.
 template <class G>
-__device__ __forceinline__ FragBase frag_bases() {
-  const int lane = threadIdx.x & 63;
-  const int r = lane & 31;
-  const int t = (lane >> 5) ^ (r & 7) ^ (r >> 3);
-  FragBase f;
+struct MNLanes {
+  static constexpr int kLoads = 32 / G::kWaves;
+  uint32_t voff[kLoads];  // relative to element (k0, m0) of the step
+  int col[kLoads];        // first m of the chunk, relative to m0
+
+  __device__ __forceinline__ void init(int64_t ld) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const uint32_t off = (uint32_t)(r * 128 + (((2 * j) ^ t) << 4));
-    f.a[j] = (uint32_t)(G::wm() * (256 / G::WM) * 128) + off;
-    f.b[j] = (uint32_t)(kTileBytes + G::wn() * (256 / G::WN) * 128) + off;
+    for (int j = 0; j < kLoads; ++j) {
+      const int b = j * G::kWaves + wave;
+      const int r = 2 * b + (lane >> 5);
+      const int c = (lane & 31) ^ ((r & 3) << 2);
+      col[j] = c * 8;
+      voff[j] = (uint32_t)((r * ld + c * 8) * 2);
+    }
   }
-  return f;
+};
+
+// gfx950 transpose load: lane 16 g + i receives, as element e (0..3), the
+// 16-bit value at byte 2 (i % 4) of the 8 bytes addressed by lane
+// 16 g + 4 e + i / 4.
+__device__ __forceinline__ uint64_t lds_read_tr16(const uint8_t* p) {
+  typedef __bf16 bf16x4 __attribute__((__vector_size__(8)));
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const auto* q = reinterpret_cast<const __attribute__((address_space(3))) uint8_t*>(
+      (uint32_t)reinterpret_cast<uintptr_t>(p));
+  const bf16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)q);
+  return __builtin_bit_cast(uint64_t, v);
 }
 
-template <class G>
-__device__ __forceinline__ void read_frags(const uint8_t* stage, const FragBase& f, int ks,
-                                        bf16x8 (&a)[G::MI], bf16x8 (&b)[G::NI]) {
+// Fragment reads from an MN-major tile.  The MFMA operand wants lane l to hold
+// X[m = l % 32][k = 8 (l / 32) .. + 8]; by the transpose-load rule above, lane
+// s must address K row kr = 8 (s / 32) + 4 h + (s % 16) / 4 (h = which half of
+// the 8 k) at m = 16 ((s / 16) % 2) + 4 (s % 4) within the 32-m block.
+template <int kCount>
+struct MNFrags {
+  uint32_t base[kCount];
+  __device__ __forceinline__ void init(uint32_t tile_off, int wave_rows) {
+    const int s = threadIdx.x & 63;
+    const int q = (s & 15) >> 2;  // == kr & 3
+    const int kr = 8 * (s >> 5) + q;
+    const int mb = 2 * (16 * ((s >> 4) & 1) + 4 * (s & 3));  // byte within a 64-byte block
 #pragma unroll
-  for (int i = 0; i < G::MI; ++i)
-    a[i] = *reinterpret_cast<const bf16x8*>(stage + f.a[((2 * ks) ^ (4 * (i & 1))) >> 1] +
-                                            4096 * i);
+    for (int i = 0; i < kCount; ++i)
+      base[i] = tile_off + (uint32_t)(kr * 512 + mb + ((2 * wave_rows + 64 * i) ^ (64 * q)));
+  }
+  __device__ __forceinline__ void read(const uint8_t* stage, int ks, bf16x8 (&v)[kCount]) const {
 #pragma unroll
-  for (int i = 0; i < G::NI; ++i)
-    b[i] = *reinterpret_cast<const bf16x8*>(stage + f.b[((2 * ks) ^ (4 * (i & 1))) >> 1] +
-                                            4096 * i);
-}
+    for (int i = 0; i < kCount; ++i) {
+      const uint8_t* p = stage + base[i] + ks * (16 * 512);
+      const uint64_t lo = lds_read_tr16(p), hi = lds_read_tr16(p + 4 * 512);
+      typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+      v[i] = __builtin_bit_cast(bf16x8, u64x2{lo, hi});
+    }
+  }
+};
+
+template <bool kMN, int kCount>
+using Frags = typename std::conditional<kMN, MNFrags<kCount>, KFrags<kCount>>::type;
 
 // One output tile: rows m0.. of A, rows n0.. of B, K range [k_begin, k_end)
 // (non-empty).  32-bit fields keep the loop's scalar state small.
@@ -183,19 +242,85 @@ __device__ __forceinline__ int32_t k_steps(const Tile& t) {
   return (t.k_end - t.k_begin + kBK - 1) / kBK;
 }
 
-// Load-side view of a tile: buffer resources of its A and B rows and its
-// first K column.  A resource of range 0 (past the end of the stream) makes
-// every load read zeros.
-struct TileRes {
-  i32x4 ra, rb;
-  int32_t kb;
+// Load side of one operand: per-lane offsets, the per-tile view (`Res`) and
+// the issue of load j of K step `step` of a tile into an LDS tile.
+template <class G, bool kMN>
+struct SideLoad;
+
+template <class G>
+struct SideLoad<G, false> {  // K-major
+  KLanes<G> lanes;
+  int32_t k_extent;
+  struct Res {
+    i32x4 rsrc;  // the tile's (at most 256) rows; range 0 past the end of the stream
+    int32_t kb;  // first K column of the tile
+  };
+  __device__ __forceinline__ void init(const Operand& op) {
+    lanes.init(op.ld);
+    k_extent = (int32_t)op.k_extent;
+  }
+  __device__ __forceinline__ Res res(const Operand& op, int32_t mn0, int32_t kb,
+                                     bool valid) const {
+    Res r;
+    r.rsrc = valid ? tile_rsrc(op, mn0) : rsrc_words(op.ptr, 0u);
+    r.kb = kb;
+    return r;
+  }
+  __device__ __forceinline__ void issue(uint32_t tile, const Res& r, int32_t step, int j) const {
+    const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int32_t k0 = r.kb + step * kBK;
+    const bool ok = k0 + lanes.kc[j] < k_extent;  // columns past K read zero
+    dma16(tile + (uint32_t)(j * G::kWaves + wave) * 1024u,
+          ok ? lanes.voff[j] + (uint32_t)(k0 * 2) : kOutOfRange, r.rsrc);
+  }
+};
+
+template <class G>
+struct SideLoad<G, true> {  // MN-major
+  MNLanes<G> lanes;
+  int32_t mn_extent;
+  int64_t ld;
+  struct Res {
+    uint64_t addr;  // byte address of element (k = kb, mn0)
+    int32_t krem;   // K rows left from kb (0 past the end of the stream)
+    int32_t mn0;
+  };
+  int32_t k_extent;
+  __device__ __forceinline__ void init(const Operand& op) {
+    lanes.init(op.ld);
+    mn_extent = (int32_t)op.mn_extent;
+    k_extent = (int32_t)op.k_extent;
+    ld = op.ld;
+  }
+  __device__ __forceinline__ Res res(const Operand& op, int32_t mn0, int32_t kb,
+                                     bool valid) const {
+    Res r;
+    r.addr = reinterpret_cast<uint64_t>(op.ptr + (int64_t)kb * op.ld + mn0);
+    r.krem = valid ? k_extent - kb : 0;
+    r.mn0 = mn0;
+    return r;
+  }
+  __device__ __forceinline__ void issue(uint32_t tile, const Res& r, int32_t step, int j) const {
+    const uint32_t wave = (uint32_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // this step's K rows as one resource: rows past K read zero
+    int32_t rows = r.krem - step * kBK;
+    rows = rows < 0 ? 0 : (rows > kBK ? kBK : rows);
+    const i32x4 rsrc =
+        rsrc_words(reinterpret_cast<const void*>(r.addr + (uint64_t)step * kBK * ld * 2),
+                   (uint32_t)(rows * ld * 2));
+    const bool ok = r.mn0 + lanes.col[j] < mn_extent;  // m past the operand reads zero
+    dma16(tile + (uint32_t)(j * G::kWaves + wave) * 1024u, ok ? lanes.voff[j] : kOutOfRange,
+          rsrc);
+  }
 };
 
 // Persistent tile loop.  This workgroup takes the virtual blocks blockIdx.x,
 // blockIdx.x + gridDim.x, ... below n_vid; tile_of(vid) gives each one's Tile
 // (every tile of a launch has the same number of K steps, nk >= 1) and
-// epi(vid, acc) consumes its finished fp32 accumulators.  Both operands are
-// K-major (k_extent % 8 == 0).
+// epi(vid, acc) consumes its finished fp32 accumulators.  kMNA / kMNB select
+// the layout of A / B: K-major (element (mn, k) at ptr[mn * ld + k]) or
+// MN-major (at ptr[k * ld + mn]); K-major needs k_extent % 8 == 0, MN-major
+// mn_extent % 8 == 0.
 //
 // The K steps of consecutive tiles form one stream through two 64-KiB LDS
 // stages (stream step g in stage g % 2), so the first steps of the next tile
@@ -211,37 +336,35 @@ struct TileRes {
 //   after the last step of a tile: epi(), which may use LDS only at byte
 //   offsets >= kLdsBytes (the stages are in use) and may contain barriers.
 // The load cursor runs two steps ahead of the MFMAs; it holds its tile's
-// resources (cur) and the following tile's (nxt), refreshed once per tile.
-template <class G, class TileFn, class EpiFn>
+// load views (cur) and the following tile's (nxt), refreshed once per tile.
+template <class G, bool kMNA, bool kMNB, class TileFn, class EpiFn>
 __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, int32_t n_vid,
                                             uint8_t* smem, TileFn&& tile_of, EpiFn&& epi) {
   const int32_t stride = (int32_t)gridDim.x;
   const int32_t vid0 = (int32_t)blockIdx.x;
   if (vid0 >= n_vid) return;
-  constexpr int L = DmaLanes<G>::kLoads;
-  DmaLanes<G> la, lb;
-  la.init(A.ld);
-  lb.init(B.ld);
-  const FragBase f = frag_bases<G>();
+  constexpr int L = 32 / G::kWaves;
+  SideLoad<G, kMNA> la;
+  SideLoad<G, kMNB> lb;
+  la.init(A);
+  lb.init(B);
+  Frags<kMNA, G::MI> fa;
+  Frags<kMNB, G::NI> fb;
+  fa.init(0u, G::wm() * (256 / G::WM));
+  fb.init((uint32_t)kTileBytes, G::wn() * (256 / G::WN));
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
   const int32_t nk = k_steps(tile_of(vid0));
-  const int32_t ka = (int32_t)A.k_extent, kbx = (int32_t)B.k_extent;
 
-  auto res_of = [&](int32_t vid) {
-    TileRes r;
-    if (vid < n_vid) {
-      const Tile t = tile_of(vid);
-      r.ra = tile_rsrc(A, t.m0);
-      r.rb = tile_rsrc(B, t.n0);
-      r.kb = t.k_begin;
-    } else {
-      r.ra = rsrc_words(A.ptr, 0u);
-      r.rb = rsrc_words(B.ptr, 0u);
-      r.kb = 0;
-    }
-    return r;
+  struct TileRes {
+    typename SideLoad<G, kMNA>::Res a;
+    typename SideLoad<G, kMNB>::Res b;
   };
-  // load cursor: tile qvid (resources cur), K step qs; nxt = tile qvid + stride
+  auto res_of = [&](int32_t vid) {
+    const bool valid = vid < n_vid;
+    const Tile t = tile_of(valid ? vid : vid0);
+    return TileRes{la.res(A, t.m0, t.k_begin, valid), lb.res(B, t.n0, t.k_begin, valid)};
+  };
+  // load cursor: tile qvid (views cur), K step qs; nxt = tile qvid + stride
   int32_t qvid = vid0, qs = 0;
   TileRes cur = res_of(vid0), nxt = res_of(vid0 + stride);
   auto advance = [&]() {
@@ -251,11 +374,11 @@ __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, 
       cur = nxt;
     }
   };
-  auto issue_a = [&](uint32_t stage, int j) {
-    la.issue(stage, cur.ra, cur.kb + qs * kBK, ka, j);
-  };
-  auto issue_b = [&](uint32_t stage, int j) {
-    lb.issue(stage + kTileBytes, cur.rb, cur.kb + qs * kBK, kbx, j);
+  auto issue_a = [&](uint32_t stage, int j) { la.issue(stage, cur.a, qs, j); };
+  auto issue_b = [&](uint32_t stage, int j) { lb.issue(stage + kTileBytes, cur.b, qs, j); };
+  auto read = [&](const uint8_t* stage, int ks, bf16x8 (&a)[G::MI], bf16x8 (&b)[G::NI]) {
+    fa.read(stage, ks, a);
+    fb.read(stage, ks, b);
   };
 
   // prologue: step 0 landed, step 1's A loads in flight (its B loads are
@@ -280,22 +403,22 @@ __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, 
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.0f;
   bf16x8 a0[G::MI], b0[G::NI], a1[G::MI], b1[G::NI];
-  read_frags<G>(smem, f, 0, a0, b0);
+  read(smem, 0, a0, b0);
   for (uint32_t g = 0;; ++g) {
     const uint8_t* cur_st = smem + (g & 1) * kStageBytes;
     const uint8_t* nxt_st = smem + ((g + 1) & 1) * kStageBytes;
     const uint32_t st_next = lds0 + ((g + 1) & 1) * kStageBytes;
     const uint32_t st_cur = lds0 + (g & 1) * kStageBytes;
-    read_frags<G>(cur_st, f, 1, a1, b1);
+    read(cur_st, 1, a1, b1);
     RBP_FENCE();
     mfma_tiles_interleaved<G>(a0, b0, acc, L, [&](int l) { issue_b(st_next, l); });
     RBP_FENCE();
     advance();
-    read_frags<G>(cur_st, f, 2, a0, b0);
+    read(cur_st, 2, a0, b0);
     RBP_FENCE();
     mfma_tiles<G>(a1, b1, acc);
     RBP_FENCE();
-    read_frags<G>(cur_st, f, 3, a1, b1);
+    read(cur_st, 3, a1, b1);
     RBP_FENCE();
     mfma_tiles<G>(a0, b0, acc);
     RBP_FENCE();
@@ -305,7 +428,7 @@ __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, 
     lds_barrier();
     // unconditional (after the last step it reads a stale stage): a read under
     // a branch would make the compiler wait for it before the MFMAs below
-    read_frags<G>(nxt_st, f, 0, a0, b0);
+    read(nxt_st, 0, a0, b0);
     RBP_FENCE();
     mfma_tiles_interleaved<G>(a1, b1, acc, L, [&](int l) { issue_a(st_cur, l); });
     RBP_FENCE();

@@ -138,7 +138,7 @@ RBP_LOGITS_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
     // lds_ms is next written in the next tile's epilogue, after at least one
     // K step (and its barrier) of that tile
   };
-  tile_stream<GL>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
+  tile_stream<GL, false, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -202,25 +202,51 @@ __global__ void __launch_bounds__(256) lse_merge_kernel(
 }
 
 // Backward step 1: recompute the tile and write dz = dlogp (onehot - p) as
-// bf16, both token-major (G[t][v]) and vocabulary-major (Gt[v][t]).  Masked
-// and padding tokens get dz = 0 (p is evaluated against lse = +inf).  A lane
-// holds four consecutive vocabulary rows of one token: G takes them as one
-// 8-byte store; for Gt, lanes of adjacent tokens swap halves so that each
-// stores 32-bit (token, token + 1) pairs of two rows.
+// bf16, vocabulary-major (Gt[v][t], the layout both later products read).
+// Masked and padding tokens get dz = 0 (p is evaluated against lse = +inf).
+//
+// A lane holds four consecutive vocabulary rows v0..v0+3 of one token.  The
+// four lanes of a quad (tokens t0..t0+3) transpose their 4 x 4 block with two
+// lane exchanges (DPP quad permutes; 16-bit halves regrouped with byte
+// permutes), after which lane j of the quad holds row v0 + j for tokens
+// t0..t0+3: one 8-byte store.  Stores go through a per-tile buffer resource,
+// so every address is a 32-bit offset from the tile's corner.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t quad_xor1(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xf, 0xf, false);  // [1,0,3,2]
+}
+__device__ __forceinline__ uint32_t quad_xor2(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xf, 0xf, false);  // [2,3,0,1]
+}
+// byte permute: selector byte k picks byte k of the result from
+// {hi (bytes 4..7), lo (bytes 0..3)}
+__device__ __forceinline__ uint32_t byte_perm(uint32_t hi, uint32_t lo, uint32_t sel) {
+  return __builtin_amdgcn_perm(hi, lo, sel);
+}
+
 RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
                                           const uint16_t* __restrict__ Hc, int64_t Tn,
                                           int32_t d, int32_t V, const int32_t* __restrict__ tokens,
                                           const int32_t* __restrict__ seq,
                                           const float* __restrict__ lse,
                                           const float* __restrict__ dlogp,
-                                          uint16_t* __restrict__ G, int64_t ldG,
                                           uint16_t* __restrict__ Gt, int64_t ldGt,
                                           int64_t tiles_m, int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const Operand A{W, d, V, d};
   const Operand B{Hc, d, Tn, d};
   const int lane = threadIdx.x & 63;
-  const bool odd = lane & 1;
+  // quad-transpose selectors (see above); j = position in the quad
+  const int j = lane & 3;
+  const bool lo2 = j < 2, ev = (j & 1) == 0;
+  const uint32_t sel_send1 = lo2 ? 0x07060504u : 0x03020100u;  // j < 2 sends rows 2,3
+  const uint32_t sel_pick = lo2 ? 0x03020100u : 0x07060504u;
+  const uint32_t sel_send2 = ev ? 0x07060302u : 0x05040100u;
+  const uint32_t sel_w0 = ev ? 0x05040100u : 0x03020504u;
+  const uint32_t sel_w1 = ev ? 0x07060100u : 0x03020706u;
+  // per-lane byte offsets inside a tile: G row of this lane's token, Gt row
+  // v0 + j at this quad's first token
   auto tile_of = [&](int32_t vid) {
     int32_t tm, tn;
     map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupLogits, tm, tn);
@@ -232,6 +258,9 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
     const int32_t vlim = V - tile.m0;
     const bool full = vlim >= 256;
     const int32_t lim = vlim - GL::row(0, 0);  // as row_off(mi, r) < lim
+    // the tile's 256 x 256 corner of Gt
+    const auto rGt = __builtin_amdgcn_make_buffer_rsrc(Gt + m0 * ldGt + n0, 0,
+                                                       (int)(256 * ldGt * 2), 0x00020000);
     float ls[GL::NI], dl[GL::NI];
     int yrow[GL::NI];
     bool hit[GL::NI];  // some token of this wave's column block has its target in the tile
@@ -254,7 +283,6 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
     for (int mi = 0; mi < GL::MI; ++mi) {
 #pragma unroll
       for (int ni = 0; ni < GL::NI; ++ni) {
-        const int64_t t = n0 + GL::col(ni);
         float g[16];  // p, then dz
 #pragma unroll
         for (int r = 0; r < 16; ++r) g[r] = exp2_hw(fmaf(acc[mi][ni][r], kLog2e, -ls[ni]));
@@ -278,87 +306,54 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
             g[r] = __uint_as_float(__float_as_uint(g[r]) & keep);
           }
         }
-        uint16_t* grow = G + t * ldG + m0;
-        const int tcol = GL::col(ni) & ~1;
+        const uint32_t offGt = (uint32_t)((GL::row(0, 0) + j) * ldGt + (GL::col(ni) - j)) * 2u;
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
-          const int v0 = GL::row(mi, rg * 4);
-          const uint32_t p01 = pack_bf16x2(g[rg * 4 + 0], g[rg * 4 + 1]);
-          const uint32_t p23 = pack_bf16x2(g[rg * 4 + 2], g[rg * 4 + 3]);
-          *reinterpret_cast<uint2*>(grow + v0) = make_uint2(p01, p23);
-          // token-pair exchange: the even lane keeps rows v0, v0 + 1, the odd
-          // lane rows v0 + 2, v0 + 3; each gets its neighbour's value of those
-          const uint32_t give = odd ? p01 : p23;
-          const uint32_t got = (uint32_t)__shfl_xor((int)give, 1, 64);
-          const uint32_t mine = odd ? p23 : p01;
-          const uint32_t lo_even = odd ? (got & 0xffffu) : (mine & 0xffffu);
-          const uint32_t lo_odd = odd ? (mine & 0xffffu) : (got & 0xffffu);
-          const uint32_t hi_even = odd ? (got >> 16) : (mine >> 16);
-          const uint32_t hi_odd = odd ? (mine >> 16) : (got >> 16);
-          uint16_t* dst = Gt + (m0 + v0 + (odd ? 2 : 0)) * ldGt + n0 + tcol;
-          *reinterpret_cast<uint32_t*>(dst) = lo_even | (lo_odd << 16);
-          *reinterpret_cast<uint32_t*>(dst + ldGt) = hi_even | (hi_odd << 16);
+          const int ro = GL::row_off(mi, rg * 4);  // v0 - row(0, 0)
+          const uint32_t P0 = pack_bf16x2(g[rg * 4 + 0], g[rg * 4 + 1]);
+          const uint32_t P1 = pack_bf16x2(g[rg * 4 + 2], g[rg * 4 + 3]);
+          // quad transpose, step 1 (partner j ^ 2): lanes 0, 1 keep rows 0, 1
+          // and get their partner's; lanes 2, 3 keep rows 2, 3.  A / B = this
+          // row pair for tokens (j & 1) and (j & 1) + 2.
+          const uint32_t r1 = quad_xor2(byte_perm(P1, P0, sel_send1));
+          const uint32_t Ah = byte_perm(r1, P0, sel_pick);
+          const uint32_t Bh = byte_perm(P1, r1, sel_pick);
+          // step 2 (partner j ^ 1): even lanes collect the first row of the
+          // pair, odd lanes the second
+          const uint32_t r2 = quad_xor1(byte_perm(Bh, Ah, sel_send2));
+          const uint32_t w0 = byte_perm(r2, Ah, sel_w0);
+          const uint32_t w1 = byte_perm(r2, Bh, sel_w1);
+          __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rGt, offGt,
+                                                (int)(ro * ldGt * 2), 0);
         }
       }
     }
   };
-  tile_stream<GL>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
+  tile_stream<GL, false, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
 }
 
-// dst[c][r] = src[r][c] for r < R, zero for R <= r < ld_dst (bf16; C % 8 == 0).
-// 64 x 64 tiles staged through LDS; 16-byte loads and stores.
-__global__ void __launch_bounds__(256) transpose_bf16_kernel(const uint16_t* __restrict__ src,
-                                                             int64_t R, int64_t C,
-                                                             uint16_t* __restrict__ dst,
-                                                             int64_t ld_dst) {
-  __shared__ uint16_t tile[64][64 + 8];
-  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
-  const int tr = threadIdx.x >> 3, tc = (threadIdx.x & 7) * 8;
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int64_t r = r0 + tr + 32 * i, c = c0 + tc;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (r < R && c < C) v = *reinterpret_cast<const uint4*>(src + r * C + c);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      tile[tr + 32 * i][tc + 2 * q] = (uint16_t)(w[q] & 0xffff);
-      tile[tr + 32 * i][tc + 2 * q + 1] = (uint16_t)(w[q] >> 16);
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int64_t c = c0 + tr + 32 * i, r = r0 + tc;
-    if (c >= C || r >= ld_dst) continue;
-    uint32_t w[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      w[q] = (uint32_t)tile[tc + 2 * q][tr + 32 * i] |
-             ((uint32_t)tile[tc + 2 * q + 1][tr + 32 * i] << 16);
-    *reinterpret_cast<uint4*>(dst + c * ld_dst + r) = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-}
-
-// Backward step 2: one K half of dH[t][m] = sum_v W[v][m] dz[t][v], reading W
-// transposed ([d][Vp]) so both operands are k-contiguous.  Virtual blocks of
-// split s write out0 (s = 0) or out1 (s = 1); the halves are added afterwards.
-RBP_LOGITS_KERNEL void dhidden_dma_kernel(const uint16_t* __restrict__ Wt,
-                                          const uint16_t* __restrict__ G, int64_t Tn, int32_t d,
-                                          int64_t ldG, int64_t k_split, int splits,
-                                          float* __restrict__ out0, float* __restrict__ out1,
-                                          int64_t tiles_m, int64_t tiles_n) {
+// Backward step 2: one K half of dH[t][m] = sum_v W[v][m] dz[t][v], with
+// A = W and B = dz^T both read MN-major (m / t contiguous, k = vocabulary).
+// Virtual blocks of split s write out0 (s = 0) or out1 (s = 1); the halves
+// are added afterwards.
+RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
+                                      const uint16_t* __restrict__ Gt, int64_t ldGt, int64_t Tn,
+                                      int32_t d, int32_t V, int64_t k_split, int splits,
+                                      float* __restrict__ out0, float* __restrict__ out1,
+                                      int64_t tiles_m, int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
-  const Operand A{Wt, ldG, d, ldG};  // (m = hidden unit, k = vocab)
-  const Operand B{G, ldG, Tn, ldG};  // (n = token, k = vocab)
+  const int64_t T256 = (Tn + 255) / 256 * 256;
+  const Operand A{W, d, d, V};          // (m = hidden unit, k = vocab): W[v][m]
+  const Operand B{Gt, ldGt, T256, V};   // (n = token, k = vocab): Gt[v][t]
   const int32_t per_split = (int32_t)(tiles_m * tiles_n);
   auto tile_of = [&](int32_t vid) {
     const int32_t split = vid >= per_split ? 1 : 0;  // at most two K splits
     int32_t tm, tn;
     map_tile(vid - split * per_split, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+    // both splits span k_split columns (uniform step count); columns past V
+    // read as zero
     const int32_t kb = split * (int32_t)k_split;
-    const int32_t ke = (kb + (int32_t)k_split) < (int32_t)ldG ? (kb + (int32_t)k_split) : (int32_t)ldG;
-    return Tile{tm * 256, tn * 256, kb, ke};
+    return Tile{tm * 256, tn * 256, kb, kb + (int32_t)k_split};
   };
   auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
     const Tile tile = tile_of(vid);
@@ -379,18 +374,19 @@ RBP_LOGITS_KERNEL void dhidden_dma_kernel(const uint16_t* __restrict__ Wt,
         }
     }
   };
-  tile_stream<GL>(A, B, (int32_t)(per_split * splits), smem, tile_of, epi);
+  tile_stream<GL, true, true>(A, B, per_split * splits, smem, tile_of, epi);
 }
 
-// Backward step 3: dW[v][m] (+)= sum_t H[t][m] dz[t][v], reading both operands
-// transposed (H^T [d][Tc], dz^T [Vp][Tc], k = token).
-RBP_LOGITS_KERNEL void dweight_dma_kernel(const uint16_t* __restrict__ Ht,
-                                          const uint16_t* __restrict__ Gt, int64_t Tn, int32_t d,
-                                          int32_t V, int64_t ldT, float* __restrict__ dW,
-                                          int accumulate, int64_t tiles_m, int64_t tiles_n) {
+// Backward step 3: dW[v][m] (+)= sum_t H[t][m] dz[t][v], with A = H read
+// MN-major (m contiguous, k = token) and B = dz^T K-major (rows v, k = token).
+RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
+                                      const uint16_t* __restrict__ Gt, int64_t ldGt, int64_t Tn,
+                                      int32_t d, int32_t V, float* __restrict__ dW, int accumulate,
+                                      int64_t tiles_m, int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
-  const Operand A{Ht, ldT, d, ldT};  // (m = hidden unit, k = token)
-  const Operand B{Gt, ldT, V, ldT};  // (n = vocab, k = token)
+  const int64_t T8 = (Tn + 7) / 8 * 8;  // dz^T columns Tn..T8 hold zeros
+  const Operand A{Hc, d, d, Tn};        // (m = hidden unit, k = token): H[t][m]
+  const Operand B{Gt, ldGt, V, T8};     // (n = vocab, k = token): Gt[v][t]
   auto tile_of = [&](int32_t vid) {
     int32_t tm, tn;
     map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
@@ -423,7 +419,7 @@ RBP_LOGITS_KERNEL void dweight_dma_kernel(const uint16_t* __restrict__ Ht,
         }
     }
   };
-  tile_stream<GL>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
+  tile_stream<GL, true, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
 }
 
 // a[i] += b[i] (n % 4 == 0), fixed order per element.
@@ -466,25 +462,19 @@ size_t rbp::logprob_fwd_ws(int64_t T, int32_t V) {
 }
 
 namespace {
-// Backward workspace carving: dz [Tc][Vp] bf16, W^T [d][Vp] bf16, the second
-// dhidden K half [Tc][d] fp32, dz^T [Vp][Tc] bf16, H^T [d][Tc] bf16.
+// Backward workspace carving: dz^T [Vp][T256] bf16, then the second dhidden
+// K half [T256][d] fp32.
 struct BwdWs {
-  uint16_t* G;
-  uint16_t* Wt;
-  float* dh_half;
   uint16_t* Gt;
-  uint16_t* Ht;
+  float* dh_half;
   size_t bytes;
 };
 BwdWs carve_bwd(void* base, int64_t Tc, int32_t d, int32_t V) {
   rbp::WsCarver c(base);
   const int64_t T256 = round256(Tc < 1 ? 1 : Tc), Vp = round256(V);
   BwdWs w;
-  w.G = c.take<uint16_t>((size_t)T256 * (size_t)Vp);
-  w.Wt = c.take<uint16_t>((size_t)d * (size_t)Vp);
-  w.dh_half = c.take<float>((size_t)T256 * (size_t)d);
   w.Gt = c.take<uint16_t>((size_t)Vp * (size_t)T256);
-  w.Ht = c.take<uint16_t>((size_t)d * (size_t)T256);
+  w.dh_half = c.take<float>((size_t)T256 * (size_t)d);
   w.bytes = rbp::align_up(c.used, 256);
   return w;
 }
@@ -548,7 +538,9 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
   // largest chunk (multiple of 256 tokens) whose workspace fits
   int64_t Tc = 0;
   if (ws) {
-    int64_t lo = 256, hi = round256(T);
+    // chunks of at most 2^21 tokens keep every per-tile byte range of dz^T
+    // (256 rows x Tc x 2 bytes) inside a 32-bit buffer offset
+    int64_t lo = 256, hi = round256(T) < (int64_t(1) << 21) ? round256(T) : (int64_t(1) << 21);
     if (rbp::logprob_bwd_ws(lo, d, V) <= ws_bytes) {
       while (lo < hi) {  // largest multiple of 256 in [lo, hi] that fits
         const int64_t mid = (lo + hi + 256) / 512 * 256;
@@ -561,24 +553,22 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
               "policy_logprob_bwd: workspace of %zu bytes holds no 256-token chunk (needs %zu)",
               ws_bytes, rbp::logprob_bwd_ws(256, d, V));
   const BwdWs w = carve_bwd(ws, Tc, d, V);
-  // W^T for the dhidden product (both operands k-contiguous)
-  hipLaunchKernelGGL(transpose_bf16_kernel, dim3(Vp / 64, rbp::ceil_div(d, 64)), dim3(256), 0, s,
-                     W, (int64_t)V, (int64_t)d, w.Wt, Vp);
   const int n_cu = device_cus();
   for (int64_t t0 = 0; t0 < T; t0 += Tc) {
     const int64_t Tn = (T - t0) < Tc ? (T - t0) : Tc;
     const int64_t tiles_t = rbp::ceil_div(Tn, 256);
     const uint16_t* Hc = hidden + t0 * d;
     hipLaunchKernelGGL(grad_logits_kernel, dim3(rbp::gemm::stream_grid(tiles_v * tiles_t, n_cu)),
-                       dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, tokens + t0, seq_of_token ? seq_of_token + t0 : nullptr,
-                       lse + t0, dlogp + t0, w.G, Vp, w.Gt, Tc, tiles_v, tiles_t);
+                       dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, tokens + t0,
+                       seq_of_token ? seq_of_token + t0 : nullptr, lse + t0, dlogp + t0, w.Gt, Tc,
+                       tiles_v, tiles_t);
     // dhidden in two K halves when one pass would give each CU only a few
     // tiles (the last, partly empty round would then cost a large share)
     const int64_t tiles_dh = tiles_d * tiles_t;
-    const int splits = tiles_dh < 4 * (int64_t)n_cu && Vp >= 512 ? 2 : 1;
-    const int64_t k_split = splits == 2 ? Vp / 2 : Vp;
-    hipLaunchKernelGGL(dhidden_dma_kernel, dim3(rbp::gemm::stream_grid(tiles_dh * splits, n_cu)),
-                       dim3(GL::kThreads), 0, s, w.Wt, w.G, Tn, d, Vp, k_split, splits,
+    const int splits = tiles_dh < 4 * (int64_t)n_cu && V >= 512 ? 2 : 1;
+    const int64_t k_split = splits == 2 ? (rbp::ceil_div(V, 2) + 63) / 64 * 64 : V;
+    hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(tiles_dh * splits, n_cu)),
+                       dim3(GL::kThreads), 0, s, W, w.Gt, Tc, Tn, d, V, k_split, splits,
                        dhidden + t0 * d, w.dh_half, tiles_d, tiles_t);
     if (splits == 2) {
       const int64_t n4 = Tn * d / 4;
@@ -587,13 +577,9 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
       hipLaunchKernelGGL(add_f32_kernel, dim3(blocks), dim3(256), 0, s, dhidden + t0 * d,
                          w.dh_half, n4);
     }
-    // dW on the direct-load engine: token-contiguous copies of dz and H
-    const int64_t T256 = round256(Tn);
-    hipLaunchKernelGGL(transpose_bf16_kernel, dim3(T256 / 64, rbp::ceil_div(d, 64)), dim3(256), 0,
-                       s, Hc, Tn, (int64_t)d, w.Ht, Tc);
-    hipLaunchKernelGGL(dweight_dma_kernel, dim3(rbp::gemm::stream_grid(tiles_d * tiles_v, n_cu)),
-                       dim3(GL::kThreads), 0, s, w.Ht, w.Gt, Tn, d, V, Tc, dW, (accumulate_dW || t0 > 0) ? 1 : 0, tiles_d,
-                       tiles_v);
+    hipLaunchKernelGGL(dweight_kernel, dim3(rbp::gemm::stream_grid(tiles_d * tiles_v, n_cu)),
+                       dim3(GL::kThreads), 0, s, Hc, w.Gt, Tc, Tn, d, V, dW,
+                       (accumulate_dW || t0 > 0) ? 1 : 0, tiles_d, tiles_v);
   }
   RBP_CHECK_LAUNCH("policy_logprob_bwd");
   return RBP_OK;

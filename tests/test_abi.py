@@ -64,12 +64,12 @@ def test_status_strings_and_workspace_sizes():
     assert lib.rbp_status_string(-3) == b"workspace too small"
     assert lib.rbp_status_string(12345) == b"unknown status"
     assert lib.rbp_workspace_bytes(99, 10, 8, 8) == 0
-    # backward workspace: dz bf16 [Tc, Vp], W^T bf16 [d, Vp], dhidden half fp32 [Tc, d]
-    # (Tc and Vp rounded up to 256)
+    # backward workspace: dz^T bf16 [Vp, Tc] and the second dhidden K half
+    # fp32 [Tc, d] (Tc and Vp rounded up to 256)
     assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_BWD, 16384, 3584, 152064) == \
-        16384 * 152064 * 2 + 3584 * 152064 * 2 + 16384 * 3584 * 4 + 152064 * 16384 * 2 + 3584 * 16384 * 2
+        152064 * 16384 * 2 + 16384 * 3584 * 4
     assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_BWD, 1, 64, 1000) == \
-        256 * 1024 * 2 + 64 * 1024 * 2 + 256 * 64 * 4 + 1024 * 256 * 2 + 64 * 256 * 2
+        1024 * 256 * 2 + 256 * 64 * 4
     # forward workspace: one (max, sum) pair per token and 256-wide vocab tile
     assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_FWD, 100, 64, 513) == \
         ((100 * 3 * 8 + 255) // 256) * 256
