@@ -62,6 +62,58 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
+// (a & mask) | (b & ~mask) with mask = all ones where x < 0: written as two
+// vector bit instructions in assembly, because the compiler would otherwise
+// turn the sign test into a compare whose lane mask lives in scalar registers
+// (64 of them live at once overflow the scalar file); volatile so that the
+// masked values are recomputed where used rather than kept live.
+__device__ __forceinline__ uint32_t select_neg(int32_t x, uint32_t a, uint32_t b) {
+  uint32_t m, r;
+  asm volatile("v_ashrrev_i32 %0, 31, %1" : "=v"(m) : "v"(x));
+  asm volatile("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(a), "v"(b));
+  return r;
+}
+
+// acc, or -inf where the row is past the vocabulary (row_off >= lim): mask
+// arithmetic rather than compares, whose masks would pile up in scalar
+// registers.
+template <bool kFull>
+__device__ __forceinline__ float logit_or_ninf(float v, int off, int32_t lim) {
+  if constexpr (kFull) return v;
+  return __uint_as_float(select_neg(off - lim, __float_as_uint(v), 0xff800000u));
+}
+
+// Per token column of this wave's 128 x 64 block: max and sum exp(z - max)
+// over the lane pair's rows (lanes l and l + 32 hold the same column).
+template <bool kFull>
+__device__ __forceinline__ void column_stats(const f32x16 (&acc)[GL::MI][GL::NI], int32_t lim,
+                                             float (&mx)[GL::NI], float (&sum)[GL::NI]) {
+#pragma unroll
+  for (int ni = 0; ni < GL::NI; ++ni) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int mi = 0; mi < GL::MI; ++mi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        m = fmaxf(m, logit_or_ninf<kFull>(acc[mi][ni][r], GL::row_off(mi, r), lim));
+    m = fmaxf(m, __shfl_xor(m, 32, 64));
+    // a column with no real row (tail tile) has m = -inf: offset 0 keeps the
+    // exponentials at exp(-inf) = 0 instead of NaN
+    const float mb = (kFull || m != -INFINITY) ? m * kLog2e : 0.0f;
+    float s4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int mi = 0; mi < GL::MI; ++mi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        s4[r & 3] += exp2_hw(
+            fmaf(logit_or_ninf<kFull>(acc[mi][ni][r], GL::row_off(mi, r), lim), kLog2e, -mb));
+    float sm = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+    sm += __shfl_xor(sm, 32, 64);
+    mx[ni] = m;
+    sum[ni] = sm;
+  }
+}
+
 // Forward: per 256 x 256 tile, the partial (max, sum exp) of each token
 // column over the tile's 256 vocabulary rows.
 RBP_LOGITS_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
@@ -83,43 +135,14 @@ RBP_LOGITS_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
   auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
     const Tile tile = tile_of(vid);
     const int32_t vlim = V - tile.m0;
-    if (vlim < 256) {  // last vocabulary tile: rows past V take no part
-      const int32_t lim = vlim - GL::row(0, 0);  // row(mi, r) < V  <=>  row_off(mi, r) < lim
+    float mx[GL::NI], sum[GL::NI];
+    if (vlim >= 256)
+      column_stats<true>(acc, 0, mx, sum);
+    else  // last vocabulary tile: rows past V take no part
+      column_stats<false>(acc, vlim - GL::row(0, 0), mx, sum);
 #pragma unroll
-      for (int mi = 0; mi < GL::MI; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < GL::NI; ++ni)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            // all ones where the row is real (mask arithmetic, not compares:
-            // 128 live compare masks would overflow the scalar registers)
-            const uint32_t keep = (uint32_t)((GL::row_off(mi, r) - lim) >> 31);
-            acc[mi][ni][r] = __uint_as_float((__float_as_uint(acc[mi][ni][r]) & keep) |
-                                             (0xff800000u & ~keep));
-          }
-    }
-#pragma unroll
-    for (int ni = 0; ni < GL::NI; ++ni) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int mi = 0; mi < GL::MI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[mi][ni][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      float sum = 0.0f;
-      if (mx != -INFINITY) {
-        const float mb = mx * kLog2e;
-        float s4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int mi = 0; mi < GL::MI; ++mi)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            s4[r & 3] += exp2_hw(fmaf(acc[mi][ni][r], kLog2e, -mb));
-        sum = (s4[0] + s4[1]) + (s4[2] + s4[3]);
-      }
-      sum += __shfl_xor(sum, 32, 64);
-      if (lane < 32) lds_ms[GL::wm() * 256 + GL::col(ni)] = make_float2(mx, sum);
-    }
+    for (int ni = 0; ni < GL::NI; ++ni)
+      if (lane < 32) lds_ms[GL::wm() * 256 + GL::col(ni)] = make_float2(mx[ni], sum[ni]);
     __syncthreads();
     if (threadIdx.x < 256) {
       const int col = threadIdx.x;
@@ -152,6 +175,25 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// h . w over d bf16 elements (d % 8 == 0), one wave cooperating; every lane
+// returns the full sum.
+__device__ __forceinline__ float dot_bf16_wave(const uint16_t* __restrict__ h,
+                                               const uint16_t* __restrict__ w, int32_t d,
+                                               int lane) {
+  float z = 0.0f;
+  for (int c = lane; c < d / 8; c += 64) {
+    const uint4 hv = *reinterpret_cast<const uint4*>(h + c * 8);
+    const uint4 wv = *reinterpret_cast<const uint4*>(w + c * 8);
+    const uint32_t hh[4] = {hv.x, hv.y, hv.z, hv.w}, ww[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      z = fmaf(bf16_to_f32((uint16_t)(hh[q] & 0xffff)), bf16_to_f32((uint16_t)(ww[q] & 0xffff)), z);
+      z = fmaf(bf16_to_f32((uint16_t)(hh[q] >> 16)), bf16_to_f32((uint16_t)(ww[q] >> 16)), z);
+    }
+  }
+  return wave_sum(z);
+}
+
 // One wave per token: merge the partials into lse, dot h_t . W_{y_t}.
 __global__ void __launch_bounds__(256) lse_merge_kernel(
     const float2* __restrict__ part, int64_t ld_part, int64_t n_part,
@@ -180,20 +222,7 @@ __global__ void __launch_bounds__(256) lse_merge_kernel(
   S = wave_sum(S);
   const int32_t y = tokens[t];
   const bool y_ok = y >= 0 && y < V;
-  const uint16_t* h = H + t * d;
-  const uint16_t* w = W + (int64_t)(y_ok ? y : 0) * d;
-  float z = 0.0f;
-  for (int c = lane; c < d / 8; c += 64) {
-    const uint4 hv = *reinterpret_cast<const uint4*>(h + c * 8);
-    const uint4 wv = *reinterpret_cast<const uint4*>(w + c * 8);
-    const uint32_t hh[4] = {hv.x, hv.y, hv.z, hv.w}, ww[4] = {wv.x, wv.y, wv.z, wv.w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      z = fmaf(bf16_to_f32((uint16_t)(hh[q] & 0xffff)), bf16_to_f32((uint16_t)(ww[q] & 0xffff)), z);
-      z = fmaf(bf16_to_f32((uint16_t)(hh[q] >> 16)), bf16_to_f32((uint16_t)(ww[q] >> 16)), z);
-    }
-  }
-  z = wave_sum(z);
+  const float z = dot_bf16_wave(H + t * d, W + (int64_t)(y_ok ? y : 0) * d, d, lane);
   if (lane == 0) {
     const float l = M + logf(S);
     lse[t] = l;
@@ -203,14 +232,17 @@ __global__ void __launch_bounds__(256) lse_merge_kernel(
 
 // Backward step 1: recompute the tile and write dz = dlogp (onehot - p) as
 // bf16, vocabulary-major (Gt[v][t], the layout both later products read).
-// Masked and padding tokens get dz = 0 (p is evaluated against lse = +inf).
+// The tile pass writes -dlogp_t p_{t,v} everywhere; the one target entry of
+// each token is then overwritten by target_dz_kernel.  Masked and padding
+// tokens get dz = 0 (p is evaluated against lse = +inf).
 //
 // A lane holds four consecutive vocabulary rows v0..v0+3 of one token.  The
 // four lanes of a quad (tokens t0..t0+3) transpose their 4 x 4 block with two
 // lane exchanges (DPP quad permutes; 16-bit halves regrouped with byte
 // permutes), after which lane j of the quad holds row v0 + j for tokens
-// t0..t0+3: one 8-byte store.  Stores go through a per-tile buffer resource,
-// so every address is a 32-bit offset from the tile's corner.
+// t0..t0+3: one 8-byte store (see dz_rows for the grouping into whole cache
+// lines).  Stores go through a per-tile buffer resource, so every address is
+// a 32-bit offset from the tile's corner.
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint32_t quad_xor1(uint32_t v) {
@@ -225,10 +257,92 @@ __device__ __forceinline__ uint32_t byte_perm(uint32_t hi, uint32_t lo, uint32_t
   return __builtin_amdgcn_perm(hi, lo, sel);
 }
 
+// Selectors of the quad transpose for lane position j = lane % 4.
+struct QuadSel {
+  uint32_t send1, pick, send2, w0, w1;
+  __device__ __forceinline__ QuadSel() {
+    const int j = threadIdx.x & 3;
+    const bool lo2 = j < 2, ev = (j & 1) == 0;
+    send1 = lo2 ? 0x07060504u : 0x03020100u;  // lanes 0, 1 send rows 2, 3
+    pick = lo2 ? 0x03020100u : 0x07060504u;
+    send2 = ev ? 0x07060302u : 0x05040100u;
+    w0 = ev ? 0x05040100u : 0x03020504u;
+    w1 = ev ? 0x07060100u : 0x03020706u;
+  }
+};
+
+// Cache policy of the dz^T stores: non-temporal.  32 tiles per XCD write 4 MB
+// per round -- the whole L2 -- and, cached normally, would evict the operand
+// rows the next tiles share (measured: 1.1 ms of 15.5 at T=16384, V=152064).
+constexpr int kStreamStore = 2;
+
+// -dl p -> bf16 for four consecutive rows of one token, packed in pairs.
+template <bool kFull>
+__device__ __forceinline__ void dz_pack(const f32x16& acc, float ls, float dl, int mi, int rg,
+                                        int32_t lim, uint32_t& P0, uint32_t& P1) {
+  float g[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    g[i] = -dl * exp2_hw(fmaf(acc[rg * 4 + i], kLog2e, -ls));
+    if constexpr (!kFull)  // rows past the vocabulary hold zeros
+      g[i] = __uint_as_float(select_neg(GL::row_off(mi, rg * 4 + i) - lim,
+                                        __float_as_uint(g[i]), 0u));
+  }
+  P0 = pack_bf16x2(g[0], g[1]);
+  P1 = pack_bf16x2(g[2], g[3]);
+}
+
+// 4 x 4 transpose inside each lane quad: in, lane j holds rows r..r+3 of
+// token t0 + j as (P0 = rows r, r+1; P1 = rows r+2, r+3); out, row r + j of
+// tokens t0..t0+3 as (w0 = tokens 0, 1; w1 = tokens 2, 3).
+__device__ __forceinline__ void quad_transpose(uint32_t P0, uint32_t P1, const QuadSel& qs,
+                                               uint32_t& w0, uint32_t& w1) {
+  // step 1 (partner j ^ 2): lanes 0, 1 keep rows r, r+1 and get their
+  // partner's; lanes 2, 3 keep rows r+2, r+3.  A / B = this row pair for
+  // tokens (j & 1) and (j & 1) + 2.
+  const uint32_t r1 = quad_xor2(byte_perm(P1, P0, qs.send1));
+  const uint32_t Ah = byte_perm(r1, P0, qs.pick);
+  const uint32_t Bh = byte_perm(P1, r1, qs.pick);
+  // step 2 (partner j ^ 1): even lanes collect the first row of the pair,
+  // odd lanes the second
+  const uint32_t r2 = quad_xor1(byte_perm(Bh, Ah, qs.send2));
+  w0 = byte_perm(r2, Ah, qs.w0);
+  w1 = byte_perm(r2, Bh, qs.w1);
+}
+
+// One 32-row block of both 32-token column blocks of a wave (NI == 2).
+// Lanes 0..31 hold rows 0..3 (+8 rg) of their token, lanes 32..63 rows 4..7;
+// a lane-half swap (v_permlane32_swap) first regroups them so that lanes
+// 0..31 hold the first column block and lanes 32..63 the second, for the
+// same four rows: each store then writes 4 rows x 128 contiguous bytes, whole
+// cache lines.
+template <bool kFull>
+__device__ __forceinline__ void dz_rows(const f32x16 (&acc)[GL::MI][GL::NI], const float (&ls)[2],
+                                        const float (&dl)[2], int mi, int32_t lim,
+                                        const QuadSel& qs, __amdgpu_buffer_rsrc_t rGt,
+                                        uint32_t off, int64_t ldGt) {
+  static_assert(GL::NI == 2, "two column blocks per wave");
+#pragma unroll
+  for (int rg = 0; rg < 4; ++rg) {
+    uint32_t X0, X1, Y0, Y1;  // column block 0 / 1, rows (0,1) / (2,3) of the lane's half
+    dz_pack<kFull>(acc[mi][0], ls[0], dl[0], mi, rg, lim, X0, X1);
+    dz_pack<kFull>(acc[mi][1], ls[1], dl[1], mi, rg, lim, Y0, Y1);
+    const auto s0 = __builtin_amdgcn_permlane32_swap(X0, Y0, false, false);
+    const auto s1 = __builtin_amdgcn_permlane32_swap(X1, Y1, false, false);
+    // s0[0], s1[0]: rows 0..3 of the group; s0[1], s1[1]: rows 4..7
+    uint32_t w0, w1;
+    const int ro = mi * 32 + rg * 8;  // first row of the 8-row group within the wave's block
+    quad_transpose(s0[0], s1[0], qs, w0, w1);
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rGt, off, (int)(ro * ldGt * 2), kStreamStore);
+    quad_transpose(s0[1], s1[1], qs, w0, w1);
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rGt, off, (int)((ro + 4) * ldGt * 2),
+                                          kStreamStore);
+  }
+}
+
 RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
                                           const uint16_t* __restrict__ Hc, int64_t Tn,
-                                          int32_t d, int32_t V, const int32_t* __restrict__ tokens,
-                                          const int32_t* __restrict__ seq,
+                                          int32_t d, int32_t V, const int32_t* __restrict__ seq,
                                           const float* __restrict__ lse,
                                           const float* __restrict__ dlogp,
                                           uint16_t* __restrict__ Gt, int64_t ldGt,
@@ -236,100 +350,72 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const Operand A{W, d, V, d};
   const Operand B{Hc, d, Tn, d};
-  const int lane = threadIdx.x & 63;
-  // quad-transpose selectors (see above); j = position in the quad
-  const int j = lane & 3;
-  const bool lo2 = j < 2, ev = (j & 1) == 0;
-  const uint32_t sel_send1 = lo2 ? 0x07060504u : 0x03020100u;  // j < 2 sends rows 2,3
-  const uint32_t sel_pick = lo2 ? 0x03020100u : 0x07060504u;
-  const uint32_t sel_send2 = ev ? 0x07060302u : 0x05040100u;
-  const uint32_t sel_w0 = ev ? 0x05040100u : 0x03020504u;
-  const uint32_t sel_w1 = ev ? 0x07060100u : 0x03020706u;
-  // per-lane byte offsets inside a tile: G row of this lane's token, Gt row
-  // v0 + j at this quad's first token
+  const QuadSel qs;
+  const int j = threadIdx.x & 3;
   auto tile_of = [&](int32_t vid) {
     int32_t tm, tn;
     map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupLogits, tm, tn);
     return Tile{tm * 256, tn * 256, 0, d};
   };
-  auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
+  // lse * log2 e and dlogp of this lane's token columns, loaded one tile
+  // ahead (issued after an epilogue, consumed at the next one)
+  float ls[GL::NI], dl[GL::NI];
+  auto load_token_terms = [&](int32_t vid) {
     const Tile tile = tile_of(vid);
-    const int64_t m0 = tile.m0, n0 = tile.n0;
-    const int32_t vlim = V - tile.m0;
-    const bool full = vlim >= 256;
-    const int32_t lim = vlim - GL::row(0, 0);  // as row_off(mi, r) < lim
-    // the tile's 256 x 256 corner of Gt
-    const auto rGt = __builtin_amdgcn_make_buffer_rsrc(Gt + m0 * ldGt + n0, 0,
-                                                       (int)(256 * ldGt * 2), 0x00020000);
-    float ls[GL::NI], dl[GL::NI];
-    int yrow[GL::NI];
-    bool hit[GL::NI];  // some token of this wave's column block has its target in the tile
 #pragma unroll
     for (int ni = 0; ni < GL::NI; ++ni) {
-      const int64_t t = n0 + GL::col(ni);
-      ls[ni] = INFINITY;
-      dl[ni] = 0.0f;
-      int64_t y = -1;
-      if (t < Tn && (seq == nullptr || seq[t] >= 0)) {
-        ls[ni] = lse[t] * kLog2e;
-        dl[ni] = dlogp[t];
-        y = (int64_t)tokens[t] - m0;
-      }
-      const bool in_tile = y >= 0 && y < 256;
-      yrow[ni] = in_tile ? (int)y - GL::row(0, 0) : -1000;  // relative to row(0, 0)
-      hit[ni] = __any(in_tile);
-    }
-#pragma unroll
-    for (int mi = 0; mi < GL::MI; ++mi) {
-#pragma unroll
-      for (int ni = 0; ni < GL::NI; ++ni) {
-        float g[16];  // p, then dz
-#pragma unroll
-        for (int r = 0; r < 16; ++r) g[r] = exp2_hw(fmaf(acc[mi][ni][r], kLog2e, -ls[ni]));
-        if (hit[ni]) {  // wave-uniform: rare, only here is the one-hot term tested
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            // dl where the row is the target, else 0 (mask arithmetic rather
-            // than compares, which would pile up in scalar registers)
-            const int32_t diff = GL::row_off(mi, r) - yrow[ni];
-            const uint32_t is_y = ~(uint32_t)((diff | -diff) >> 31);
-            g[r] = fmaf(-dl[ni], g[r], __uint_as_float(__float_as_uint(dl[ni]) & is_y));
-          }
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) g[r] = -dl[ni] * g[r];
-        }
-        if (!full) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const uint32_t keep = (uint32_t)((GL::row_off(mi, r) - lim) >> 31);
-            g[r] = __uint_as_float(__float_as_uint(g[r]) & keep);
-          }
-        }
-        const uint32_t offGt = (uint32_t)((GL::row(0, 0) + j) * ldGt + (GL::col(ni) - j)) * 2u;
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-          const int ro = GL::row_off(mi, rg * 4);  // v0 - row(0, 0)
-          const uint32_t P0 = pack_bf16x2(g[rg * 4 + 0], g[rg * 4 + 1]);
-          const uint32_t P1 = pack_bf16x2(g[rg * 4 + 2], g[rg * 4 + 3]);
-          // quad transpose, step 1 (partner j ^ 2): lanes 0, 1 keep rows 0, 1
-          // and get their partner's; lanes 2, 3 keep rows 2, 3.  A / B = this
-          // row pair for tokens (j & 1) and (j & 1) + 2.
-          const uint32_t r1 = quad_xor2(byte_perm(P1, P0, sel_send1));
-          const uint32_t Ah = byte_perm(r1, P0, sel_pick);
-          const uint32_t Bh = byte_perm(P1, r1, sel_pick);
-          // step 2 (partner j ^ 1): even lanes collect the first row of the
-          // pair, odd lanes the second
-          const uint32_t r2 = quad_xor1(byte_perm(Bh, Ah, sel_send2));
-          const uint32_t w0 = byte_perm(r2, Ah, sel_w0);
-          const uint32_t w1 = byte_perm(r2, Bh, sel_w1);
-          __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rGt, offGt,
-                                                (int)(ro * ldGt * 2), 0);
-        }
-      }
+      const int64_t t = tile.n0 + GL::col(ni);
+      const bool valid = t < Tn && (seq == nullptr || seq[t] >= 0);
+      ls[ni] = valid ? lse[t] * kLog2e : INFINITY;
+      dl[ni] = valid ? dlogp[t] : 0.0f;
     }
   };
-  tile_stream<GL, false, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
+  load_token_terms((int32_t)blockIdx.x);
+  const int32_t n_vid = (int32_t)(tiles_m * tiles_n);
+  auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
+    const Tile tile = tile_of(vid);
+    const int32_t vlim = V - tile.m0;
+    const int32_t lim = vlim - GL::row(0, 0);  // as row_off(mi, r) < lim
+    // the tile's 256 x 256 corner of Gt
+    const auto rGt = __builtin_amdgcn_make_buffer_rsrc(Gt + (int64_t)tile.m0 * ldGt + tile.n0, 0,
+                                                       (int)(256 * ldGt * 2), 0x00020000);
+    // this lane's store: row (wave's first row) + j, tokens (wave's first
+    // token) + 32 (lane / 32) + 4 (quad) .. + 3
+    const int lane = threadIdx.x & 63;
+    const uint32_t off =
+        (uint32_t)((GL::wm() * (256 / GL::WM) + j) * ldGt + GL::wn() * (256 / GL::WN) +
+                   32 * (lane >> 5) + ((lane & 31) - j)) * 2u;
+#pragma unroll
+    for (int mi = 0; mi < GL::MI; ++mi) {
+      if (vlim >= 256)
+        dz_rows<true>(acc, ls, dl, mi, lim, qs, rGt, off, ldGt);
+      else
+        dz_rows<false>(acc, ls, dl, mi, lim, qs, rGt, off, ldGt);
+    }
+    if (vid + (int32_t)gridDim.x < n_vid) load_token_terms(vid + (int32_t)gridDim.x);
+  };
+  tile_stream<GL, false, false>(A, B, n_vid, smem, tile_of, epi);
+}
+
+// Backward step 1b, after the tile pass: the target entry of each valid
+// token, dz_{t,y_t} = dlogp_t (1 - exp(z_{t,y_t} - lse_t)), with the target
+// logit as one fp32 dot product h_t . W_{y_t}.  One wave per token.
+__global__ void __launch_bounds__(256) target_dz_kernel(
+    const uint16_t* __restrict__ Hc, const uint16_t* __restrict__ W,
+    const int32_t* __restrict__ tokens, const int32_t* __restrict__ seq,
+    const float* __restrict__ lse, const float* __restrict__ dlogp, int64_t Tn, int32_t d,
+    int32_t V, uint16_t* __restrict__ Gt, int64_t ldGt) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= Tn || (seq != nullptr && seq[t] < 0)) return;
+  const int32_t y = tokens[t];
+  if (y < 0 || y >= V) return;
+  const float z = dot_bf16_wave(Hc + t * d, W + (int64_t)y * d, d, lane);
+  if (lane == 0) {
+    const float p = exp2_hw((z - lse[t]) * kLog2e);
+    const __bf16 g = (__bf16)(dlogp[t] * (1.0f - p));
+    Gt[(int64_t)y * ldGt + t] = __builtin_bit_cast(uint16_t, g);
+  }
 }
 
 // Backward step 2: one K half of dH[t][m] = sum_v W[v][m] dz[t][v], with
@@ -559,9 +645,12 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
     const int64_t tiles_t = rbp::ceil_div(Tn, 256);
     const uint16_t* Hc = hidden + t0 * d;
     hipLaunchKernelGGL(grad_logits_kernel, dim3(rbp::gemm::stream_grid(tiles_v * tiles_t, n_cu)),
-                       dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, tokens + t0,
-                       seq_of_token ? seq_of_token + t0 : nullptr, lse + t0, dlogp + t0, w.Gt, Tc,
-                       tiles_v, tiles_t);
+                       dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V,
+                       seq_of_token ? seq_of_token + t0 : nullptr, lse + t0, dlogp + t0, w.Gt,
+                       Tc, tiles_v, tiles_t);
+    hipLaunchKernelGGL(target_dz_kernel, dim3(rbp::ceil_div(Tn, 4)), dim3(256), 0, s, Hc, W,
+                       tokens + t0, seq_of_token ? seq_of_token + t0 : nullptr, lse + t0,
+                       dlogp + t0, Tn, d, V, w.Gt, Tc);
     // dhidden in two K halves when one pass would give each CU only a few
     // tiles (the last, partly empty round would then cost a large share)
     const int64_t tiles_dh = tiles_d * tiles_t;
