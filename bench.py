@@ -37,11 +37,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # 1.0).  Only valid for the sources the counters were read on.
 TRAFFIC_SOURCES = ("logprob.hip", "gemm_core.h", "gemm_dma.h")
 TRAFFIC = {
-    "sources_sha256": "902b8192f7421d881a7ffe25ae987fad7e453efded898897a67da4674b1086af",
-    "fetch_bytes": {"logits_lse_partial_kernel": 27359900081,   # 13359692 KiB x 2.0
-                    "lse_merge_kernel": 373312410},             # 182294 KiB x 2.0
-    "write_bytes": {"logits_lse_partial_kernel": 116963904,     # 114223 KiB
-                    "lse_merge_kernel": 264704},                # 258.5 KiB
+    "sources_sha256": "9c855af5dc0ae7d5f86116880989454f81b8e2bb884b8a2944e657933a584c20",
+    "fetch_bytes": {"logits_lse_partial_kernel": 27484116608,   # 13420347 KiB x 2.0
+                    "lse_merge_kernel": 373010553},             # 182139 KiB x 2.0
+    "write_bytes": {"logits_lse_partial_kernel": 116942797,     # 114202 KiB
+                    "lse_merge_kernel": 265267},                # 259.1 KiB
 }
 
 
