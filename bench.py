@@ -37,7 +37,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # 1.0).  Only valid for the sources the counters were read on.
 TRAFFIC_SOURCES = ("logprob.hip", "gemm_core.h", "gemm_dma.h")
 TRAFFIC = {
-    "sources_sha256": "9c855af5dc0ae7d5f86116880989454f81b8e2bb884b8a2944e657933a584c20",
+    "sources_sha256": "e294450e0a07a15b59a31e2bcb60ef1b2e933ee15a5d505613f2fad2673d0fbb",
     "fetch_bytes": {"logits_lse_partial_kernel": 27484116608,   # 13420347 KiB x 2.0
                     "lse_merge_kernel": 373010553},             # 182139 KiB x 2.0
     "write_bytes": {"logits_lse_partial_kernel": 116942797,     # 114202 KiB

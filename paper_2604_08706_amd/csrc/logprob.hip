@@ -13,15 +13,15 @@
 // the target logit z_{t,y_t} = h_t . W_{y_t} directly (one dot product).
 //
 // Backward, per chunk of Tc tokens:
-//   1. the same product is recomputed; its epilogue turns the tile into
-//      dz = dlogp (onehot - exp(z - lse)), rounded to bf16, written both
-//      token-major (dz [Tc][Vp]) and vocabulary-major (dz^T [Vp][Tc]);
-//      Vp = V rounded up to 256, padding written as zeros;
-//   2. dH = dz W as sum_v W^T[m][v] dz[t][v], W^T transposed once per call;
-//   3. dW = dz^T H as sum_t H^T[m][t] dz^T[v][t], H^T transposed per chunk.
-// Every product keeps both operands k-contiguous and runs on the persistent
-// direct-load stream of gemm_dma.h (one 256 x 256 workgroup per CU).  No
-// floating-point atomics are used, so results are bitwise reproducible.
+//   1. the same product is recomputed; its epilogue writes dz = -dlogp p as
+//      bf16 into dz^T [Vp][Tc] (Vp = V rounded up to 256, padding zero), and
+//      a small pass overwrites each token's target entry with
+//      dlogp (1 - p_{t,y_t}) from a direct dot product for z_{t,y_t};
+//   2. dH[t][m] = sum_v W[v][m] dz^T[v][t]: W and dz^T read MN-major;
+//   3. dW[v][m] (+)= sum_t H[t][m] dz^T[v][t]: H read MN-major, dz^T K-major.
+// Every product runs on the persistent direct-load stream of gemm_dma.h (one
+// 256 x 256 workgroup per CU), reading W and H in place.  No floating-point
+// atomics are used, so results are bitwise reproducible.
 
 #include <cmath>
 
