@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=3072,
                     help="tokens of the bounded sample the CPU oracle is timed on")
+    ap.add_argument("--no-aux", action="store_true",
+                    help="skip the HBM-rate measurement of sample+gather and loss on the "
+                         "10^6-record stress buffer")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB three "
                          "times (calibrates the HBM byte counters) and exit")
@@ -181,6 +184,107 @@ def run_step(rbp, wl, S, step, out, ev=None):
         ev[3].record()
 
 
+def aux_stress(iters=20):
+    """HBM rate of the two memory-bound steps on the long-sequence stress
+    buffer (10^6 records, ~1.8e9 stored tokens in HBM):
+      sample+gather: 256 positive-mixture draws (p_pos = 0.5), padded to 8192;
+      loss: policy_loss_fwd_bwd over the same draws packed (~4.7e5 tokens).
+    Algorithmic bytes: gather = 4 B/record reward scan + 4 B per positive slot
+    + 20 B record metadata per draw + 8 B read per gathered token + 12 B
+    written per padded position; loss = 16 B per token (logp, old_logp,
+    seq_of_token read, dlogp written) + 8 B per sequence."""
+    import torch
+
+    import paper_2604_08706_amd as rbp
+    from paper_2604_08706_amd import workloads as wlm
+
+    dev = "cuda"
+    wl = wlm.WORKLOADS["stress"]
+    tab = wlm.record_table(wl, 3)
+    n = len(tab.length)
+    total = int(tab.length.sum())
+    tok = wlm.arena_tokens(total, wl.V, 3, device=dev)
+    old = wlm.normal(total, 1.0, 4, device=dev)
+    adv = wlm.normal(n, 1.0, 5, device=dev)
+    keep = (torch.from_numpy(tab.arena_off).to(dev),
+            torch.from_numpy(tab.length.astype(np.int32)).to(dev),
+            torch.from_numpy(tab.reward).to(dev), adv, torch.from_numpy(tab.version).to(dev))
+    rec = rbp.make_records(n, n, 0, *keep, tok, old)
+    p_q32 = int(wl.p_pos * 2.0 ** 32)  # floor(p_pos * 2^32), the sampler's coin threshold
+    n_pos = int((tab.reward > 0).sum())
+    ws = rbp.workspace(rbp.RBP_OP_SAMPLE_GATHER, n)
+
+    def cfg(step, layout, **kw):
+        return rbp.make_sample_cfg(rbp.RB_POS_MIX, layout, 3, step, wl.n_draw, p_pos_q32=p_q32,
+                                   cur_version=tab.cur_version, **kw)
+
+    c_pad = cfg(0, rbp.RB_LAYOUT_PADDED, l_max=wl.l_max)
+    out = rbp.alloc_batch(c_pad)
+    for k in range(3):
+        rbp.rb_sample_gather(rec, cfg(100 + k, rbp.RB_LAYOUT_PADDED, l_max=wl.l_max), out, ws)
+    cfgs = [cfg(i, rbp.RB_LAYOUT_PADDED, l_max=wl.l_max) for i in range(iters)]
+    # The calls take less GPU time than the host needs to issue them: a spin
+    # kernel ahead of the timed region lets all of them queue, so the events
+    # measure the GPU executing them back to back.
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for c in cfgs:
+        rbp.rb_sample_gather(rec, c, out, ws)
+    b.record()
+    torch.cuda.synchronize()
+    g_ms = a.elapsed_time(b) / iters
+    n_tok = []  # valid tokens per call, from an untimed repeat (draws depend on the step only)
+    for c in cfgs:
+        rbp.rb_sample_gather(rec, c, out, ws)
+        n_tok.append(int(out["n_tokens"].item()))
+    g_bytes = float(np.mean([4 * n + 4 * n_pos + 20 * wl.n_draw + 8 * v
+                             + 12 * wl.n_draw * wl.l_max for v in n_tok]))
+    g_rate = g_bytes / (g_ms / 1e3)
+
+    # loss over the draws packed (one micro-batch holding every drawn token)
+    c_pk = cfg(0, rbp.RB_LAYOUT_PACKED, max_tokens=wl.n_draw * wl.l_max)
+    pk = rbp.alloc_batch(c_pk)
+    rbp.rb_sample_gather(rec, c_pk, pk, ws)
+    T = int(pk["n_tokens"].item())
+    old_t = pk["old_logp"][:T]
+    logp = old_t + wlm.normal(T, 0.05, 6, device=dev)
+    seq = pk["seq_of_token"][:T]
+    dlogp = torch.empty(T, device=dev)
+    loss = torch.zeros(1, device=dev)
+    stats = torch.zeros(4, device=dev)
+    ws_l = rbp.workspace(rbp.RBP_OP_LOSS, T)
+    for _ in range(3):
+        rbp.policy_loss_fwd_bwd(logp, old_t, seq, pk["adv"], pk["len"], wl.n_draw, loss, dlogp,
+                                stats, ws_l)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(iters):
+        rbp.policy_loss_fwd_bwd(logp, old_t, seq, pk["adv"], pk["len"], wl.n_draw, loss, dlogp,
+                                stats, ws_l)
+    b.record()
+    torch.cuda.synchronize()
+    l_ms = a.elapsed_time(b) / iters
+    l_bytes = 16 * T + 8 * wl.n_draw
+    del tok, old, keep, rec
+    torch.cuda.empty_cache()
+    return {
+        "workload": "stress: 10^6 records, 256 positive-mixture draws (p_pos 0.5), "
+                    "log-normal lengths capped at 8192",
+        "sample_gather": {"layout": "padded [256, 8192]", "ms": round(g_ms, 4),
+                          "tokens": int(np.mean(n_tok)),
+                          "bytes": int(g_bytes),
+                          "GB/s": round(g_rate / 1e9, 1),
+                          "frac_hbm": round(g_rate / PEAK_HBM, 4)},
+        "loss": {"tokens": T, "ms": round(l_ms, 4), "bytes": l_bytes,
+                 "GB/s": round(l_bytes / (l_ms / 1e3) / 1e9, 1),
+                 "frac_hbm": round(l_bytes / (l_ms / 1e3) / PEAK_HBM, 4)},
+    }
+
+
 def cpu_baseline(wl, n_tokens, seed=0):
     """The oracle (fp64 numpy) timed on a bounded sample of the same workload:
     the buffer draw and gather, then log-probs, loss and backward over the
@@ -271,6 +375,8 @@ def main():
     loss_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
     n_valid = int(out["n_tokens"].item())
+    # forward + loss + backward only (the sampler excluded), median over steps
+    k24_ms = float(np.median([e[0].elapsed_time(e[3]) for e in evs]))
     tok_s = n_valid * args.steps / (ms_total / 1e3)
     dV = wl.d * wl.V
     frac = tok_s * 6 * dV / PEAK_BF16
@@ -293,6 +399,8 @@ def main():
                    "tokens_per_step": n_valid, "d": wl.d, "V": wl.V},
         "mfma_peak_frac_6dV": round(frac, 4),
         "mfma_peak_frac_8dV_executed": round(tok_s * 8 * dV / PEAK_BF16, 4),
+        "median_ms_fwd_loss_bwd": round(k24_ms, 3),
+        "tokens_per_s_median_fwd_loss_bwd": round(n_valid / (k24_ms / 1e3), 1),
         "phase_ms": {"fwd": round(fwd_ms, 3), "loss": round(loss_ms, 3),
                      "bwd": round(bwd_ms, 3),
                      "sample+adv+rest": round(ms_step - fwd_ms - loss_ms - bwd_ms, 3)},
@@ -307,6 +415,8 @@ def main():
         },
         "wall_s_timed": round(t_wall, 3),
     }
+    if not args.no_aux:
+        rec["memory_bound_steps"] = aux_stress()
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_tokens)
     print(json.dumps(rec), flush=True)

@@ -51,32 +51,69 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Loss terms of one token (a masked token, s < 0, contributes nothing).
+struct TokenTerms {
+  float g, wterm, rho, cut, valid, term;
+};
+__device__ __forceinline__ TokenTerms token_terms(float lp, float olp, int32_t s,
+                                                  const float* __restrict__ adv,
+                                                  const int32_t* __restrict__ seq_len,
+                                                  float inv_nseq, float lo_b, float hi_b) {
+  TokenTerms r{0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  if (s < 0) return r;
+  const float A = adv[s];
+  const float w = inv_nseq / (float)seq_len[s];
+  const float rho = expf(lp - olp);
+  const float clipped = fminf(fmaxf(rho, lo_b), hi_b);
+  const float term = fminf(rho * A, clipped * A);
+  const bool cut = (A > 0.0f && rho > hi_b) || (A < 0.0f && rho < lo_b);
+  r.g = cut ? 0.0f : -A * rho * w;
+  r.wterm = term * w;
+  r.rho = rho;
+  r.cut = cut ? 1.0f : 0.0f;
+  r.valid = 1.0f;
+  r.term = term;
+  return r;
+}
+
+// Four consecutive tokens per thread and iteration (16-byte loads and
+// stores) when the arrays are 16-byte aligned; a scalar loop takes the rest.
 __global__ void __launch_bounds__(kLossThreads) grpo_token_kernel(
     const float* __restrict__ logp, const float* __restrict__ old_logp,
     const int32_t* __restrict__ seq_of_token, const float* __restrict__ adv,
-    const int32_t* __restrict__ seq_len, int64_t T, float inv_nseq, float eps_low,
+    const int32_t* __restrict__ seq_len, int64_t T, int vec, float inv_nseq, float eps_low,
     float eps_high, float* __restrict__ dlogp, float* __restrict__ partials) {
   float acc[kNumSums] = {0.f, 0.f, 0.f, 0.f, 0.f};
   const float lo_b = 1.0f - eps_low, hi_b = 1.0f + eps_high;
-  for (int64_t t = (int64_t)blockIdx.x * kLossThreads + threadIdx.x; t < T;
-       t += (int64_t)gridDim.x * kLossThreads) {
-    const int32_t s = seq_of_token[t];
-    float g = 0.0f;
-    if (s >= 0) {
-      const float A = adv[s];
-      const float w = inv_nseq / (float)seq_len[s];
-      const float rho = expf(logp[t] - old_logp[t]);
-      const float clipped = fminf(fmaxf(rho, lo_b), hi_b);
-      const float term = fminf(rho * A, clipped * A);
-      const bool cut = (A > 0.0f && rho > hi_b) || (A < 0.0f && rho < lo_b);
-      g = cut ? 0.0f : -A * rho * w;
-      acc[0] -= term * w;
-      acc[1] += rho;
-      acc[2] += cut ? 1.0f : 0.0f;
-      acc[3] += 1.0f;
-      acc[4] += term;
-    }
-    dlogp[t] = g;
+  auto add = [&](const TokenTerms& r) {
+    acc[0] -= r.wterm;
+    acc[1] += r.rho;
+    acc[2] += r.cut;
+    acc[3] += r.valid;
+    acc[4] += r.term;
+  };
+  const int64_t T4 = vec ? T / 4 : 0;  // vec: all four arrays 16-byte aligned
+  const int64_t stride = (int64_t)gridDim.x * kLossThreads;
+  for (int64_t q = (int64_t)blockIdx.x * kLossThreads + threadIdx.x; q < T4; q += stride) {
+    const float4 lp = reinterpret_cast<const float4*>(logp)[q];
+    const float4 ol = reinterpret_cast<const float4*>(old_logp)[q];
+    const int4 sq = reinterpret_cast<const int4*>(seq_of_token)[q];
+    const TokenTerms a = token_terms(lp.x, ol.x, sq.x, adv, seq_len, inv_nseq, lo_b, hi_b);
+    const TokenTerms b = token_terms(lp.y, ol.y, sq.y, adv, seq_len, inv_nseq, lo_b, hi_b);
+    const TokenTerms c = token_terms(lp.z, ol.z, sq.z, adv, seq_len, inv_nseq, lo_b, hi_b);
+    const TokenTerms e = token_terms(lp.w, ol.w, sq.w, adv, seq_len, inv_nseq, lo_b, hi_b);
+    reinterpret_cast<float4*>(dlogp)[q] = make_float4(a.g, b.g, c.g, e.g);
+    add(a);
+    add(b);
+    add(c);
+    add(e);
+  }
+  for (int64_t t = T4 * 4 + (int64_t)blockIdx.x * kLossThreads + threadIdx.x; t < T;
+       t += stride) {
+    const TokenTerms a =
+        token_terms(logp[t], old_logp[t], seq_of_token[t], adv, seq_len, inv_nseq, lo_b, hi_b);
+    dlogp[t] = a.g;
+    add(a);
   }
   __shared__ float lds[kLossThreads / 64][kNumSums];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -93,19 +130,21 @@ __global__ void __launch_bounds__(kLossThreads) grpo_token_kernel(
   }
 }
 
-__global__ void __launch_bounds__(64) grpo_finalize_kernel(const float* __restrict__ partials,
-                                                           int nblocks,
-                                                           float* __restrict__ loss_accum,
-                                                           float* __restrict__ stats) {
-  // one lane per sum, blocks added in block order
-  const int k = threadIdx.x;
-  if (k >= kNumSums) return;
+// Wave k sums the block partials of sum k: lane l takes blocks l, l + 64, ...
+// in order, then a fixed butterfly combines the lanes (bitwise reproducible).
+__global__ void __launch_bounds__(64 * kNumSums) grpo_finalize_kernel(
+    const float* __restrict__ partials, int nblocks, float* __restrict__ loss_accum,
+    float* __restrict__ stats) {
+  const int k = threadIdx.x >> 6, lane = threadIdx.x & 63;
   float v = 0.0f;
-  for (int b = 0; b < nblocks; ++b) v += partials[b * kNumSums + k];
-  if (k == 0)
-    loss_accum[0] += v;
-  else
-    stats[k - 1] += v;
+  for (int b = lane; b < nblocks; b += 64) v += partials[b * kNumSums + k];
+  v = wave_sum(v);
+  if (lane == 0) {
+    if (k == 0)
+      loss_accum[0] += v;
+    else
+      stats[k - 1] += v;
+  }
 }
 
 }  // namespace
@@ -154,10 +193,13 @@ extern "C" int policy_loss_fwd_bwd(const float* logp, const float* old_logp,
   if (nb > kLossMaxBlocks) nb = kLossMaxBlocks;
   float* partials = static_cast<float*>(ws);
   const float inv_nseq = (float)(1.0 / (double)n_seq_total);
+  const int vec = ((reinterpret_cast<uintptr_t>(logp) | reinterpret_cast<uintptr_t>(old_logp) |
+                    reinterpret_cast<uintptr_t>(seq_of_token) | reinterpret_cast<uintptr_t>(dlogp)) &
+                   15) == 0;
   hipLaunchKernelGGL(grpo_token_kernel, dim3(nb), dim3(kLossThreads), 0, s, logp, old_logp,
-                     seq_of_token, adv, seq_len, T, inv_nseq, eps_low, eps_high, dlogp,
+                     seq_of_token, adv, seq_len, T, vec, inv_nseq, eps_low, eps_high, dlogp,
                      partials);
-  hipLaunchKernelGGL(grpo_finalize_kernel, dim3(1), dim3(64), 0, s, partials, (int)nb,
+  hipLaunchKernelGGL(grpo_finalize_kernel, dim3(1), dim3(64 * kNumSums), 0, s, partials, (int)nb,
                      loss_accum, stats);
   RBP_CHECK_LAUNCH("policy_loss_fwd_bwd");
   return RBP_OK;

@@ -234,6 +234,11 @@ __global__ void __launch_bounds__(256) gather_packed_kernel(
   }
 }
 
+// Padded rows: draw j fills row j of [n_draw, l_max] (positions past the
+// record's length: token 0, log-prob 0, seq -1).  kVec: four positions per
+// thread with 16-byte stores (l_max % 4 == 0, rows 16-byte aligned); the
+// arena is read with 4-byte loads, its rows start anywhere.
+template <bool kVec>
 __global__ void __launch_bounds__(256) gather_padded_kernel(
     int64_t l_max, int64_t head, int64_t cap, const int32_t* __restrict__ idx,
     const int32_t* __restrict__ len, const int64_t* __restrict__ arena_off,
@@ -245,16 +250,38 @@ __global__ void __launch_bounds__(256) gather_padded_kernel(
   int32_t* tok_row = tokens + j * l_max;
   float* old_row = old_logp + j * l_max;
   int32_t* seq_row = seq + j * l_max;
-  for (int64_t p = (int64_t)blockIdx.y * blockDim.x + threadIdx.x; p < l_max;
-       p += (int64_t)gridDim.y * blockDim.x) {
-    if (p < n) {
-      tok_row[p] = arena_tokens[off + p];
-      old_row[p] = arena_old[off + p];
-      seq_row[p] = (int32_t)j;
-    } else {
-      tok_row[p] = 0;
-      old_row[p] = 0.0f;
-      seq_row[p] = -1;
+  if constexpr (kVec) {
+    for (int64_t p = ((int64_t)blockIdx.y * blockDim.x + threadIdx.x) * 4; p < l_max;
+         p += (int64_t)gridDim.y * blockDim.x * 4) {
+      int4 tk;
+      float4 ol;
+      int4 sq;
+      int32_t* tkp = &tk.x;
+      float* olp = &ol.x;
+      int32_t* sqp = &sq.x;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool in = p + i < n;
+        tkp[i] = in ? arena_tokens[off + p + i] : 0;
+        olp[i] = in ? arena_old[off + p + i] : 0.0f;
+        sqp[i] = in ? (int32_t)j : -1;
+      }
+      *reinterpret_cast<int4*>(tok_row + p) = tk;
+      *reinterpret_cast<float4*>(old_row + p) = ol;
+      *reinterpret_cast<int4*>(seq_row + p) = sq;
+    }
+  } else {
+    for (int64_t p = (int64_t)blockIdx.y * blockDim.x + threadIdx.x; p < l_max;
+         p += (int64_t)gridDim.y * blockDim.x) {
+      if (p < n) {
+        tok_row[p] = arena_tokens[off + p];
+        old_row[p] = arena_old[off + p];
+        seq_row[p] = (int32_t)j;
+      } else {
+        tok_row[p] = 0;
+        old_row[p] = 0.0f;
+        seq_row[p] = -1;
+      }
     }
   }
 }
@@ -357,11 +384,16 @@ extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
                        out->cu_seqlens, out->idx, rec->arena_off, rec->arena_tokens,
                        rec->arena_old_logp, out->tokens, out->old_logp, out->seq_of_token);
   } else {
-    int64_t by = rbp::ceil_div(cfg->l_max, 256);
+    const bool vec = cfg->l_max % 4 == 0 &&
+                     ((reinterpret_cast<uintptr_t>(out->tokens) |
+                       reinterpret_cast<uintptr_t>(out->old_logp) |
+                       reinterpret_cast<uintptr_t>(out->seq_of_token)) & 15) == 0;
+    int64_t by = rbp::ceil_div(cfg->l_max, vec ? 1024 : 256);
     if (by > 64) by = 64;
-    hipLaunchKernelGGL(gather_padded_kernel, dim3(cfg->n_draw, by), dim3(256), 0, s, cfg->l_max,
-                       rec->head, rec->capacity, out->idx, out->len, rec->arena_off,
-                       rec->arena_tokens, rec->arena_old_logp, out->tokens, out->old_logp,
+    hipLaunchKernelGGL(vec ? gather_padded_kernel<true> : gather_padded_kernel<false>,
+                       dim3(cfg->n_draw, by), dim3(256), 0, s, cfg->l_max, rec->head,
+                       rec->capacity, out->idx, out->len, rec->arena_off, rec->arena_tokens,
+                       rec->arena_old_logp, out->tokens, out->old_logp,
                        out->seq_of_token);
   }
   RBP_CHECK_LAUNCH("rb_sample_gather");
