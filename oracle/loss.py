@@ -31,7 +31,11 @@ Masked tokens (seq_of_token < 0) contribute nothing and get dlogp = 0.
 Parity: pinned by the on-policy identity (old = current gives rho = 1,
 loss = -(1/n_seq) sum_i A_i and dlogp_t = -A_i / (n_seq len_i)), zero loss on
 whole groups with equal lengths, the clip cases on both sides of each boundary,
-and central finite differences -- tests/test_oracle_loss.py.
+and central finite differences -- tests/test_oracle_loss.py.  The two variants
+at the end of this module (AsymRE, whole-sequence ratio) are pinned by finite
+differences, the sign of delta_V through the group sum of the coefficients,
+shift identities, the on-policy identity and, for one-token sequences, by the
+token-level objective above -- tests/test_oracle_loss_variants.py.
 """
 
 import numpy as np
@@ -68,3 +72,78 @@ def grpo_loss(logp, old_logp, seq_of_token, adv, seq_len, n_seq, eps_low=0.2,
         float(np.sum(term[valid])),
     ])
     return -J, dlogp, stats
+
+
+# ---- objective variants (the paper's AsymRE; a whole-sequence ratio) -------
+#
+# AsymRE (App. D.2): J = E[(1/G) sum_i (r_i - (V_hat + delta_V)) log pi(z_i|q)],
+# V_hat the mean reward of rollout i's group (known at generation), delta_V =
+# -0.1, log pi(z|q) the sum of the rollout's token log-probabilities.
+# Readings (design notes R13, R15): the per-rollout coefficient
+# c_i = r_i - V_hat_g - delta_V is stored at insert like the GRPO advantage;
+# the group average over G becomes the average over the n_seq sampled
+# rollouts of the optimizer batch (as for GRPO); no ratio, no clip, no
+# per-token length normalisation (log pi is a sum over the rollout's tokens).
+#
+# Sequence-ratio GRPO (R1's alternative reading, R16): rho_i =
+# pi(z_i|q) / pi_old(z_i|q) = exp(sum_{t in i} (logp_t - old_logp_t)),
+# J = (1/n_seq) sum_i min(rho_i A_i, clip(rho_i, 1 - eps_low, 1 + eps_high) A_i),
+# with the clip-gradient rule of R4 applied to rho_i.  The sum runs over the
+# whole rollout, so a call must hold complete sequences (given by cu_seqlens).
+
+
+def asymre_coef(rewards, group_off, delta_v=-0.1):
+    """c_i = r_i - (mean reward of i's group + delta_v), plain loops in fp64."""
+    c = [0.0] * len(rewards)
+    for g in range(len(group_off) - 1):
+        lo, hi = int(group_off[g]), int(group_off[g + 1])
+        if hi <= lo:
+            continue
+        v_hat = sum(float(rewards[i]) for i in range(lo, hi)) / (hi - lo)
+        for i in range(lo, hi):
+            c[i] = float(rewards[i]) - (v_hat + float(delta_v))
+    return c
+
+
+def asymre_loss(logp, seq_of_token, coef, n_seq):
+    """Return (loss, dlogp [T], stats) in fp64 for the AsymRE objective.
+
+    loss = -(1/n_seq) sum_t c_{s(t)} logp_t over valid tokens; dlogp_t =
+    -c_{s(t)} / n_seq; stats = [number of valid tokens, sum_t c_{s(t)} logp_t].
+    """
+    logp = np.asarray(logp, dtype=np.float64)
+    seq = np.asarray(seq_of_token, dtype=np.int64)
+    coef = np.asarray(coef, dtype=np.float64)
+    valid = seq >= 0
+    c = np.where(valid, coef[np.where(valid, seq, 0)], 0.0)
+    s = float(np.sum(c * logp))
+    loss = -s / float(n_seq)
+    dlogp = np.where(valid, -c / float(n_seq), 0.0)
+    return loss, dlogp, np.array([float(np.sum(valid)), s])
+
+
+def grpo_seq_loss(logp, old_logp, cu_seqlens, adv, n_seq, eps_low=0.2, eps_high=0.2):
+    """Return (loss, dlogp [T], stats) in fp64 for the whole-sequence ratio.
+
+    Sequence i holds tokens [cu_seqlens[i], cu_seqlens[i+1]); tokens outside
+    every sequence get dlogp = 0.  stats = [sum_i rho_i, number of sequences
+    on a clipped branch with zero gradient, number of sequences, sum_i l_i].
+    """
+    logp = np.asarray(logp, dtype=np.float64)
+    old = np.asarray(old_logp, dtype=np.float64)
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    adv = np.asarray(adv, dtype=np.float64)
+    dlogp = np.zeros_like(logp)
+    J = 0.0
+    st = np.zeros(4)
+    for i in range(len(cu) - 1):
+        lo, hi = int(cu[i]), int(cu[i + 1])
+        rho = float(np.exp(np.sum(logp[lo:hi] - old[lo:hi])))
+        A = float(adv[i])
+        term = min(rho * A, min(max(rho, 1.0 - eps_low), 1.0 + eps_high) * A)
+        cut = (A > 0 and rho > 1.0 + eps_high) or (A < 0 and rho < 1.0 - eps_low)
+        J += term / float(n_seq)
+        if not cut:
+            dlogp[lo:hi] = -A * rho / float(n_seq)
+        st += [rho, 1.0 if cut else 0.0, 1.0, term]
+    return -J, dlogp, st
