@@ -15,6 +15,12 @@
  *   policy_loss_fwd_bwd  clipped GRPO loss and d loss / d logp        (App. D.2)
  *   policy_logprob_bwd   d loss / d hidden and d loss / d W           (chain rule of the above)
  *
+ * and two objective variants on the same tokens:
+ *
+ *   policy_loss_seq_fwd_bwd  the GRPO objective with the whole-rollout ratio (App. D.2)
+ *   rb_asymre_coef,          AsymRE: coefficient at insert and the
+ *   policy_asymre_fwd_bwd    objective with its gradient                (App. D.2)
+ *
  * Conventions shared by every entry point:
  *   - Pointers marked "device" are HIP device pointers (or managed memory); the
  *     structs themselves and every scalar argument live on the host.
@@ -75,8 +81,9 @@ enum {
 enum {
   RBP_OP_SAMPLE_GATHER = 1, /* n = capacity of the record table              */
   RBP_OP_LOGPROB_FWD = 2,   /* n = T                                          */
-  RBP_OP_LOSS = 3,          /* n = T                                          */
-  RBP_OP_LOGPROB_BWD = 4    /* n = tokens per backward chunk (T for one chunk) */
+  RBP_OP_LOSS = 3,          /* n = T (also policy_asymre_fwd_bwd)            */
+  RBP_OP_LOGPROB_BWD = 4,   /* n = tokens per backward chunk (T for one chunk) */
+  RBP_OP_LOSS_SEQ = 5       /* n = B, sequences of policy_loss_seq_fwd_bwd     */
 };
 
 /*
@@ -219,6 +226,58 @@ int policy_loss_fwd_bwd(const float* logp, const float* old_logp,
                         int64_t n_seq_total, float eps_low, float eps_high,
                         float* loss_accum, float* dlogp, float* stats,
                         void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Whole-sequence-ratio form of the same objective -- the printed App. D.2
+ * formula read literally (the ratio of the rollout's probabilities):
+ *   rho_i   = exp(sum_{t in i} (logp_t - old_logp_t))
+ *   l_i     = min(rho_i A_i, clip(rho_i, 1 - eps_low, 1 + eps_high) A_i)
+ *   loss    = -sum_i l_i / n_seq_total
+ *   dlogp_t = -A_i rho_i act_i / n_seq_total for every token t of sequence i,
+ *             act_i as above with rho_i.
+ * Sequence i is tokens [cu_seqlens[i], cu_seqlens[i+1]) and must be complete
+ * in this call (the ratio needs every token); tokens from cu_seqlens[B] to T
+ * get dlogp = 0.  logp, old_logp device fp32 [T]; cu_seqlens device int32
+ * [B + 1], non-decreasing, cu_seqlens[0] = 0, cu_seqlens[B] <= T; adv device
+ * fp32 [B].  loss_accum [1] and stats [4] ACCUMULATE:
+ *   stats = {sum rho_i, sequences clipped with zero gradient, sequences, sum l_i}.
+ * ws device, >= rbp_workspace_bytes(RBP_OP_LOSS_SEQ, B, 0, 0).
+ * Errors: RBP_EINVAL (null pointers, T < 0, B < 1, n_seq_total < 1, eps < 0);
+ *         RBP_EWORKSPACE.
+ */
+int policy_loss_seq_fwd_bwd(const float* logp, const float* old_logp,
+                            const int32_t* cu_seqlens, const float* adv, int64_t T,
+                            int32_t B, int64_t n_seq_total, float eps_low, float eps_high,
+                            float* loss_accum, float* dlogp, float* stats, void* ws,
+                            size_t ws_bytes, void* stream);
+
+/*
+ * AsymRE coefficient at insert (App. D.2): for every record of group g
+ * (records [group_off[g], group_off[g+1])),
+ *   coef_i = reward_i - (mean reward of the group + delta_v),
+ * the paper's delta_v being -0.1.  Stored in the record table's advantage
+ * slot when training with policy_asymre_fwd_bwd.  reward, coef device fp32;
+ * group_off device int32 [n_groups + 1].
+ * Errors: RBP_EINVAL (null pointers, n_groups < 0).
+ */
+int rb_asymre_coef(const float* reward, const int32_t* group_off, int32_t n_groups,
+                   float delta_v, float* coef, void* stream);
+
+/*
+ * AsymRE objective (App. D.2) on replayed tokens, no ratio and no clip:
+ *   loss    = -sum_t coef_i logp_t / n_seq_total       (i = seq_of_token[t])
+ *   dlogp_t = -coef_i / n_seq_total
+ * logp, seq_of_token device [T] (seq_of_token < 0 masks the token: dlogp = 0);
+ * coef device fp32 [B] (rb_asymre_coef).  loss_accum [1] and stats [2]
+ * ACCUMULATE: stats = {valid tokens, sum coef_i logp_t}.  dlogp overwritten.
+ * ws device, >= rbp_workspace_bytes(RBP_OP_LOSS, T, 0, 0).
+ * Errors: RBP_EINVAL (null pointers, T < 0, B < 1, n_seq_total < 1);
+ *         RBP_EWORKSPACE.
+ */
+int policy_asymre_fwd_bwd(const float* logp, const int32_t* seq_of_token, const float* coef,
+                          int64_t T, int32_t B, int64_t n_seq_total, float* loss_accum,
+                          float* dlogp, float* stats, void* ws, size_t ws_bytes,
+                          void* stream);
 
 /*
  * Backward of policy_logprob_fwd: with p_t = exp(z_t - lse_t) and

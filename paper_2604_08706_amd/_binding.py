@@ -30,11 +30,13 @@ RBP_OP_SAMPLE_GATHER = 1
 RBP_OP_LOGPROB_FWD = 2
 RBP_OP_LOSS = 3
 RBP_OP_LOGPROB_BWD = 4
+RBP_OP_LOSS_SEQ = 5
 
 EXPORTED = (
     "rb_sample_gather", "rb_group_advantage", "policy_logprob_fwd",
     "policy_loss_fwd_bwd", "policy_logprob_bwd", "rbp_workspace_bytes",
-    "rbp_status_string", "rbp_last_error",
+    "rbp_status_string", "rbp_last_error", "policy_loss_seq_fwd_bwd", "rb_asymre_coef",
+    "policy_asymre_fwd_bwd",
 )
 
 
@@ -92,6 +94,10 @@ def load_library(path=LIB_PATH):
                                         vp, vp, vp, vp, sz, vp]
     lib.policy_logprob_bwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i32, i32, vp, vp,
                                        ctypes.c_int, vp, sz, vp]
+    lib.policy_loss_seq_fwd_bwd.argtypes = [vp, vp, vp, vp, i64, i32, i64, f32, f32, vp, vp,
+                                            vp, vp, sz, vp]
+    lib.rb_asymre_coef.argtypes = [vp, vp, i32, f32, vp, vp]
+    lib.policy_asymre_fwd_bwd.argtypes = [vp, vp, vp, i64, i32, i64, vp, vp, vp, vp, sz, vp]
     lib.rbp_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i32]
     lib.rbp_workspace_bytes.restype = sz
     lib.rbp_status_string.argtypes = [ctypes.c_int]
@@ -273,6 +279,48 @@ def policy_loss_fwd_bwd(logp, old_logp, seq_of_token, adv, seq_len, n_seq_total,
                                    _dev(stats, torch.float32, "stats", 4), wsp, wsb,
                                    _stream(stream))
     _check("policy_loss_fwd_bwd", st)
+
+
+def policy_loss_seq_fwd_bwd(logp, old_logp, cu_seqlens, adv, n_seq_total, loss_accum, dlogp,
+                            stats, ws, eps_low=0.2, eps_high=0.2, stream=None):
+    T = logp.numel()
+    B = adv.numel()
+    wsp, wsb = _ws(ws)
+    st = lib().policy_loss_seq_fwd_bwd(_dev(logp, torch.float32, "logp", T),
+                                       _dev(old_logp, torch.float32, "old_logp", T),
+                                       _dev(cu_seqlens, torch.int32, "cu_seqlens", B + 1),
+                                       _dev(adv, torch.float32, "adv", B), T, B,
+                                       int(n_seq_total), eps_low, eps_high,
+                                       _dev(loss_accum, torch.float32, "loss_accum", 1),
+                                       _dev(dlogp, torch.float32, "dlogp", T),
+                                       _dev(stats, torch.float32, "stats", 4), wsp, wsb,
+                                       _stream(stream))
+    _check("policy_loss_seq_fwd_bwd", st)
+
+
+def rb_asymre_coef(reward, group_off, coef, delta_v=-0.1, stream=None):
+    n_groups = group_off.numel() - 1
+    st = lib().rb_asymre_coef(_dev(reward, torch.float32, "reward"),
+                              _dev(group_off, torch.int32, "group_off"), n_groups,
+                              float(delta_v), _dev(coef, torch.float32, "coef", reward.numel()),
+                              _stream(stream))
+    _check("rb_asymre_coef", st)
+
+
+def policy_asymre_fwd_bwd(logp, seq_of_token, coef, n_seq_total, loss_accum, dlogp, stats, ws,
+                          stream=None):
+    T = logp.numel()
+    B = coef.numel()
+    wsp, wsb = _ws(ws)
+    st = lib().policy_asymre_fwd_bwd(_dev(logp, torch.float32, "logp", T),
+                                     _dev(seq_of_token, torch.int32, "seq_of_token", T),
+                                     _dev(coef, torch.float32, "coef", B), T, B,
+                                     int(n_seq_total),
+                                     _dev(loss_accum, torch.float32, "loss_accum", 1),
+                                     _dev(dlogp, torch.float32, "dlogp", T),
+                                     _dev(stats, torch.float32, "stats", 2), wsp, wsb,
+                                     _stream(stream))
+    _check("policy_asymre_fwd_bwd", st)
 
 
 def policy_logprob_bwd(hidden, W, tokens, seq_of_token, lse, dlogp, dhidden, dW, ws,

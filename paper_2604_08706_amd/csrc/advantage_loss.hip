@@ -147,10 +147,164 @@ __global__ void __launch_bounds__(64 * kNumSums) grpo_finalize_kernel(
   }
 }
 
+// ---- objective variants -------------------------------------------------
+
+__global__ void __launch_bounds__(64) asymre_coef_kernel(const float* __restrict__ reward,
+                                                         const int32_t* __restrict__ group_off,
+                                                         int32_t n_groups, float delta_v,
+                                                         float* __restrict__ coef) {
+  const int32_t g = blockIdx.x * 64 + threadIdx.x;
+  if (g >= n_groups) return;
+  const int32_t lo = group_off[g], hi = group_off[g + 1];
+  if (hi <= lo) return;
+  float sum = 0.0f;
+  for (int32_t i = lo; i < hi; ++i) sum += reward[i];
+  const float base = sum / (float)(hi - lo) + delta_v;
+  for (int32_t i = lo; i < hi; ++i) coef[i] = reward[i] - base;
+}
+
+// AsymRE per token: dlogp = -c / n_seq; sums {-sum c logp / n_seq, valid, sum c logp}
+// in the slots {0, 3, 4} of the shared partial layout (1, 2 unused).
+__global__ void __launch_bounds__(kLossThreads) asymre_token_kernel(
+    const float* __restrict__ logp, const int32_t* __restrict__ seq_of_token,
+    const float* __restrict__ coef, int64_t T, float inv_nseq, float* __restrict__ dlogp,
+    float* __restrict__ partials) {
+  float s_cl = 0.0f, n_valid = 0.0f;
+  for (int64_t t = (int64_t)blockIdx.x * kLossThreads + threadIdx.x; t < T;
+       t += (int64_t)gridDim.x * kLossThreads) {
+    const int32_t s = seq_of_token[t];
+    float g = 0.0f;
+    if (s >= 0) {
+      const float c = coef[s];
+      g = -c * inv_nseq;
+      s_cl = fmaf(c, logp[t], s_cl);
+      n_valid += 1.0f;
+    }
+    dlogp[t] = g;
+  }
+  __shared__ float lds[kLossThreads / 64][2];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float a = wave_sum(s_cl), b = wave_sum(n_valid);
+  if (lane == 0) {
+    lds[wave][0] = a;
+    lds[wave][1] = b;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float v0 = 0.0f, v1 = 0.0f;
+    for (int w = 0; w < kLossThreads / 64; ++w) {
+      v0 += lds[w][0];
+      v1 += lds[w][1];
+    }
+    float* p = partials + (int64_t)blockIdx.x * kNumSums;
+    p[0] = -v0 * inv_nseq;
+    p[1] = 0.0f;
+    p[2] = 0.0f;
+    p[3] = v1;
+    p[4] = v0;
+  }
+}
+
+// Sum k of the partials over blocks (one wave per sum, fixed order), added to
+// out[k]; AsymRE and the sequence form share the partial layout above.
+__global__ void __launch_bounds__(64) sums_finalize_kernel(const float* __restrict__ partials,
+                                                           int nblocks, int k_first, int k_count,
+                                                           float* __restrict__ loss_accum,
+                                                           float* __restrict__ stats) {
+  const int lane = threadIdx.x & 63;
+  const int k = blockIdx.x;
+  float v = 0.0f;
+  for (int b = lane; b < nblocks; b += 64) v += partials[b * kNumSums + k];
+  v = wave_sum(v);
+  if (lane == 0) {
+    if (k == 0)
+      loss_accum[0] += v;
+    else if (k >= k_first && k < k_first + k_count)
+      stats[k - k_first] += v;
+  }
+}
+
+// Whole-sequence ratio: one wave per sequence sums log-ratios over its tokens
+// (lane-strided, fixed butterfly), forms rho_i, the term and the gradient,
+// writes dlogp over the sequence and the per-sequence values into `seqv`
+// ([B][4]: -l_i / n_seq, rho_i, clipped, l_i).
+__global__ void __launch_bounds__(256) seq_ratio_kernel(
+    const float* __restrict__ logp, const float* __restrict__ old_logp,
+    const int32_t* __restrict__ cu, const float* __restrict__ adv, int32_t B, float inv_nseq,
+    float eps_low, float eps_high, float* __restrict__ dlogp, float* __restrict__ seqv) {
+  const int32_t i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= B) return;
+  const int64_t lo = cu[i], hi = cu[i + 1];
+  float s = 0.0f;
+  for (int64_t t = lo + lane; t < hi; t += 64) s += logp[t] - old_logp[t];
+  s = wave_sum(s);
+  const float rho = expf(s);
+  const float A = adv[i];
+  const float lo_b = 1.0f - eps_low, hi_b = 1.0f + eps_high;
+  const float term = fminf(rho * A, fminf(fmaxf(rho, lo_b), hi_b) * A);
+  const bool cut = (A > 0.0f && rho > hi_b) || (A < 0.0f && rho < lo_b);
+  const float g = cut ? 0.0f : -A * rho * inv_nseq;
+  for (int64_t t = lo + lane; t < hi; t += 64) dlogp[t] = g;
+  if (lane == 0) {
+    float* v = seqv + (int64_t)i * 4;
+    v[0] = -term * inv_nseq;
+    v[1] = rho;
+    v[2] = cut ? 1.0f : 0.0f;
+    v[3] = term;
+  }
+}
+
+// Partials of the per-sequence values: block b covers sequences
+// [b * 256, b * 256 + 256), in the shared layout {-sum l/n, sum rho, clipped,
+// sequences, sum l}.
+__global__ void __launch_bounds__(256) seq_partials_kernel(const float* __restrict__ seqv,
+                                                           int32_t B,
+                                                           float* __restrict__ partials) {
+  const int32_t i = blockIdx.x * 256 + threadIdx.x;
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  float n = 0.0f;
+  if (i < B) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = seqv[(int64_t)i * 4 + k];
+    n = 1.0f;
+  }
+  __shared__ float lds[4][kNumSums];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float r[kNumSums] = {wave_sum(v[0]), wave_sum(v[1]), wave_sum(v[2]), wave_sum(n),
+                             wave_sum(v[3])};
+  if (lane == 0) {
+#pragma unroll
+    for (int k = 0; k < kNumSums; ++k) lds[wave][k] = r[k];
+  }
+  __syncthreads();
+  if (threadIdx.x < kNumSums) {
+    float a = 0.0f;
+    for (int w = 0; w < 4; ++w) a += lds[w][threadIdx.x];
+    partials[(int64_t)blockIdx.x * kNumSums + threadIdx.x] = a;
+  }
+}
+
+// dlogp = 0 for tokens [cu[B], T), past the last sequence.
+__global__ void __launch_bounds__(256) zero_tail_kernel(const int32_t* __restrict__ cu, int32_t B,
+                                                        int64_t T, float* __restrict__ dlogp) {
+  const int64_t start = cu[B];
+  for (int64_t t = start + (int64_t)blockIdx.x * 256 + threadIdx.x; t < T;
+       t += (int64_t)gridDim.x * 256)
+    dlogp[t] = 0.0f;
+}
+
 }  // namespace
 
 size_t rbp::loss_ws(int64_t /*T*/) {
   return align_up(sizeof(float) * kLossMaxBlocks * kNumSums, 256);
+}
+
+size_t rbp::loss_seq_ws(int64_t B) {
+  // per-sequence values [B][4], then one partial row per 256 sequences
+  const int64_t n = B < 1 ? 1 : B;
+  return align_up(sizeof(float) * (size_t)n * 4, 256) +
+         align_up(sizeof(float) * (size_t)ceil_div(n, 256) * kNumSums, 256);
 }
 
 extern "C" int rb_group_advantage(const float* reward, const int32_t* group_off,
@@ -202,5 +356,85 @@ extern "C" int policy_loss_fwd_bwd(const float* logp, const float* old_logp,
   hipLaunchKernelGGL(grpo_finalize_kernel, dim3(1), dim3(64 * kNumSums), 0, s, partials, (int)nb,
                      loss_accum, stats);
   RBP_CHECK_LAUNCH("policy_loss_fwd_bwd");
+  return RBP_OK;
+}
+
+extern "C" int rb_asymre_coef(const float* reward, const int32_t* group_off, int32_t n_groups,
+                              float delta_v, float* coef, void* stream) {
+  rbp::clear_error();
+  RBP_REQUIRE(n_groups >= 0, RBP_EINVAL, "rb_asymre_coef: n_groups < 0");
+  if (n_groups == 0) return RBP_OK;
+  RBP_REQUIRE(reward && group_off && coef, RBP_EINVAL, "rb_asymre_coef: null pointer");
+  hipLaunchKernelGGL(asymre_coef_kernel, dim3((n_groups + 63) / 64), dim3(64), 0,
+                     rbp::as_stream(stream), reward, group_off, n_groups, delta_v, coef);
+  RBP_CHECK_LAUNCH("rb_asymre_coef");
+  return RBP_OK;
+}
+
+extern "C" int policy_asymre_fwd_bwd(const float* logp, const int32_t* seq_of_token,
+                                     const float* coef, int64_t T, int32_t B, int64_t n_seq_total,
+                                     float* loss_accum, float* dlogp, float* stats, void* ws,
+                                     size_t ws_bytes, void* stream) {
+  rbp::clear_error();
+  RBP_REQUIRE(T >= 0, RBP_EINVAL, "policy_asymre_fwd_bwd: T < 0");
+  RBP_REQUIRE(B >= 1 && n_seq_total >= 1, RBP_EINVAL,
+              "policy_asymre_fwd_bwd: need B >= 1 and n_seq_total >= 1");
+  RBP_REQUIRE(coef && loss_accum && stats, RBP_EINVAL, "policy_asymre_fwd_bwd: null pointer");
+  RBP_REQUIRE(T == 0 || (logp && seq_of_token && dlogp), RBP_EINVAL,
+              "policy_asymre_fwd_bwd: null per-token pointer");
+  const size_t need = rbp::loss_ws(T);
+  RBP_REQUIRE(ws && ws_bytes >= need, RBP_EWORKSPACE,
+              "policy_asymre_fwd_bwd: workspace needs %zu bytes, got %zu", need, ws_bytes);
+  hipStream_t s = rbp::as_stream(stream);
+  int64_t nb = rbp::ceil_div(T, kLossThreads * 4);
+  if (nb < 1) nb = 1;
+  if (nb > kLossMaxBlocks) nb = kLossMaxBlocks;
+  float* partials = static_cast<float*>(ws);
+  const float inv_nseq = (float)(1.0 / (double)n_seq_total);
+  hipLaunchKernelGGL(asymre_token_kernel, dim3(nb), dim3(kLossThreads), 0, s, logp, seq_of_token,
+                     coef, T, inv_nseq, dlogp, partials);
+  // loss (sum 0) and stats {valid, sum c logp} = sums 3, 4
+  hipLaunchKernelGGL(sums_finalize_kernel, dim3(kNumSums), dim3(64), 0, s, partials, (int)nb, 3,
+                     2, loss_accum, stats);
+  RBP_CHECK_LAUNCH("policy_asymre_fwd_bwd");
+  return RBP_OK;
+}
+
+extern "C" int policy_loss_seq_fwd_bwd(const float* logp, const float* old_logp,
+                                       const int32_t* cu_seqlens, const float* adv, int64_t T,
+                                       int32_t B, int64_t n_seq_total, float eps_low,
+                                       float eps_high, float* loss_accum, float* dlogp,
+                                       float* stats, void* ws, size_t ws_bytes, void* stream) {
+  rbp::clear_error();
+  RBP_REQUIRE(T >= 0, RBP_EINVAL, "policy_loss_seq_fwd_bwd: T < 0");
+  RBP_REQUIRE(B >= 1 && n_seq_total >= 1, RBP_EINVAL,
+              "policy_loss_seq_fwd_bwd: need B >= 1 and n_seq_total >= 1");
+  RBP_REQUIRE(eps_low >= 0.0f && eps_high >= 0.0f, RBP_EINVAL,
+              "policy_loss_seq_fwd_bwd: negative clip range");
+  RBP_REQUIRE(cu_seqlens && adv && loss_accum && stats, RBP_EINVAL,
+              "policy_loss_seq_fwd_bwd: null pointer");
+  RBP_REQUIRE(T == 0 || (logp && old_logp && dlogp), RBP_EINVAL,
+              "policy_loss_seq_fwd_bwd: null per-token pointer");
+  const size_t need = rbp::loss_seq_ws(B);
+  RBP_REQUIRE(ws && ws_bytes >= need, RBP_EWORKSPACE,
+              "policy_loss_seq_fwd_bwd: workspace needs %zu bytes, got %zu", need, ws_bytes);
+  hipStream_t s = rbp::as_stream(stream);
+  rbp::WsCarver c(ws);
+  float* seqv = c.take<float>((size_t)B * 4);
+  const int64_t nbp = rbp::ceil_div(B, 256);
+  float* partials = c.take<float>((size_t)nbp * kNumSums);
+  const float inv_nseq = (float)(1.0 / (double)n_seq_total);
+  hipLaunchKernelGGL(seq_ratio_kernel, dim3(rbp::ceil_div(B, 4)), dim3(256), 0, s, logp,
+                     old_logp, cu_seqlens, adv, B, inv_nseq, eps_low, eps_high, dlogp, seqv);
+  if (T > 0) {
+    int64_t blocks = rbp::ceil_div(T, 256);
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(zero_tail_kernel, dim3(blocks), dim3(256), 0, s, cu_seqlens, B, T, dlogp);
+  }
+  hipLaunchKernelGGL(seq_partials_kernel, dim3(nbp), dim3(256), 0, s, seqv, B, partials);
+  // loss (sum 0) and stats {sum rho, clipped, sequences, sum l} = sums 1..4
+  hipLaunchKernelGGL(sums_finalize_kernel, dim3(kNumSums), dim3(64), 0, s, partials, (int)nbp, 1,
+                     4, loss_accum, stats);
+  RBP_CHECK_LAUNCH("policy_loss_seq_fwd_bwd");
   return RBP_OK;
 }

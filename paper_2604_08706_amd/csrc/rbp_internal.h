@@ -37,6 +37,7 @@ struct WsCarver {
 size_t sample_gather_ws(int64_t capacity);
 size_t logprob_fwd_ws(int64_t T, int32_t V);
 size_t loss_ws(int64_t T);
+size_t loss_seq_ws(int64_t B);
 size_t logprob_bwd_ws(int64_t Tc, int32_t d, int32_t V);
 
 }  // namespace rbp
