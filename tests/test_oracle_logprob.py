@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 from scipy.special import logsumexp
 
-from oracle.logprob import logprob, logprob_rows
+from oracle.logprob import entropy, logprob, logprob_rows
 
 
 def _inputs(T, d, V, seed, w_std=0.5):
@@ -85,3 +85,41 @@ def test_shift_invariance_in_a_direction_shared_by_all_rows_of_W():
     a, _ = logprob(h, W, y)
     b, _ = logprob(h, W + c[None, :], y)
     assert np.allclose(a, b, rtol=0, atol=1e-11)
+
+
+# ---- entropy ----------------------------------------------------------------
+
+def test_entropy_of_uniform_logits_is_log_v():
+    h, W, _ = _inputs(5, 8, 37, 11)
+    assert np.allclose(entropy(h, np.zeros_like(W)), math.log(37), rtol=0, atol=1e-13)
+
+
+def test_entropy_two_logits_is_binary_entropy_of_a_sigmoid():
+    # z = (a, 0): p = sigmoid(a), H = -p ln p - (1 - p) ln(1 - p)
+    a = np.array([-3.0, -0.5, 0.0, 0.7, 4.0])
+    h = a[:, None]
+    W = np.array([[1.0], [0.0]])
+    p = 1.0 / (1.0 + np.exp(-a))
+    want = -(p * np.log(p) + (1 - p) * np.log(1 - p))
+    assert np.allclose(entropy(h, W), want, rtol=1e-13, atol=0)
+
+
+def test_entropy_matches_scipy_and_its_bounds():
+    from scipy.stats import entropy as scipy_entropy
+    h, W, _ = _inputs(40, 16, 300, 12, w_std=0.4)
+    z = h @ W.T
+    p = np.exp(z - z.max(axis=1, keepdims=True))
+    want = np.array([scipy_entropy(row) for row in p])  # normalises, uses ln
+    got = entropy(h, W, chunk=7)
+    assert np.allclose(got, want, rtol=1e-12, atol=0)
+    assert np.all(got >= 0) and np.all(got <= math.log(300) + 1e-12)
+
+
+def test_entropy_of_a_peaked_distribution_and_masking():
+    # one logit 30 above three zeros: H = ln(1 + 3e^-30) + 90 e^-30 / (1 + 3e^-30)
+    h = np.array([[1.0], [1.0]])
+    W = np.array([[30.0], [0.0], [0.0], [0.0]])
+    e = math.exp(-30.0)
+    want = math.log1p(3 * e) + 90 * e / (1 + 3 * e)
+    got = entropy(h, W, seq_of_token=[0, -1])
+    assert got[0] == pytest.approx(want, rel=1e-9) and got[1] == 0.0
