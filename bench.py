@@ -57,6 +57,8 @@ def parse():
     ap.add_argument("--no-aux", action="store_true",
                     help="skip the HBM-rate measurement of sample+gather and loss on the "
                          "10^6-record stress buffer")
+    ap.add_argument("--no-fused", action="store_true",
+                    help="skip the separately reported single-pass policy_fused_fwd_bwd leg")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB three "
                          "times (calibrates the HBM byte counters) and exit")
@@ -332,6 +334,57 @@ def cpu_baseline(wl, n_tokens, seed=0):
                       f"backward in fp64 numpy); {dt:.1f} s"}
 
 
+def run_step_fused(rbp, wl, S, step, out, ev=None):
+    """The same step through policy_fused_fwd_bwd (forward, loss, backward and
+    entropy in one call; keeps T x V exp(z - max) in its workspace)."""
+    rbp.rb_group_advantage(S["rewards"], S["group_off"], S["adv_rec"])
+    rbp.rb_sample_gather(S["rec"], cfg_for(rbp, wl, step), out, S["ws_sample"])
+    if ev is not None:
+        ev[0].record()
+    rbp.policy_fused_fwd_bwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"],
+                             out["old_logp"], out["adv"], out["len"], wl.n_draw, S["logp"],
+                             S["lse"], S["entropy"], S["loss"], S["dlogp"], S["stats"], S["dh"],
+                             S["dW"], S["ws_fused"], accumulate_dW=True)
+    if ev is not None:
+        ev[1].record()
+
+
+def fused_leg(rbp, wl, S, out, first_step, steps, warmup):
+    """Time the single-pass path on the same sampled batches as the main loop."""
+    import torch
+
+    S["entropy"] = torch.empty(S["T"], device="cuda")
+    S["ws_fused"] = rbp.workspace(rbp.RBP_OP_FUSED, S["T"], wl.d, wl.V)
+    for k in range(warmup):
+        run_step_fused(rbp, wl, S, first_step + k, out)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        run_step_fused(rbp, wl, S, first_step + warmup + i, out, evs[i])
+    stop.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / steps
+    n_valid = int(out["n_tokens"].item())
+    med = float(np.median([e[0].elapsed_time(e[1]) for e in evs]))
+    dV = wl.d * wl.V
+    del S["ws_fused"]
+    torch.cuda.empty_cache()
+    return {
+        "entry": "policy_fused_fwd_bwd (stores T x V exp(z - max) in bf16; "
+                 "not the headline, whose forward never materialises T x V)",
+        "tokens_per_s": round(n_valid / (ms_step / 1e3), 1),
+        "ms_per_step": round(ms_step, 3),
+        "median_ms_fwd_loss_bwd": round(med, 3),
+        "tokens_per_s_median_fwd_loss_bwd": round(n_valid / (med / 1e3), 1),
+        "mfma_peak_frac_6dV": round(n_valid / (ms_step / 1e3) * 6 * dV / PEAK_BF16, 4),
+        "steps": steps,
+        "warmup": warmup,
+    }
+
+
 def main():
     args = parse()
     if args.copy_probe_mib:
@@ -351,7 +404,7 @@ def main():
         raise SystemExit("bench workload must use the packed layout")
     S = setup(wl)
     T = S["T"]
-    steps = list(range(args.warmup + args.steps))
+    steps = list(range((args.warmup + args.steps) * (1 if args.no_fused else 2)))
     align_old_logp(rbp, wl, S, steps, wl.noise_sd)
     cfg0 = cfg_for(rbp, wl, 0)
     out = rbp.alloc_batch(cfg0)
@@ -415,6 +468,9 @@ def main():
         },
         "wall_s_timed": round(t_wall, 3),
     }
+    if not args.no_fused:
+        rec["fused_single_pass"] = fused_leg(rbp, wl, S, out, args.warmup + args.steps,
+                                             args.steps, args.warmup)
     if not args.no_aux:
         rec["memory_bound_steps"] = aux_stress()
     if not args.no_cpu_baseline:

@@ -15,6 +15,10 @@
  *   policy_loss_fwd_bwd  clipped GRPO loss and d loss / d logp        (App. D.2)
  *   policy_logprob_bwd   d loss / d hidden and d loss / d W           (chain rule of the above)
  *
+ * the three token-level calls above in one pass, with the policy entropy:
+ *
+ *   policy_fused_fwd_bwd forward, loss and backward, 6 d V flop per token (App. D.2, E)
+ *
  * and two objective variants on the same tokens:
  *
  *   policy_loss_seq_fwd_bwd  the GRPO objective with the whole-rollout ratio (App. D.2)
@@ -83,7 +87,8 @@ enum {
   RBP_OP_LOGPROB_FWD = 2,   /* n = T                                          */
   RBP_OP_LOSS = 3,          /* n = T (also policy_asymre_fwd_bwd)            */
   RBP_OP_LOGPROB_BWD = 4,   /* n = tokens per backward chunk (T for one chunk) */
-  RBP_OP_LOSS_SEQ = 5       /* n = B, sequences of policy_loss_seq_fwd_bwd     */
+  RBP_OP_LOSS_SEQ = 5,      /* n = B, sequences of policy_loss_seq_fwd_bwd     */
+  RBP_OP_FUSED = 6          /* n = tokens per policy_fused_fwd_bwd chunk       */
 };
 
 /*
@@ -303,6 +308,41 @@ int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
                        int32_t d, int32_t V, float* dhidden, float* dW,
                        int accumulate_dW, void* ws, size_t ws_bytes,
                        void* stream);
+
+/*
+ * policy_logprob_fwd + policy_loss_fwd_bwd + policy_logprob_bwd in one pass,
+ * plus the per-token entropy of the policy, H_t = -sum_v p_{t,v} log p_{t,v}
+ * (the training entropy of App. E).  The separate calls execute 8 d V flop
+ * per token because the backward recomputes the logits; this one executes the
+ * 6 d V of the definition by keeping, per token, the forward tile pass's
+ * exp(z - max) for every vocabulary entry as bf16 in the workspace (2 V bytes
+ * per token; it does materialise a T x V array, which policy_logprob_fwd
+ * never does).  dz is rounded to bf16 twice instead of once.
+ * Arguments: hidden, W, tokens, seq_of_token as in policy_logprob_fwd
+ * (seq_of_token required); old_logp, adv, seq_len, B, n_seq_total, eps_low,
+ * eps_high, loss_accum, stats as in policy_loss_fwd_bwd (loss_accum and stats
+ * ACCUMULATE); logp, lse, dlogp device fp32 [T] (overwritten); entropy device
+ * fp32 [T] (overwritten; may be NULL; 0 for masked tokens); dhidden, dW,
+ * accumulate_dW as in policy_logprob_bwd.
+ * ws device: tokens are processed in chunks of Tc tokens, with Tc the largest
+ * multiple of 256 (at most T rounded up to 256, at most 2^21) whose
+ * rbp_workspace_bytes(RBP_OP_FUSED, Tc, d, V) fits in ws_bytes: with
+ * Vp = V rounded up to 256, bf16 [Vp, Tc], fp32 [3 Vp / 128, Tc] partial
+ * sums, fp32 [Tc, d] and the loss pass's sums -- 5.5 GB for Tc = 16384 at
+ * d = 3584, V = 152064.
+ * Errors: RBP_EINVAL (null pointers, T < 0, d < 1, V < 1, B < 1,
+ *         n_seq_total < 1, eps < 0); RBP_EUNSUPPORTED (d % 8 != 0);
+ *         RBP_EWORKSPACE (not even a 256-token chunk fits).
+ */
+int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
+                         const int32_t* tokens, const int32_t* seq_of_token,
+                         const float* old_logp, const float* adv,
+                         const int32_t* seq_len, int64_t T, int32_t d, int32_t V,
+                         int32_t B, int64_t n_seq_total, float eps_low,
+                         float eps_high, float* logp, float* lse, float* entropy,
+                         float* loss_accum, float* dlogp, float* stats,
+                         float* dhidden, float* dW, int accumulate_dW, void* ws,
+                         size_t ws_bytes, void* stream);
 
 /* Workspace bytes an operation needs (see RBP_OP_*); 0 for an invalid op. */
 size_t rbp_workspace_bytes(int op, int64_t n, int32_t d, int32_t V);

@@ -25,6 +25,7 @@ from ._binding import (  # noqa: F401
     RBP_OP_LOGPROB_BWD,
     RBP_OP_LOGPROB_FWD,
     RBP_OP_LOSS,
+    RBP_OP_FUSED,
     RBP_OP_LOSS_SEQ,
     RBP_OP_SAMPLE_GATHER,
     RbpError,
@@ -36,6 +37,7 @@ from ._binding import (  # noqa: F401
     policy_logprob_bwd,
     policy_logprob_fwd,
     policy_asymre_fwd_bwd,
+    policy_fused_fwd_bwd,
     policy_loss_fwd_bwd,
     policy_loss_seq_fwd_bwd,
     rb_asymre_coef,

@@ -31,12 +31,13 @@ RBP_OP_LOGPROB_FWD = 2
 RBP_OP_LOSS = 3
 RBP_OP_LOGPROB_BWD = 4
 RBP_OP_LOSS_SEQ = 5
+RBP_OP_FUSED = 6
 
 EXPORTED = (
     "rb_sample_gather", "rb_group_advantage", "policy_logprob_fwd",
     "policy_loss_fwd_bwd", "policy_logprob_bwd", "rbp_workspace_bytes",
     "rbp_status_string", "rbp_last_error", "policy_loss_seq_fwd_bwd", "rb_asymre_coef",
-    "policy_asymre_fwd_bwd",
+    "policy_asymre_fwd_bwd", "policy_fused_fwd_bwd",
 )
 
 
@@ -98,6 +99,9 @@ def load_library(path=LIB_PATH):
                                             vp, vp, sz, vp]
     lib.rb_asymre_coef.argtypes = [vp, vp, i32, f32, vp, vp]
     lib.policy_asymre_fwd_bwd.argtypes = [vp, vp, vp, i64, i32, i64, vp, vp, vp, vp, sz, vp]
+    lib.policy_fused_fwd_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i32, i32, i32, i64,
+                                         f32, f32, vp, vp, vp, vp, vp, vp, vp, vp,
+                                         ctypes.c_int, vp, sz, vp]
     lib.rbp_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i32]
     lib.rbp_workspace_bytes.restype = sz
     lib.rbp_status_string.argtypes = [ctypes.c_int]
@@ -337,3 +341,30 @@ def policy_logprob_bwd(hidden, W, tokens, seq_of_token, lse, dlogp, dhidden, dW,
                                   _dev(dW, torch.float32, "dW", V * d),
                                   1 if accumulate_dW else 0, wsp, wsb, _stream(stream))
     _check("policy_logprob_bwd", st)
+
+
+def policy_fused_fwd_bwd(hidden, W, tokens, seq_of_token, old_logp, adv, seq_len, n_seq_total,
+                         logp, lse, entropy, loss_accum, dlogp, stats, dhidden, dW, ws,
+                         accumulate_dW=False, eps_low=0.2, eps_high=0.2, stream=None):
+    T, d = hidden.shape
+    V = W.shape[0]
+    B = adv.numel()
+    wsp, wsb = _ws(ws)
+    st = lib().policy_fused_fwd_bwd(_bf16_bits(hidden, "hidden", T * d),
+                                    _bf16_bits(W, "W", V * d),
+                                    _dev(tokens, torch.int32, "tokens", T),
+                                    _dev(seq_of_token, torch.int32, "seq_of_token", T),
+                                    _dev(old_logp, torch.float32, "old_logp", T),
+                                    _dev(adv, torch.float32, "adv", B),
+                                    _dev(seq_len, torch.int32, "seq_len", B), T, d, V, B,
+                                    int(n_seq_total), eps_low, eps_high,
+                                    _dev(logp, torch.float32, "logp", T),
+                                    _dev(lse, torch.float32, "lse", T),
+                                    _opt(entropy, torch.float32, "entropy", T),
+                                    _dev(loss_accum, torch.float32, "loss_accum", 1),
+                                    _dev(dlogp, torch.float32, "dlogp", T),
+                                    _dev(stats, torch.float32, "stats", 4),
+                                    _dev(dhidden, torch.float32, "dhidden", T * d),
+                                    _dev(dW, torch.float32, "dW", V * d),
+                                    1 if accumulate_dW else 0, wsp, wsb, _stream(stream))
+    _check("policy_fused_fwd_bwd", st)

@@ -1,0 +1,340 @@
+// Single-pass log-prob forward, GRPO loss and log-prob backward
+// (policy_fused_fwd_bwd), plus the per-token policy entropy.
+//
+// Same mathematics as policy_logprob_fwd + policy_loss_fwd_bwd +
+// policy_logprob_bwd (App. D.2): z_t = W h_t, lse_t, logp_t = z_{t,y_t} - lse_t,
+// the clipped objective's dlogp_t, dz_t = dlogp_t (e_{y_t} - p_t), dh_t = W^T dz_t,
+// dW (+)= sum_t dz_t h_t^T; and H_t = -sum_v p log p = lse_t - sum_v p_{t,v} z_{t,v},
+// the training entropy the paper tracks (App. E).
+//
+// The 4-call path recomputes the logit product in its backward, 8 d V flop per
+// token; this path executes the 6 d V of the definition by keeping the forward
+// tile pass's exponentials.  Per chunk of Tc tokens:
+//   1. Z^T = W H^T tile by tile.  For each token column and 128-row half tile
+//      i (one wave's rows), the epilogue writes the partial M_i = max z,
+//      S_i = sum exp(z - M_i), E_i = sum exp(z - M_i) z, and stores
+//      q = exp(z - M_i) as bf16 into Q^T [Vp][Tc] -- the layout the backward
+//      products read (dz^T);
+//   2. merge: lse and entropy from the partials, logp from one target dot
+//      product;
+//   3. the loss pass writes dlogp (policy_loss_fwd_bwd);
+//   4. in place, q -> dz = -dlogp_t exp(M_i - lse_t) q, and each token's target
+//      entry -> dlogp_t (1 - exp(logp_t)) from the fp32 logp;
+//   5. dhidden and dW, the products of the 4-call backward.
+// Unlike policy_logprob_fwd this keeps a T x V array (2 V bytes per token, in
+// the workspace).  dz is rounded to bf16 twice (q, then the scaled value)
+// instead of once.
+
+#include "logits_epilogue.h"
+#include "rbp_internal.h"
+
+namespace {
+
+using namespace rbp::lp;
+using rbp::gemm::kLdsBytes;
+using rbp::gemm::map_tile;
+using rbp::gemm::Operand;
+using rbp::gemm::Tile;
+using rbp::gemm::tile_stream;
+
+// Step 1: logit tiles -> partials (M, S, E) per (half tile, token) and
+// q = exp(z - M) into Q^T.
+RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
+                                           const uint16_t* __restrict__ Hc, int64_t Tn,
+                                           int32_t d, int32_t V, float* __restrict__ pM,
+                                           float* __restrict__ pS, float* __restrict__ pE,
+                                           int64_t ldp, uint16_t* __restrict__ Qt, int64_t ldQ,
+                                           int64_t tiles_m, int64_t tiles_n) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
+  const Operand A{W, d, V, d};
+  const Operand B{Hc, d, Tn, d};
+  const QuadSel qs;
+  const int lane = threadIdx.x & 63;
+  const int j = threadIdx.x & 3;
+  auto tile_of = [&](int32_t vid) {
+    int32_t tm, tn;
+    map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupLogits, tm, tn);
+    return Tile{tm * 256, tn * 256, 0, d};
+  };
+  auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
+    const Tile tile = tile_of(vid);
+    const int32_t vlim = V - tile.m0;
+    const int32_t lim = vlim - GL::row(0, 0);
+    float mx[GL::NI], sum[GL::NI], ez[GL::NI];
+    if (vlim >= 256)
+      column_stats_ent<true>(acc, 0, mx, sum, ez);
+    else
+      column_stats_ent<false>(acc, lim, mx, sum, ez);
+    // lanes l and l + 32 hold the same column's values: the lower half writes
+    // them, 128 contiguous bytes per array and column block
+    const int64_t half = (int64_t)(tile.m0 >> 7) + GL::wm();
+    if (lane < 32) {
+#pragma unroll
+      for (int ni = 0; ni < GL::NI; ++ni) {
+        const int64_t o = half * ldp + tile.n0 + GL::col(ni);
+        pM[o] = mx[ni];
+        pS[o] = sum[ni];
+        pE[o] = ez[ni];
+      }
+    }
+    // q = exp(z - M) with the store of the backward's dz (g = -dl exp(z - ls))
+    float ls[GL::NI], dl[GL::NI];
+#pragma unroll
+    for (int ni = 0; ni < GL::NI; ++ni) {
+      ls[ni] = mx[ni] == -INFINITY ? 0.0f : mx[ni] * kLog2e;
+      dl[ni] = -1.0f;
+    }
+    const auto rQ = __builtin_amdgcn_make_buffer_rsrc(
+        uniform_ptr(Qt + (int64_t)tile.m0 * ldQ + tile.n0), 0, (int)(256 * ldQ * 2), 0x00020000);
+    const uint32_t off =
+        (uint32_t)((GL::wm() * (256 / GL::WM) + j) * ldQ + GL::wn() * (256 / GL::WN) +
+                   32 * (lane >> 5) + ((lane & 31) - j)) * 2u;
+#pragma unroll
+    for (int mi = 0; mi < GL::MI; ++mi) {
+      if (vlim >= 256)
+        dz_rows<true>(acc, ls, dl, mi, lim, qs, rQ, off, ldQ);
+      else
+        dz_rows<false>(acc, ls, dl, mi, lim, qs, rQ, off, ldQ);
+    }
+  };
+  tile_stream<GL, false, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
+}
+
+// (m, s, e) <- merge with the partial (Mi, Si, Ei), rescaling to the larger max.
+__device__ __forceinline__ void merge_partial(float& m, float& s, float& e, float Mi, float Si,
+                                              float Ei) {
+  if (Mi == -INFINITY) return;  // a half tile past the vocabulary
+  if (Mi > m) {
+    const float f = exp2f((m - Mi) * kLog2e);
+    s = fmaf(s, f, Si);
+    e = fmaf(e, f, Ei);
+    m = Mi;
+  } else {
+    const float f = exp2f((Mi - m) * kLog2e);
+    s = fmaf(Si, f, s);
+    e = fmaf(Ei, f, e);
+  }
+}
+
+// Step 2: 64 tokens per block.  Four waves merge interleaved quarters of each
+// token's partials (coalesced: consecutive lanes read consecutive tokens), the
+// quarters are combined in a fixed order, then each wave forms the target
+// logits of 16 tokens with one dot product each.
+constexpr int kMergeTokens = 64;
+
+__global__ void __launch_bounds__(256) fused_merge_kernel(
+    const float* __restrict__ pM, const float* __restrict__ pS, const float* __restrict__ pE,
+    int64_t ldp, int32_t n_half, const uint16_t* __restrict__ Hc,
+    const uint16_t* __restrict__ W, const int32_t* __restrict__ tokens,
+    const int32_t* __restrict__ seq, int64_t Tn, int32_t d, int32_t V, float* __restrict__ logp,
+    float* __restrict__ lse, float* __restrict__ ent) {
+  __shared__ float sm[4][kMergeTokens], ss[4][kMergeTokens], se[4][kMergeTokens];
+  __shared__ float sl[kMergeTokens];
+  const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int64_t t0 = (int64_t)blockIdx.x * kMergeTokens;
+  const int64_t t = t0 + c;
+  float m = -INFINITY, s = 0.0f, e = 0.0f;
+  if (t < Tn)
+    for (int32_t i = q; i < n_half; i += 4) {
+      const int64_t o = (int64_t)i * ldp + t;
+      merge_partial(m, s, e, pM[o], pS[o], pE[o]);
+    }
+  sm[q][c] = m;
+  ss[q][c] = s;
+  se[q][c] = e;
+  __syncthreads();
+  if (threadIdx.x < kMergeTokens) {
+    float M = -INFINITY, S = 0.0f, E = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) merge_partial(M, S, E, sm[k][c], ss[k][c], se[k][c]);
+    const bool valid = t < Tn && (seq == nullptr || seq[t] >= 0);
+    const float l = M + logf(S);
+    sl[c] = valid ? l : 0.0f;
+    if (t < Tn) {
+      lse[t] = valid ? l : 0.0f;
+      if (ent != nullptr) ent[t] = valid ? l - E / S : 0.0f;
+    }
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  for (int k = 0; k < kMergeTokens / 4; ++k) {
+    const int cc = q * (kMergeTokens / 4) + k;
+    const int64_t tt = t0 + cc;
+    if (tt >= Tn) break;
+    if (seq != nullptr && seq[tt] < 0) {
+      if (lane == 0) logp[tt] = 0.0f;
+      continue;
+    }
+    const int32_t y = tokens[tt];
+    const bool y_ok = y >= 0 && y < V;
+    const float z = dot_bf16_wave(Hc + tt * d, W + (int64_t)(y_ok ? y : 0) * d, d, lane);
+    if (lane == 0) logp[tt] = y_ok ? z - sl[cc] : NAN;
+  }
+}
+
+// Step 4: one block per (128 vocabulary rows, 2048 tokens), eight tokens per
+// thread.  q -> -dlogp_t exp(M_i - lse_t) q in place; invalid tokens and the
+// padding columns Tn..T256 become zero; then the target entries.
+constexpr int kScaleTokens = 2048;
+
+template <int kRows>
+__device__ __forceinline__ void scale_rows(uint16_t* __restrict__ q, int64_t ldQ, int rows,
+                                           const float (&c)[8]) {
+#pragma unroll 8
+  for (int r = 0; r < (kRows > 0 ? kRows : rows); ++r) {
+    uint4* p = reinterpret_cast<uint4*>(q + r * ldQ);
+    const uint4 x = *p;
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      o[k] = pack_bf16x2(c[2 * k] * bf16_to_f32((uint16_t)(w[k] & 0xffff)),
+                         c[2 * k + 1] * bf16_to_f32((uint16_t)(w[k] >> 16)));
+    *p = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+__global__ void __launch_bounds__(256) grad_scale_kernel(
+    uint16_t* __restrict__ Qt, int64_t ldQ, int64_t T256, const float* __restrict__ pM,
+    int64_t ldp, const float* __restrict__ lse, const float* __restrict__ logp,
+    const float* __restrict__ dlogp, const int32_t* __restrict__ tokens,
+    const int32_t* __restrict__ seq, int64_t Tn, int32_t V) {
+  const int64_t tb = (int64_t)blockIdx.x * kScaleTokens + threadIdx.x * 8;
+  const int32_t v0 = (int32_t)blockIdx.y * 128;
+  const int32_t rows = V - v0 < 128 ? V - v0 : 128;
+  if (tb >= T256 || rows <= 0) return;
+  const float* m = pM + (int64_t)blockIdx.y * ldp + tb;
+  float c[8], gy[8];
+  int32_t y[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int64_t t = tb + k;
+    const bool valid = t < Tn && (seq == nullptr || seq[t] >= 0);
+    c[k] = 0.0f;
+    gy[k] = 0.0f;
+    y[k] = -1;
+    if (valid) {
+      const float dl = dlogp[t];
+      c[k] = -dl * exp2_hw((m[k] - lse[t]) * kLog2e);
+      gy[k] = -dl * expm1f(logp[t]);
+      y[k] = tokens[t];
+    }
+  }
+  uint16_t* q = Qt + (int64_t)v0 * ldQ + tb;
+  if (rows == 128)
+    scale_rows<128>(q, ldQ, rows, c);
+  else
+    scale_rows<0>(q, ldQ, rows, c);
+  // the target rows, written after this thread's own scaled stores to them
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    if (y[k] >= v0 && y[k] < v0 + rows)
+      q[(int64_t)(y[k] - v0) * ldQ + k] = __builtin_bit_cast(uint16_t, (__bf16)gy[k]);
+}
+
+// Workspace: Q^T [Vp][Tc] bf16, partials M, S, E [Vp / 128][Tc] fp32, the
+// second dhidden K half [Tc][d] fp32, the loss pass's partial sums.
+struct FusedWs {
+  uint16_t* Qt;
+  float *pM, *pS, *pE;
+  float* dh_half;
+  void* loss;
+  size_t loss_bytes;
+  size_t bytes;
+};
+
+FusedWs carve_fused(void* base, int64_t Tc, int32_t d, int32_t V) {
+  rbp::WsCarver c(base);
+  const int64_t Vp = round256(V);
+  FusedWs w;
+  w.Qt = c.take<uint16_t>((size_t)Vp * (size_t)Tc);
+  w.pM = c.take<float>((size_t)(Vp / 128) * (size_t)Tc);
+  w.pS = c.take<float>((size_t)(Vp / 128) * (size_t)Tc);
+  w.pE = c.take<float>((size_t)(Vp / 128) * (size_t)Tc);
+  w.dh_half = c.take<float>((size_t)Tc * (size_t)d);
+  w.loss_bytes = rbp::loss_ws(Tc);
+  w.loss = c.take<uint8_t>(w.loss_bytes);
+  w.bytes = rbp::align_up(c.used, 256);
+  return w;
+}
+
+}  // namespace
+
+size_t rbp::fused_ws(int64_t Tc, int32_t d, int32_t V) {
+  return carve_fused(nullptr, round256(Tc < 1 ? 1 : Tc), d < 1 ? 1 : d, V < 1 ? 1 : V).bytes;
+}
+
+extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
+                                    const int32_t* tokens, const int32_t* seq_of_token,
+                                    const float* old_logp, const float* adv,
+                                    const int32_t* seq_len, int64_t T, int32_t d, int32_t V,
+                                    int32_t B, int64_t n_seq_total, float eps_low,
+                                    float eps_high, float* logp, float* lse, float* entropy,
+                                    float* loss_accum, float* dlogp, float* stats,
+                                    float* dhidden, float* dW, int accumulate_dW, void* ws,
+                                    size_t ws_bytes, void* stream) {
+  rbp::clear_error();
+  RBP_REQUIRE(T >= 0 && d >= 1 && V >= 1, RBP_EINVAL,
+              "policy_fused_fwd_bwd: need T >= 0, d >= 1, V >= 1");
+  RBP_REQUIRE(d % 8 == 0, RBP_EUNSUPPORTED, "policy_fused_fwd_bwd: d %% 8 != 0 (d = %d)", d);
+  RBP_REQUIRE(B >= 1 && n_seq_total >= 1, RBP_EINVAL,
+              "policy_fused_fwd_bwd: need B >= 1 and n_seq_total >= 1");
+  RBP_REQUIRE(eps_low >= 0.0f && eps_high >= 0.0f, RBP_EINVAL,
+              "policy_fused_fwd_bwd: negative clip range");
+  RBP_REQUIRE(W && dW && adv && seq_len && loss_accum && stats, RBP_EINVAL,
+              "policy_fused_fwd_bwd: null pointer");
+  RBP_REQUIRE(T == 0 || (hidden && tokens && seq_of_token && old_logp && logp && lse && dlogp &&
+                         dhidden),
+              RBP_EINVAL, "policy_fused_fwd_bwd: null per-token pointer");
+  hipStream_t s = rbp::as_stream(stream);
+  if (T == 0) {
+    rbp::launch_grad_products(nullptr, W, nullptr, 0, 0, d, V, nullptr, nullptr, dW,
+                              accumulate_dW, s);
+    RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+    return RBP_OK;
+  }
+  // largest chunk (multiple of 256 tokens, at most 2^21 so that every per-tile
+  // byte range of Q^T fits a 32-bit buffer offset) whose workspace fits
+  int64_t Tc = 0;
+  if (ws) {
+    int64_t lo = 256, hi = round256(T) < (int64_t(1) << 21) ? round256(T) : (int64_t(1) << 21);
+    if (rbp::fused_ws(lo, d, V) <= ws_bytes) {
+      while (lo < hi) {
+        const int64_t mid = (lo + hi + 256) / 512 * 256;
+        if (rbp::fused_ws(mid, d, V) <= ws_bytes) lo = mid; else hi = mid - 256;
+      }
+      Tc = lo;
+    }
+  }
+  RBP_REQUIRE(Tc >= 256, RBP_EWORKSPACE,
+              "policy_fused_fwd_bwd: workspace of %zu bytes holds no 256-token chunk (needs %zu)",
+              ws_bytes, rbp::fused_ws(256, d, V));
+  const FusedWs w = carve_fused(ws, Tc, d, V);
+  const int64_t Vp = round256(V), tiles_v = Vp / 256;
+  const int n_cu = device_cus();
+  for (int64_t t0 = 0; t0 < T; t0 += Tc) {
+    const int64_t Tn = (T - t0) < Tc ? (T - t0) : Tc;
+    const int64_t T256 = round256(Tn), tiles_t = T256 / 256;
+    const uint16_t* Hc = hidden + t0 * d;
+    const int32_t* sq = seq_of_token + t0;
+    hipLaunchKernelGGL(logits_store_kernel, dim3(rbp::gemm::stream_grid(tiles_v * tiles_t, n_cu)),
+                       dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, w.pM, w.pS, w.pE, Tc, w.Qt, Tc,
+                       tiles_v, tiles_t);
+    hipLaunchKernelGGL(fused_merge_kernel, dim3(rbp::ceil_div(Tn, kMergeTokens)), dim3(256), 0, s,
+                       w.pM, w.pS, w.pE, Tc, (int32_t)(Vp / 128), Hc, W, tokens + t0, sq, Tn, d, V,
+                       logp + t0, lse + t0, entropy ? entropy + t0 : nullptr);
+    RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+    const int st = policy_loss_fwd_bwd(logp + t0, old_logp + t0, sq, adv, seq_len, Tn, B,
+                                       n_seq_total, eps_low, eps_high, loss_accum, dlogp + t0,
+                                       stats, w.loss, w.loss_bytes, stream);
+    if (st != RBP_OK) return st;
+    hipLaunchKernelGGL(grad_scale_kernel,
+                       dim3(rbp::ceil_div(T256, kScaleTokens), (unsigned)(Vp / 128)), dim3(256), 0,
+                       s, w.Qt, Tc, T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0, tokens + t0,
+                       sq, Tn, V);
+    rbp::launch_grad_products(Hc, W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, dW,
+                              (accumulate_dW || t0 > 0) ? 1 : 0, s);
+  }
+  RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+  return RBP_OK;
+}

@@ -23,96 +23,17 @@
 // 256 x 256 workgroup per CU), reading W and H in place.  No floating-point
 // atomics are used, so results are bitwise reproducible.
 
-#include <cmath>
-
-#include "gemm_core.h"
-#include "gemm_dma.h"
+#include "logits_epilogue.h"
 #include "rbp_internal.h"
 
 namespace {
 
-using rbp::gemm::f32x16;
+using namespace rbp::lp;
 using rbp::gemm::kLdsBytes;
 using rbp::gemm::Tile;
 using rbp::gemm::tile_stream;
 using rbp::gemm::map_tile;
 using rbp::gemm::Operand;
-
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kGroupLogits = 4;
-constexpr int kGroupGrad = 8;
-
-// Every product runs on the 8-wave grid (two waves per SIMD).
-using GL = rbp::gemm::Grid8;
-#define RBP_LOGITS_KERNEL                                                        \
-  __global__ __attribute__((amdgpu_flat_work_group_size(GL::kThreads, GL::kThreads), \
-                            amdgpu_waves_per_eu(GL::kWaves / 4, GL::kWaves / 4)))
-
-// 2^x on the hardware unit (v_exp_f32, ~1 ulp).  Arguments here are
-// (z - max) * log2 e <= 0; below -126 the result flushes toward zero, which
-// only drops terms under 2^-126 of the largest one in a sum.
-__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
-
-__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
-  return __uint_as_float((uint32_t)b << 16);
-}
-
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const __bf16 a = (__bf16)lo, b = (__bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
-}
-
-// (a & mask) | (b & ~mask) with mask = all ones where x < 0: written as two
-// vector bit instructions in assembly, because the compiler would otherwise
-// turn the sign test into a compare whose lane mask lives in scalar registers
-// (64 of them live at once overflow the scalar file); volatile so that the
-// masked values are recomputed where used rather than kept live.
-__device__ __forceinline__ uint32_t select_neg(int32_t x, uint32_t a, uint32_t b) {
-  uint32_t m, r;
-  asm volatile("v_ashrrev_i32 %0, 31, %1" : "=v"(m) : "v"(x));
-  asm volatile("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(a), "v"(b));
-  return r;
-}
-
-// acc, or -inf where the row is past the vocabulary (row_off >= lim): mask
-// arithmetic rather than compares, whose masks would pile up in scalar
-// registers.
-template <bool kFull>
-__device__ __forceinline__ float logit_or_ninf(float v, int off, int32_t lim) {
-  if constexpr (kFull) return v;
-  return __uint_as_float(select_neg(off - lim, __float_as_uint(v), 0xff800000u));
-}
-
-// Per token column of this wave's 128 x 64 block: max and sum exp(z - max)
-// over the lane pair's rows (lanes l and l + 32 hold the same column).
-template <bool kFull>
-__device__ __forceinline__ void column_stats(const f32x16 (&acc)[GL::MI][GL::NI], int32_t lim,
-                                             float (&mx)[GL::NI], float (&sum)[GL::NI]) {
-#pragma unroll
-  for (int ni = 0; ni < GL::NI; ++ni) {
-    float m = -INFINITY;
-#pragma unroll
-    for (int mi = 0; mi < GL::MI; ++mi)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        m = fmaxf(m, logit_or_ninf<kFull>(acc[mi][ni][r], GL::row_off(mi, r), lim));
-    m = fmaxf(m, __shfl_xor(m, 32, 64));
-    // a column with no real row (tail tile) has m = -inf: offset 0 keeps the
-    // exponentials at exp(-inf) = 0 instead of NaN
-    const float mb = (kFull || m != -INFINITY) ? m * kLog2e : 0.0f;
-    float s4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int mi = 0; mi < GL::MI; ++mi)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        s4[r & 3] += exp2_hw(
-            fmaf(logit_or_ninf<kFull>(acc[mi][ni][r], GL::row_off(mi, r), lim), kLog2e, -mb));
-    float sm = (s4[0] + s4[1]) + (s4[2] + s4[3]);
-    sm += __shfl_xor(sm, 32, 64);
-    mx[ni] = m;
-    sum[ni] = sm;
-  }
-}
 
 // Forward: per 256 x 256 tile, the partial (max, sum exp) of each token
 // column over the tile's 256 vocabulary rows.
@@ -164,35 +85,6 @@ RBP_LOGITS_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
   tile_stream<GL, false, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
 }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
-}
-
-// h . w over d bf16 elements (d % 8 == 0), one wave cooperating; every lane
-// returns the full sum.
-__device__ __forceinline__ float dot_bf16_wave(const uint16_t* __restrict__ h,
-                                               const uint16_t* __restrict__ w, int32_t d,
-                                               int lane) {
-  float z = 0.0f;
-  for (int c = lane; c < d / 8; c += 64) {
-    const uint4 hv = *reinterpret_cast<const uint4*>(h + c * 8);
-    const uint4 wv = *reinterpret_cast<const uint4*>(w + c * 8);
-    const uint32_t hh[4] = {hv.x, hv.y, hv.z, hv.w}, ww[4] = {wv.x, wv.y, wv.z, wv.w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      z = fmaf(bf16_to_f32((uint16_t)(hh[q] & 0xffff)), bf16_to_f32((uint16_t)(ww[q] & 0xffff)), z);
-      z = fmaf(bf16_to_f32((uint16_t)(hh[q] >> 16)), bf16_to_f32((uint16_t)(ww[q] >> 16)), z);
-    }
-  }
-  return wave_sum(z);
-}
 
 // One wave per token: merge the partials into lse, dot h_t . W_{y_t}.
 __global__ void __launch_bounds__(256) lse_merge_kernel(
@@ -235,110 +127,6 @@ __global__ void __launch_bounds__(256) lse_merge_kernel(
 // The tile pass writes -dlogp_t p_{t,v} everywhere; the one target entry of
 // each token is then overwritten by target_dz_kernel.  Masked and padding
 // tokens get dz = 0 (p is evaluated against lse = +inf).
-//
-// A lane holds four consecutive vocabulary rows v0..v0+3 of one token.  The
-// four lanes of a quad (tokens t0..t0+3) transpose their 4 x 4 block with two
-// lane exchanges (DPP quad permutes; 16-bit halves regrouped with byte
-// permutes), after which lane j of the quad holds row v0 + j for tokens
-// t0..t0+3: one 8-byte store (see dz_rows for the grouping into whole cache
-// lines).  Stores go through a per-tile buffer resource, so every address is
-// a 32-bit offset from the tile's corner.
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ uint32_t quad_xor1(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xf, 0xf, false);  // [1,0,3,2]
-}
-__device__ __forceinline__ uint32_t quad_xor2(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xf, 0xf, false);  // [2,3,0,1]
-}
-// byte permute: selector byte k picks byte k of the result from
-// {hi (bytes 4..7), lo (bytes 0..3)}
-__device__ __forceinline__ uint32_t byte_perm(uint32_t hi, uint32_t lo, uint32_t sel) {
-  return __builtin_amdgcn_perm(hi, lo, sel);
-}
-
-// Selectors of the quad transpose for lane position j = lane % 4.
-struct QuadSel {
-  uint32_t send1, pick, send2, w0, w1;
-  __device__ __forceinline__ QuadSel() {
-    const int j = threadIdx.x & 3;
-    const bool lo2 = j < 2, ev = (j & 1) == 0;
-    send1 = lo2 ? 0x07060504u : 0x03020100u;  // lanes 0, 1 send rows 2, 3
-    pick = lo2 ? 0x03020100u : 0x07060504u;
-    send2 = ev ? 0x07060302u : 0x05040100u;
-    w0 = ev ? 0x05040100u : 0x03020504u;
-    w1 = ev ? 0x07060100u : 0x03020706u;
-  }
-};
-
-// Cache policy of the dz^T stores: non-temporal.  32 tiles per XCD write 4 MB
-// per round -- the whole L2 -- and, cached normally, would evict the operand
-// rows the next tiles share (measured: 1.1 ms of 15.5 at T=16384, V=152064).
-constexpr int kStreamStore = 2;
-
-// -dl p -> bf16 for four consecutive rows of one token, packed in pairs.
-template <bool kFull>
-__device__ __forceinline__ void dz_pack(const f32x16& acc, float ls, float dl, int mi, int rg,
-                                        int32_t lim, uint32_t& P0, uint32_t& P1) {
-  float g[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    g[i] = -dl * exp2_hw(fmaf(acc[rg * 4 + i], kLog2e, -ls));
-    if constexpr (!kFull)  // rows past the vocabulary hold zeros
-      g[i] = __uint_as_float(select_neg(GL::row_off(mi, rg * 4 + i) - lim,
-                                        __float_as_uint(g[i]), 0u));
-  }
-  P0 = pack_bf16x2(g[0], g[1]);
-  P1 = pack_bf16x2(g[2], g[3]);
-}
-
-// 4 x 4 transpose inside each lane quad: in, lane j holds rows r..r+3 of
-// token t0 + j as (P0 = rows r, r+1; P1 = rows r+2, r+3); out, row r + j of
-// tokens t0..t0+3 as (w0 = tokens 0, 1; w1 = tokens 2, 3).
-__device__ __forceinline__ void quad_transpose(uint32_t P0, uint32_t P1, const QuadSel& qs,
-                                               uint32_t& w0, uint32_t& w1) {
-  // step 1 (partner j ^ 2): lanes 0, 1 keep rows r, r+1 and get their
-  // partner's; lanes 2, 3 keep rows r+2, r+3.  A / B = this row pair for
-  // tokens (j & 1) and (j & 1) + 2.
-  const uint32_t r1 = quad_xor2(byte_perm(P1, P0, qs.send1));
-  const uint32_t Ah = byte_perm(r1, P0, qs.pick);
-  const uint32_t Bh = byte_perm(P1, r1, qs.pick);
-  // step 2 (partner j ^ 1): even lanes collect the first row of the pair,
-  // odd lanes the second
-  const uint32_t r2 = quad_xor1(byte_perm(Bh, Ah, qs.send2));
-  w0 = byte_perm(r2, Ah, qs.w0);
-  w1 = byte_perm(r2, Bh, qs.w1);
-}
-
-// One 32-row block of both 32-token column blocks of a wave (NI == 2).
-// Lanes 0..31 hold rows 0..3 (+8 rg) of their token, lanes 32..63 rows 4..7;
-// a lane-half swap (v_permlane32_swap) first regroups them so that lanes
-// 0..31 hold the first column block and lanes 32..63 the second, for the
-// same four rows: each store then writes 4 rows x 128 contiguous bytes, whole
-// cache lines.
-template <bool kFull>
-__device__ __forceinline__ void dz_rows(const f32x16 (&acc)[GL::MI][GL::NI], const float (&ls)[2],
-                                        const float (&dl)[2], int mi, int32_t lim,
-                                        const QuadSel& qs, __amdgpu_buffer_rsrc_t rGt,
-                                        uint32_t off, int64_t ldGt) {
-  static_assert(GL::NI == 2, "two column blocks per wave");
-#pragma unroll
-  for (int rg = 0; rg < 4; ++rg) {
-    uint32_t X0, X1, Y0, Y1;  // column block 0 / 1, rows (0,1) / (2,3) of the lane's half
-    dz_pack<kFull>(acc[mi][0], ls[0], dl[0], mi, rg, lim, X0, X1);
-    dz_pack<kFull>(acc[mi][1], ls[1], dl[1], mi, rg, lim, Y0, Y1);
-    const auto s0 = __builtin_amdgcn_permlane32_swap(X0, Y0, false, false);
-    const auto s1 = __builtin_amdgcn_permlane32_swap(X1, Y1, false, false);
-    // s0[0], s1[0]: rows 0..3 of the group; s0[1], s1[1]: rows 4..7
-    uint32_t w0, w1;
-    const int ro = mi * 32 + rg * 8;  // first row of the 8-row group within the wave's block
-    quad_transpose(s0[0], s1[0], qs, w0, w1);
-    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rGt, off, (int)(ro * ldGt * 2), kStreamStore);
-    quad_transpose(s0[1], s1[1], qs, w0, w1);
-    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rGt, off, (int)((ro + 4) * ldGt * 2),
-                                          kStreamStore);
-  }
-}
 
 RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
                                           const uint16_t* __restrict__ Hc, int64_t Tn,
@@ -528,17 +316,6 @@ __global__ void __launch_bounds__(256) fill_zero_kernel(float* __restrict__ p, i
     p[i] = 0.0f;
 }
 
-int64_t round256(int64_t x) { return (x + 255) / 256 * 256; }
-
-// Compute units of the current device (the persistent products launch one
-// workgroup per CU).
-int device_cus() {
-  int dev = 0, n = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
-    n = 256;
-  return n;
-}
 
 }  // namespace
 
@@ -596,6 +373,40 @@ extern "C" int policy_logprob_fwd(const uint16_t* hidden, const uint16_t* W,
   return RBP_OK;
 }
 
+void rbp::launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint16_t* Gt,
+                               int64_t ldGt, int64_t Tn, int32_t d, int32_t V, float* dhidden_c,
+                               float* dh_half, float* dW, int accumulate, hipStream_t s) {
+  const int64_t tiles_d = rbp::ceil_div(d, 256), tiles_v = round256(V) / 256;
+  if (Tn == 0) {
+    if (!accumulate) {
+      const int64_t n = (int64_t)V * d;
+      int64_t blocks = rbp::ceil_div(n, 256);
+      if (blocks > 65536) blocks = 65536;
+      hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, s, dW, n);
+    }
+    return;
+  }
+  const int n_cu = device_cus();
+  const int64_t tiles_t = rbp::ceil_div(Tn, 256);
+  // dhidden in two K halves when one pass would give each CU only a few
+  // tiles (the last, partly empty round would then cost a large share)
+  const int64_t tiles_dh = tiles_d * tiles_t;
+  const int splits = tiles_dh < 4 * (int64_t)n_cu && V >= 512 ? 2 : 1;
+  const int64_t k_split = splits == 2 ? (rbp::ceil_div(V, 2) + 63) / 64 * 64 : V;
+  hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(tiles_dh * splits, n_cu)),
+                     dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, k_split, splits, dhidden_c,
+                     dh_half, tiles_d, tiles_t);
+  if (splits == 2) {
+    const int64_t n4 = Tn * d / 4;
+    int64_t blocks = rbp::ceil_div(n4, 256);
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(add_f32_kernel, dim3(blocks), dim3(256), 0, s, dhidden_c, dh_half, n4);
+  }
+  hipLaunchKernelGGL(dweight_kernel, dim3(rbp::gemm::stream_grid(tiles_d * tiles_v, n_cu)),
+                     dim3(GL::kThreads), 0, s, Hc, Gt, ldGt, Tn, d, V, dW, accumulate, tiles_d,
+                     tiles_v);
+}
+
 extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
                                   const int32_t* tokens, const int32_t* seq_of_token,
                                   const float* lse, const float* dlogp, int64_t T, int32_t d,
@@ -609,16 +420,10 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
   RBP_REQUIRE(T == 0 || (hidden && tokens && lse && dlogp && dhidden), RBP_EINVAL,
               "policy_logprob_bwd: null pointer");
   hipStream_t s = rbp::as_stream(stream);
-  const int64_t Vp = round256(V);
-  const int64_t tiles_d = rbp::ceil_div(d, 256), tiles_v = Vp / 256;
   if (T == 0) {
-    if (!accumulate_dW) {
-      const int64_t n = (int64_t)V * d;
-      int64_t blocks = rbp::ceil_div(n, 256);
-      if (blocks > 65536) blocks = 65536;
-      hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, s, dW, n);
-      RBP_CHECK_LAUNCH("policy_logprob_bwd");
-    }
+    rbp::launch_grad_products(nullptr, W, nullptr, 0, 0, d, V, nullptr, nullptr, dW,
+                              accumulate_dW, s);
+    RBP_CHECK_LAUNCH("policy_logprob_bwd");
     return RBP_OK;
   }
   // largest chunk (multiple of 256 tokens) whose workspace fits
@@ -639,6 +444,7 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
               "policy_logprob_bwd: workspace of %zu bytes holds no 256-token chunk (needs %zu)",
               ws_bytes, rbp::logprob_bwd_ws(256, d, V));
   const BwdWs w = carve_bwd(ws, Tc, d, V);
+  const int64_t tiles_v = round256(V) / 256;
   const int n_cu = device_cus();
   for (int64_t t0 = 0; t0 < T; t0 += Tc) {
     const int64_t Tn = (T - t0) < Tc ? (T - t0) : Tc;
@@ -651,24 +457,8 @@ extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
     hipLaunchKernelGGL(target_dz_kernel, dim3(rbp::ceil_div(Tn, 4)), dim3(256), 0, s, Hc, W,
                        tokens + t0, seq_of_token ? seq_of_token + t0 : nullptr, lse + t0,
                        dlogp + t0, Tn, d, V, w.Gt, Tc);
-    // dhidden in two K halves when one pass would give each CU only a few
-    // tiles (the last, partly empty round would then cost a large share)
-    const int64_t tiles_dh = tiles_d * tiles_t;
-    const int splits = tiles_dh < 4 * (int64_t)n_cu && V >= 512 ? 2 : 1;
-    const int64_t k_split = splits == 2 ? (rbp::ceil_div(V, 2) + 63) / 64 * 64 : V;
-    hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(tiles_dh * splits, n_cu)),
-                       dim3(GL::kThreads), 0, s, W, w.Gt, Tc, Tn, d, V, k_split, splits,
-                       dhidden + t0 * d, w.dh_half, tiles_d, tiles_t);
-    if (splits == 2) {
-      const int64_t n4 = Tn * d / 4;
-      int64_t blocks = rbp::ceil_div(n4, 256);
-      if (blocks > 8192) blocks = 8192;
-      hipLaunchKernelGGL(add_f32_kernel, dim3(blocks), dim3(256), 0, s, dhidden + t0 * d,
-                         w.dh_half, n4);
-    }
-    hipLaunchKernelGGL(dweight_kernel, dim3(rbp::gemm::stream_grid(tiles_d * tiles_v, n_cu)),
-                       dim3(GL::kThreads), 0, s, Hc, w.Gt, Tc, Tn, d, V, dW,
-                       (accumulate_dW || t0 > 0) ? 1 : 0, tiles_d, tiles_v);
+    rbp::launch_grad_products(Hc, W, w.Gt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, dW,
+                              (accumulate_dW || t0 > 0) ? 1 : 0, s);
   }
   RBP_CHECK_LAUNCH("policy_logprob_bwd");
   return RBP_OK;

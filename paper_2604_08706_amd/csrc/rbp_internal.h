@@ -39,6 +39,15 @@ size_t logprob_fwd_ws(int64_t T, int32_t V);
 size_t loss_ws(int64_t T);
 size_t loss_seq_ws(int64_t B);
 size_t logprob_bwd_ws(int64_t Tc, int32_t d, int32_t V);
+size_t fused_ws(int64_t Tc, int32_t d, int32_t V);
+
+// The two products of the log-prob backward for one chunk of Tn tokens, from
+// dz^T (bf16 [round256(V)][ldGt], columns Tn..round256(Tn) zero):
+// dhidden_c [Tn][d] overwritten (dh_half: fp32 [ldGt][d] scratch), dW [V][d]
+// overwritten or accumulated.  Tn = 0 only zeroes dW (unless accumulating).
+void launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint16_t* Gt,
+                          int64_t ldGt, int64_t Tn, int32_t d, int32_t V, float* dhidden_c,
+                          float* dh_half, float* dW, int accumulate, hipStream_t s);
 
 }  // namespace rbp
 

@@ -1,0 +1,206 @@
+"""GPU parity of policy_fused_fwd_bwd (forward, loss, backward and entropy in
+one pass) against the oracle: logp, lse and entropy within 2e-3 absolute;
+loss within 1e-2 relative; dlogp, dhidden and dW within 1e-2 relative L2."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.grad import dW_from_rows, dhidden_rows, dz_rows, logprob_backward
+from oracle.logprob import entropy, logprob, logprob_rows
+from oracle.loss import grpo_loss
+from paper_2604_08706_amd import workloads as wlm
+
+from gpu_util import bf16_to_f64, rel_l2, require_gpu, to_np
+
+pytestmark = pytest.mark.gpu
+
+ATOL = 2e-3
+RTOL = 1e-2
+
+
+def _sequences(T, seed, masked=0.1, mean_len=40):
+    """Packed sequences covering T tokens (ids in order), some tokens masked."""
+    rng = np.random.default_rng(seed)
+    lens = []
+    while sum(lens) < T:
+        lens.append(int(max(1, rng.poisson(mean_len))))
+    lens[-1] -= sum(lens) - T
+    if lens[-1] == 0:
+        lens.pop()
+    seq = np.repeat(np.arange(len(lens)), lens).astype(np.int32)
+    seq[rng.random(T) < masked] = -1
+    return seq, np.array(lens, dtype=np.int32)
+
+
+def _run(rbp, hidden, W, tokens, seq, old, adv, slen, n_seq, ws_tokens=None, dW0=None,
+         want_entropy=True):
+    T, d = hidden.shape
+    V = W.shape[0]
+    out = {k: torch.empty(T, device="cuda") for k in ("logp", "lse", "dlogp")}
+    out["entropy"] = torch.empty(T, device="cuda") if want_entropy else None
+    out["loss"] = torch.full((1,), 0.25, device="cuda")
+    out["stats"] = torch.zeros(4, device="cuda")
+    out["dh"] = torch.empty((T, d), device="cuda")
+    out["dW"] = torch.empty((V, d), device="cuda") if dW0 is None else dW0.clone()
+    ws = rbp.workspace(rbp.RBP_OP_FUSED, T if ws_tokens is None else ws_tokens, d, V)
+    rbp.policy_fused_fwd_bwd(hidden, W, tokens, seq, old, adv, slen, n_seq, out["logp"],
+                             out["lse"], out["entropy"], out["loss"], out["dlogp"],
+                             out["stats"], out["dh"], out["dW"], ws,
+                             accumulate_dW=dW0 is not None)
+    torch.cuda.synchronize()
+    return out
+
+
+def _case(T, d, V, w_sd, seed, device="cpu"):
+    hidden, W, tokens = wlm.head(T, d, V, seed=seed, w_sd=w_sd, device=device)
+    seq, lens = _sequences(T, seed + 1)
+    h64, W64, y = bf16_to_f64(hidden), bf16_to_f64(W), to_np(tokens)
+    want_logp, want_lse = logprob(h64, W64, y, seq)
+    # behaviour log-probs: the oracle's plus staleness noise, stored as fp32
+    old = (want_logp + wlm.normal(T, 0.1, seed + 2).numpy()).astype(np.float32)
+    adv = wlm.normal(len(lens), 1.0, seed + 3).numpy()
+    return hidden, W, tokens, seq, lens, h64, W64, y, want_logp, want_lse, old, adv
+
+
+def _check(out, h64, W64, y, seq, lens, want_logp, want_lse, old, adv, n_seq, loss0=0.25,
+           dW_extra=None):
+    assert np.abs(to_np(out["logp"]) - want_logp).max() < ATOL
+    assert np.abs(to_np(out["lse"]) - want_lse).max() < ATOL
+    if out["entropy"] is not None:
+        want_H = entropy(h64, W64, seq)
+        assert np.abs(to_np(out["entropy"]) - want_H).max() < ATOL
+    loss, dlogp, st = grpo_loss(want_logp, old, seq, adv, lens, n_seq)
+    assert abs(to_np(out["loss"])[0] - loss0 - loss) <= RTOL * max(abs(loss), 1e-6)
+    assert rel_l2(to_np(out["dlogp"]), dlogp) < RTOL
+    assert to_np(out["stats"])[2] == st[2]
+    want_dh, want_dW = logprob_backward(h64, W64, y, want_lse, dlogp, seq)
+    if dW_extra is not None:
+        want_dW = want_dW + dW_extra
+    assert rel_l2(to_np(out["dh"]), want_dh) < RTOL
+    assert rel_l2(to_np(out["dW"]), want_dW) < RTOL
+    assert np.all(to_np(out["dh"])[seq < 0] == 0)
+
+
+SHAPES = [(1, 8, 1), (37, 8, 300), (300, 72, 1000), (513, 136, 2049), (1000, 264, 4097)]
+
+
+@pytest.mark.parametrize("T,d,V", SHAPES)
+@pytest.mark.parametrize("w_sd", [0.02, 1.0])
+def test_fused_small_shapes(T, d, V, w_sd):
+    rbp = require_gpu()
+    print(f"[fused] T={T} d={d} V={V} w_sd={w_sd}", flush=True)
+    (hidden, W, tokens, seq, lens, h64, W64, y, want_logp, want_lse, old,
+     adv) = _case(T, d, V, w_sd, T + d + V)
+    n_seq = len(lens) + 3
+    out = _run(rbp, hidden.cuda(), W.cuda(), tokens.cuda(), torch.from_numpy(seq).cuda(),
+               torch.from_numpy(old).cuda(), torch.from_numpy(adv).cuda(),
+               torch.from_numpy(lens).cuda(), n_seq)
+    _check(out, h64, W64, y, seq, lens, want_logp, want_lse, old, adv, n_seq)
+
+
+def test_fused_real_vocab_chunked_and_accumulating():
+    """Real vocabulary (151936: a V tail), then 256-token chunks with dW
+    accumulation and no entropy output."""
+    rbp = require_gpu()
+    wl = wlm.WORKLOADS["head05b"]
+    T = 700
+    print(f"[fused] head05b T={T}", flush=True)
+    (hidden, W, tokens, seq, lens, h64, W64, y, want_logp, want_lse, old,
+     adv) = _case(T, wl.d, wl.V, 0.02, 21, device="cuda")
+    n_seq = len(lens)
+    args = (rbp, hidden, W, tokens, torch.from_numpy(seq).cuda(), torch.from_numpy(old).cuda(),
+            torch.from_numpy(adv).cuda(), torch.from_numpy(lens).cuda(), n_seq)
+    out = _run(*args)
+    _check(out, h64, W64, y, seq, lens, want_logp, want_lse, old, adv, n_seq)
+    dW0 = wlm.normal((wl.V, wl.d), 1e-4, 7, device="cuda")
+    out2 = _run(*args, ws_tokens=256, dW0=dW0, want_entropy=False)
+    _check(out2, h64, W64, y, seq, lens, want_logp, want_lse, old, adv, n_seq,
+           dW_extra=to_np(dW0).astype(np.float64))
+
+
+def test_fused_head7b_full_size_sampled_rows():
+    """T = 16384, d = 3584, V = 152064 in one chunk.  Only three short
+    sequences have a nonzero advantage, so dlogp, dhidden and dW involve their
+    rows alone and the oracle computes them row by row."""
+    rbp = require_gpu()
+    wl = wlm.WORKLOADS["head7b"]
+    T = 16384
+    print("[fused] head7b full size", flush=True)
+    hidden, W, tokens = wlm.head(T, wl.d, wl.V, seed=0, device="cuda")
+    lens = np.full(T // 64, 64, dtype=np.int32)
+    seq = np.repeat(np.arange(len(lens)), lens).astype(np.int32)
+    live = [0, 100, len(lens) - 1]  # first, middle and last sequence
+    lens[live] = [7, 9, 11]  # full lengths; their remaining tokens are masked
+    rows = np.concatenate([np.arange(64 * s, 64 * s + lens[s]) for s in live])
+    mask_rows = np.concatenate([np.arange(64 * s + lens[s], 64 * s + 64) for s in live])
+    seq[mask_rows] = -1
+    adv = np.zeros(len(lens), dtype=np.float32)
+    adv[live] = [1.0, -0.7, 0.4]
+    check_rows = np.concatenate([rows, [1000, 5000, 9999]])
+    h64 = hidden[torch.from_numpy(check_rows).cuda()].cpu().to(torch.float64).numpy()
+    W64 = bf16_to_f64(W)
+    y = to_np(tokens)[check_rows]
+    want_logp, want_lse = logprob_rows(h64, W64, y, range(len(check_rows)))
+    rng = np.random.default_rng(1)
+    old = np.full(T, -5.0, dtype=np.float32)
+    old[check_rows] = (want_logp + rng.normal(0, 0.1, len(check_rows))).astype(np.float32)
+    n_seq = len(lens)
+    out = _run(rbp, hidden, W, tokens, torch.from_numpy(seq).cuda(),
+               torch.from_numpy(old).cuda(), torch.from_numpy(adv).cuda(),
+               torch.from_numpy(lens).cuda(), n_seq)
+    assert np.abs(to_np(out["logp"])[check_rows] - want_logp).max() < ATOL
+    assert np.abs(to_np(out["lse"])[check_rows] - want_lse).max() < ATOL
+    want_H = entropy(h64, W64)
+    assert np.abs(to_np(out["entropy"])[check_rows] - want_H).max() < ATOL
+    assert np.all(to_np(out["logp"])[mask_rows] == 0)
+    k = len(rows)
+    _, dl_rows, _ = grpo_loss(want_logp[:k], old[rows], seq[rows], adv, lens, n_seq)
+    dl = to_np(out["dlogp"])
+    assert rel_l2(dl[rows], dl_rows) < RTOL
+    others = np.ones(T, dtype=bool)
+    others[rows] = False
+    assert np.all(dl[others] == 0)
+    dh = to_np(out["dh"])
+    assert np.all(dh[others] == 0)
+    dz = dz_rows(h64[:k], W64, y[:k], want_lse[:k], dl_rows, range(k))
+    want_dh = dhidden_rows(h64[:k], W64, y[:k], want_lse[:k], dl_rows, range(k), dz=dz)
+    assert rel_l2(dh[rows], want_dh) < RTOL
+    num = den = 0.0
+    for v0 in range(0, wl.V, 16384):
+        v1 = min(v0 + 16384, wl.V)
+        want = dW_from_rows(h64[:k], W64, y[:k], want_lse[:k], dl_rows, range(k), v0, v1, dz=dz)
+        got = out["dW"][v0:v1].cpu().numpy().astype(np.float64)
+        num += ((got - want) ** 2).sum()
+        den += (want ** 2).sum()
+    assert np.sqrt(num / den) < RTOL
+    del hidden, W, out
+    torch.cuda.empty_cache()
+
+
+def test_fused_reproducible_empty_and_bad_args():
+    rbp = require_gpu()
+    T, d, V = 600, 128, 3000
+    (hidden, W, tokens, seq, lens, *_rest) = _case(T, d, V, 0.02, 5, device="cuda")
+    old, adv = _rest[-2], _rest[-1]
+    args = (rbp, hidden, W, tokens, torch.from_numpy(seq).cuda(), torch.from_numpy(old).cuda(),
+            torch.from_numpy(adv).cuda(), torch.from_numpy(lens).cuda(), len(lens))
+    a, b = _run(*args), _run(*args)
+    for key in ("logp", "lse", "entropy", "loss", "dlogp", "stats", "dh", "dW"):
+        assert torch.equal(a[key], b[key]), key
+    # T = 0 zeroes dW (overwrite mode)
+    dW = torch.full((V, d), 3.0, device="cuda")
+    e0 = torch.empty(0, device="cuda")
+    rbp.policy_fused_fwd_bwd(hidden[:0], W, tokens[:0], torch.empty(0, dtype=torch.int32,
+                                                                     device="cuda"),
+                             e0, args[6], args[7], len(lens), e0, e0, None,
+                             torch.zeros(1, device="cuda"), e0, torch.zeros(4, device="cuda"),
+                             torch.empty((0, d), device="cuda"), dW, None)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(dW).item() == 0
+    with pytest.raises(rbp.RbpError) as e:
+        rbp.policy_fused_fwd_bwd(hidden, W, tokens, args[4], args[5], args[6], args[7], len(lens),
+                                 a["logp"], a["lse"], None, a["loss"], a["dlogp"], a["stats"],
+                                 a["dh"], a["dW"],
+                                 torch.empty(16, dtype=torch.uint8, device="cuda"))
+    assert e.value.status == rbp.RBP_EWORKSPACE
