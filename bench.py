@@ -35,7 +35,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # read for a plain copy of known size (--copy-probe-mib: a 1 GiB copy reads
 # 524302 KiB of FETCH_SIZE, factor 2.0, and 1048576 KiB of WRITE_SIZE, factor
 # 1.0).  Only valid for the sources the counters were read on.
-TRAFFIC_SOURCES = ("logprob.hip", "gemm_core.h", "gemm_dma.h")
+TRAFFIC_SOURCES = ("logprob.hip", "logits_epilogue.h", "gemm_core.h", "gemm_dma.h")
 TRAFFIC = {
     "sources_sha256": "e294450e0a07a15b59a31e2bcb60ef1b2e933ee15a5d505613f2fad2673d0fbb",
     "fetch_bytes": {"logits_lse_partial_kernel": 27484116608,   # 13420347 KiB x 2.0

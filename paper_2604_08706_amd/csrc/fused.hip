@@ -37,8 +37,71 @@ using rbp::gemm::Operand;
 using rbp::gemm::Tile;
 using rbp::gemm::tile_stream;
 
+// Per token column of this wave's 128 x 64 block: the max over the lane
+// pair's rows (lanes l and l + 32 hold the same column).
+template <bool kFull>
+__device__ __forceinline__ void column_max(const f32x16 (&acc)[GL::MI][GL::NI], int32_t lim,
+                                           float (&mx)[GL::NI]) {
+#pragma unroll
+  for (int ni = 0; ni < GL::NI; ++ni) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int mi = 0; mi < GL::MI; ++mi)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        m = fmaxf(m, logit_or_ninf<kFull>(acc[mi][ni][r], GL::row_off(mi, r), lim));
+    mx[ni] = fmaxf(m, __shfl_xor(m, 32, 64));
+  }
+}
+
+// q = exp(z - M) for four consecutive rows of one token, packed to bf16 pairs;
+// the fp32 q and q z are added to the column's sums (rows past the vocabulary
+// hold q = 0).
+template <bool kFull>
+__device__ __forceinline__ void q_pack(const f32x16& acc, float ls, int mi, int rg, int32_t lim,
+                                       uint32_t& P0, uint32_t& P1, float& S, float& E) {
+  float q[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float z = acc[rg * 4 + i];
+    q[i] = exp2_hw(fmaf(z, kLog2e, -ls));
+    if constexpr (!kFull)
+      q[i] = __uint_as_float(select_neg(GL::row_off(mi, rg * 4 + i) - lim,
+                                        __float_as_uint(q[i]), 0u));
+    S += q[i];
+    E = fmaf(q[i], z, E);
+  }
+  P0 = pack_bf16x2(q[0], q[1]);
+  P1 = pack_bf16x2(q[2], q[3]);
+}
+
+// dz_rows of the backward with q in place of dz, plus the sums.
+template <bool kFull>
+__device__ __forceinline__ void q_rows(const f32x16 (&acc)[GL::MI][GL::NI], const float (&ls)[2],
+                                       int mi, int32_t lim, const QuadSel& qs,
+                                       __amdgpu_buffer_rsrc_t rQ, uint32_t off, int64_t ldQ,
+                                       float (&S)[2], float (&E)[2]) {
+  static_assert(GL::NI == 2, "two column blocks per wave");
+#pragma unroll
+  for (int rg = 0; rg < 4; ++rg) {
+    uint32_t X0, X1, Y0, Y1;
+    q_pack<kFull>(acc[mi][0], ls[0], mi, rg, lim, X0, X1, S[0], E[0]);
+    q_pack<kFull>(acc[mi][1], ls[1], mi, rg, lim, Y0, Y1, S[1], E[1]);
+    const auto s0 = __builtin_amdgcn_permlane32_swap(X0, Y0, false, false);
+    const auto s1 = __builtin_amdgcn_permlane32_swap(X1, Y1, false, false);
+    uint32_t w0, w1;
+    const int ro = mi * 32 + rg * 8;
+    quad_transpose(s0[0], s1[0], qs, w0, w1);
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rQ, off, (int)(ro * ldQ * 2), kStreamStore);
+    quad_transpose(s0[1], s1[1], qs, w0, w1);
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rQ, off, (int)((ro + 4) * ldQ * 2),
+                                          kStreamStore);
+  }
+}
+
 // Step 1: logit tiles -> partials (M, S, E) per (half tile, token) and
-// q = exp(z - M) into Q^T.
+// q = exp(z - M) into Q^T.  One exponential per logit: a max pass, then the
+// store pass, which also sums q and q z.
 RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
                                            const uint16_t* __restrict__ Hc, int64_t Tn,
                                            int32_t d, int32_t V, float* __restrict__ pM,
@@ -60,30 +123,16 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
     const Tile tile = tile_of(vid);
     const int32_t vlim = V - tile.m0;
     const int32_t lim = vlim - GL::row(0, 0);
-    float mx[GL::NI], sum[GL::NI], ez[GL::NI];
+    float mx[GL::NI];
     if (vlim >= 256)
-      column_stats_ent<true>(acc, 0, mx, sum, ez);
+      column_max<true>(acc, 0, mx);
     else
-      column_stats_ent<false>(acc, lim, mx, sum, ez);
-    // lanes l and l + 32 hold the same column's values: the lower half writes
-    // them, 128 contiguous bytes per array and column block
-    const int64_t half = (int64_t)(tile.m0 >> 7) + GL::wm();
-    if (lane < 32) {
+      column_max<false>(acc, lim, mx);
+    // a half tile past the vocabulary has M = -inf: offset 0 keeps its
+    // (discarded) exponentials finite
+    float ls[GL::NI], S[GL::NI] = {0.0f, 0.0f}, E[GL::NI] = {0.0f, 0.0f};
 #pragma unroll
-      for (int ni = 0; ni < GL::NI; ++ni) {
-        const int64_t o = half * ldp + tile.n0 + GL::col(ni);
-        pM[o] = mx[ni];
-        pS[o] = sum[ni];
-        pE[o] = ez[ni];
-      }
-    }
-    // q = exp(z - M) with the store of the backward's dz (g = -dl exp(z - ls))
-    float ls[GL::NI], dl[GL::NI];
-#pragma unroll
-    for (int ni = 0; ni < GL::NI; ++ni) {
-      ls[ni] = mx[ni] == -INFINITY ? 0.0f : mx[ni] * kLog2e;
-      dl[ni] = -1.0f;
-    }
+    for (int ni = 0; ni < GL::NI; ++ni) ls[ni] = mx[ni] == -INFINITY ? 0.0f : mx[ni] * kLog2e;
     const auto rQ = __builtin_amdgcn_make_buffer_rsrc(
         uniform_ptr(Qt + (int64_t)tile.m0 * ldQ + tile.n0), 0, (int)(256 * ldQ * 2), 0x00020000);
     const uint32_t off =
@@ -92,9 +141,23 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
 #pragma unroll
     for (int mi = 0; mi < GL::MI; ++mi) {
       if (vlim >= 256)
-        dz_rows<true>(acc, ls, dl, mi, lim, qs, rQ, off, ldQ);
+        q_rows<true>(acc, ls, mi, lim, qs, rQ, off, ldQ, S, E);
       else
-        dz_rows<false>(acc, ls, dl, mi, lim, qs, rQ, off, ldQ);
+        q_rows<false>(acc, ls, mi, lim, qs, rQ, off, ldQ, S, E);
+    }
+    // both lane halves hold rows of the same columns; the lower half writes
+    // the sums, 128 contiguous bytes per array and column block
+    const int64_t half = (int64_t)(tile.m0 >> 7) + GL::wm();
+#pragma unroll
+    for (int ni = 0; ni < GL::NI; ++ni) {
+      const float s = S[ni] + __shfl_xor(S[ni], 32, 64);
+      const float e = E[ni] + __shfl_xor(E[ni], 32, 64);
+      if (lane < 32) {
+        const int64_t o = half * ldp + tile.n0 + GL::col(ni);
+        pM[o] = mx[ni];
+        pS[o] = s;
+        pE[o] = e;
+      }
     }
   };
   tile_stream<GL, false, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
@@ -116,29 +179,41 @@ __device__ __forceinline__ void merge_partial(float& m, float& s, float& e, floa
   }
 }
 
-// Step 2: 64 tokens per block.  Four waves merge interleaved quarters of each
-// token's partials (coalesced: consecutive lanes read consecutive tokens), the
-// quarters are combined in a fixed order, then each wave forms the target
-// logits of 16 tokens with one dot product each.
+// Step 2: 64 tokens per block of 16 waves.  Wave q merges the partials
+// i = q, q + 16, ... of the block's tokens (coalesced: consecutive lanes read
+// consecutive tokens), the 16 results are combined in a fixed order, then
+// each wave forms the target logits of 4 tokens with one dot product each.
 constexpr int kMergeTokens = 64;
+constexpr int kMergeWaves = 16;
 
-__global__ void __launch_bounds__(256) fused_merge_kernel(
+__global__ void __launch_bounds__(64 * kMergeWaves) fused_merge_kernel(
     const float* __restrict__ pM, const float* __restrict__ pS, const float* __restrict__ pE,
     int64_t ldp, int32_t n_half, const uint16_t* __restrict__ Hc,
     const uint16_t* __restrict__ W, const int32_t* __restrict__ tokens,
     const int32_t* __restrict__ seq, int64_t Tn, int32_t d, int32_t V, float* __restrict__ logp,
     float* __restrict__ lse, float* __restrict__ ent) {
-  __shared__ float sm[4][kMergeTokens], ss[4][kMergeTokens], se[4][kMergeTokens];
+  __shared__ float sm[kMergeWaves][kMergeTokens], ss[kMergeWaves][kMergeTokens],
+      se[kMergeWaves][kMergeTokens];
   __shared__ float sl[kMergeTokens];
   const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
   const int64_t t0 = (int64_t)blockIdx.x * kMergeTokens;
   const int64_t t = t0 + c;
   float m = -INFINITY, s = 0.0f, e = 0.0f;
-  if (t < Tn)
-    for (int32_t i = q; i < n_half; i += 4) {
+  if (t < Tn) {
+    int32_t i = q;
+    // two partials per iteration: their loads are issued together
+    for (; i + kMergeWaves < n_half; i += 2 * kMergeWaves) {
+      const int64_t o0 = (int64_t)i * ldp + t, o1 = o0 + (int64_t)kMergeWaves * ldp;
+      const float M0 = pM[o0], S0 = pS[o0], E0 = pE[o0];
+      const float M1 = pM[o1], S1 = pS[o1], E1 = pE[o1];
+      merge_partial(m, s, e, M0, S0, E0);
+      merge_partial(m, s, e, M1, S1, E1);
+    }
+    if (i < n_half) {
       const int64_t o = (int64_t)i * ldp + t;
       merge_partial(m, s, e, pM[o], pS[o], pE[o]);
     }
+  }
   sm[q][c] = m;
   ss[q][c] = s;
   se[q][c] = e;
@@ -146,7 +221,7 @@ __global__ void __launch_bounds__(256) fused_merge_kernel(
   if (threadIdx.x < kMergeTokens) {
     float M = -INFINITY, S = 0.0f, E = 0.0f;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) merge_partial(M, S, E, sm[k][c], ss[k][c], se[k][c]);
+    for (int k = 0; k < kMergeWaves; ++k) merge_partial(M, S, E, sm[k][c], ss[k][c], se[k][c]);
     const bool valid = t < Tn && (seq == nullptr || seq[t] >= 0);
     const float l = M + logf(S);
     sl[c] = valid ? l : 0.0f;
@@ -157,8 +232,9 @@ __global__ void __launch_bounds__(256) fused_merge_kernel(
   }
   __syncthreads();
   const int lane = threadIdx.x & 63;
-  for (int k = 0; k < kMergeTokens / 4; ++k) {
-    const int cc = q * (kMergeTokens / 4) + k;
+#pragma unroll
+  for (int k = 0; k < kMergeTokens / kMergeWaves; ++k) {
+    const int cc = q * (kMergeTokens / kMergeWaves) + k;
     const int64_t tt = t0 + cc;
     if (tt >= Tn) break;
     if (seq != nullptr && seq[tt] < 0) {
@@ -320,7 +396,8 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
     hipLaunchKernelGGL(logits_store_kernel, dim3(rbp::gemm::stream_grid(tiles_v * tiles_t, n_cu)),
                        dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, w.pM, w.pS, w.pE, Tc, w.Qt, Tc,
                        tiles_v, tiles_t);
-    hipLaunchKernelGGL(fused_merge_kernel, dim3(rbp::ceil_div(Tn, kMergeTokens)), dim3(256), 0, s,
+    hipLaunchKernelGGL(fused_merge_kernel, dim3(rbp::ceil_div(Tn, kMergeTokens)),
+                       dim3(64 * kMergeWaves), 0, s,
                        w.pM, w.pS, w.pE, Tc, (int32_t)(Vp / 128), Hc, W, tokens + t0, sq, Tn, d, V,
                        logp + t0, lse + t0, entropy ? entropy + t0 : nullptr);
     RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");

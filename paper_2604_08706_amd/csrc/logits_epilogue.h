@@ -90,44 +90,6 @@ __device__ __forceinline__ void column_stats(const f32x16 (&acc)[GL::MI][GL::NI]
   }
 }
 
-// column_stats plus, per column, E = sum exp(z - max) z over the same rows
-// (for the entropy H = lse - sum_v p_v z_v).  Rows past the vocabulary have
-// exp(...) = 0 and a finite accumulator (their operand rows read as zero).
-template <bool kFull>
-__device__ __forceinline__ void column_stats_ent(const f32x16 (&acc)[GL::MI][GL::NI], int32_t lim,
-                                                 float (&mx)[GL::NI], float (&sum)[GL::NI],
-                                                 float (&ez)[GL::NI]) {
-#pragma unroll
-  for (int ni = 0; ni < GL::NI; ++ni) {
-    float m = -INFINITY;
-#pragma unroll
-    for (int mi = 0; mi < GL::MI; ++mi)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        m = fmaxf(m, logit_or_ninf<kFull>(acc[mi][ni][r], GL::row_off(mi, r), lim));
-    m = fmaxf(m, __shfl_xor(m, 32, 64));
-    const float mb = (kFull || m != -INFINITY) ? m * kLog2e : 0.0f;
-    float s4[4] = {0.0f, 0.0f, 0.0f, 0.0f}, e4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int mi = 0; mi < GL::MI; ++mi)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float z = acc[mi][ni][r];
-        const float e = exp2_hw(
-            fmaf(logit_or_ninf<kFull>(z, GL::row_off(mi, r), lim), kLog2e, -mb));
-        s4[r & 3] += e;
-        e4[r & 3] = fmaf(e, z, e4[r & 3]);
-      }
-    float sm = (s4[0] + s4[1]) + (s4[2] + s4[3]);
-    float em = (e4[0] + e4[1]) + (e4[2] + e4[3]);
-    sm += __shfl_xor(sm, 32, 64);
-    em += __shfl_xor(em, 32, 64);
-    mx[ni] = m;
-    sum[ni] = sm;
-    ez[ni] = em;
-  }
-}
-
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
