@@ -10,7 +10,7 @@
  * generated (App. D.2).  This library is that trainer-side path for the LM head:
  *
  *   rb_group_advantage   advantages of a freshly generated group     (App. D.2)
- *   rb_sample_gather     draw records and gather their tokens         (Sec. 3.1, 5; App. B, D.3)
+ *   rb_sample_gather     draw records and gather their tokens         (Sec. 3.1, 5; App. B, D.4)
  *   policy_logprob_fwd   log pi(y_t) from hidden states and W         (App. D.2)
  *   policy_loss_fwd_bwd  clipped GRPO loss and d loss / d logp        (App. D.2)
  *   policy_logprob_bwd   d loss / d hidden and d loss / d W           (chain rule of the above)
@@ -70,7 +70,7 @@ enum {
   RB_POS_MIX = 1,    /* per draw, a coin with probability p_pos picks a uniform
                         positive record (reward > 0), else a uniform live record;
                         no positives -> uniform.  Not in the paper.             */
-  RB_POS_RETAIN = 2  /* positive-bias sampling (Sec. 5; App. D.3): uniform over
+  RB_POS_RETAIN = 2  /* positive-bias sampling (Sec. 5; App. D.4): uniform over
                         the freshest n_fresh records plus the freshest
                         n_pos_keep positive records older than those            */
 };
@@ -162,7 +162,7 @@ typedef struct rb_batch {
 /*
  * Draw a training batch from the replay buffer and gather it (Sec. 3.1:
  * sampling does not remove records; Sec. 4: draws are uniform with
- * replacement; Sec. 5 and App. D.3: positive-bias retention).  Draws are
+ * replacement; Sec. 5 and App. D.4: positive-bias retention).  Draws are
  * kept in draw order, duplicates included.
  * Errors: RBP_EINVAL for null pointers, n_live outside [1, capacity], n_draw
  *   outside [1, 2^20], an unknown mode/layout, p_pos_q32 > 2^32, negative

@@ -15,7 +15,7 @@ Training for LLMs with Experience Replay"):
                    paper is silent on the generator.
 * ``buffer``    -- the FIFO replay buffer and its sampling rules
                    (Sec. 3.1; App. B "BufferStructure"; Sec. 5 "Further
-                   optimization" and App. D.3 "Positive-bias sampling").
+                   optimization" and App. D.4 "Positive-bias sampling").
 * ``advantage`` -- group-normalised advantages at insert time (App. D.2).
 * ``logprob``   -- per-token policy log-probabilities from hidden states and the
                    LM-head weight (App. D.2, temperature 1).

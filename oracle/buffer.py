@@ -10,15 +10,27 @@ Paper passages followed:
 * Sec. 4 (synchronous analysis) and App. C.1: a minibatch of B draws is taken
   uniformly from the buffer *with replacement*; the pseudo-code's library call
   samples without replacement -- this build follows the analysis (reading R7).
-* Sec. 5 ("Further optimization") and App. D.3 ("Positive-bias sampling"): with
+* Sec. 5 ("Further optimization") and App. D.4 ("Positive-bias sampling"): with
   coefficient delta the buffer keeps the freshest (1-delta)N rollouts and, among
   the rollouts not in that fresh part, the freshest delta*N correct ones; the
   sampler draws uniformly over what is kept.  delta = 0 is plain uniform.
-  Pinned by the worked example of App. D.3, which the rule reproduces at
+  Pinned by the worked example of App. D.4, which the rule reproduces at
   delta = 0.5 (the example prints 0.75; reading R8).
 * Positive-prioritised mixture (p_pos): not in the paper (reading R9).  A coin
   with probability p_pos picks the positive stratum, otherwise the draw is over
   all live records; with no positives the draw falls back to all records.
+
+* Sampling variants compared in App. E (the "vanilla" / "No replacement" /
+  "No replacement, at least once" figure): uniform *without* replacement, and
+  the same after first taking records never used before.  Defined here as the
+  B records with the smallest per-record random keys (a uniformly random
+  B-subset), listed in slot order; "at least once" ranks never-used records
+  ahead of used ones (reading R17).
+* Steps-since-last-use (App. D.3, "Metrics"): samples are ordered batch by
+  batch, in a random order inside a batch (here: draw order); a sample of a
+  rollout seen for the first time is "new" (-1 here), any later one gets the
+  number of gradient steps since that rollout's previous sample.  Pinned by
+  the paper's worked example.
 
 Record order: slot 0 is the oldest live record, slot n_live-1 the newest.  A
 record is "positive" ("correct") when its reward is > 0 (binary rewards).
@@ -71,7 +83,7 @@ def positive_slots(rewards):
 
 
 def retained_set(rewards, n_fresh, n_pos_keep):
-    """Slots kept by positive-bias retention (Sec. 5; App. D.3).
+    """Slots kept by positive-bias retention (Sec. 5; App. D.4).
 
     The freshest ``n_fresh`` slots are kept; among the older slots, the
     freshest ``n_pos_keep`` positive ones are kept as well.  Returned in
@@ -120,6 +132,43 @@ def sample_indices(rewards, mode, seed, step, n_draw, p_q32=0, n_fresh=0,
                 out.append(philox.uniform_index(x0, n_live))
         else:
             out.append(pool[philox.uniform_index(x0, len(pool))])
+    return out
+
+
+def slot_key(seed, step, s):
+    """63-bit random key of slot ``s`` at sampling step ``step``: the first
+    word of the Philox4x64-10 block with counter (s, step, 1, 0) and key
+    (seed, 0), shifted right by one bit."""
+    return philox.philox4x64((s, step, 1, 0), (seed, 0))[0] >> 1
+
+
+def sample_without_replacement(seed, step, n_live, n_draw, use_count=None):
+    """``n_draw`` distinct slots, ascending.  Plain: the slots with the
+    ``n_draw`` smallest (key, slot) pairs.  With ``use_count`` ("at least
+    once"): slots never used before rank ahead of used ones, i.e. the order is
+    by (used, key, slot)."""
+    if not 1 <= n_draw <= n_live:
+        raise ValueError("need 1 <= n_draw <= n_live without replacement")
+    rank = []
+    for s in range(n_live):
+        used = 0 if use_count is None else int(use_count[s] > 0)
+        rank.append((used, slot_key(seed, step, s), s))
+    rank.sort()
+    return sorted(r[2] for r in rank[:n_draw])
+
+
+def steps_since_last_use(batches):
+    """``batches``: list of (step, rollout ids in draw order), in processing
+    order.  Returns one list per batch: -1 for a rollout's first sample, else
+    the steps since its previous sample (0 for a repeat inside a batch)."""
+    last = {}
+    out = []
+    for step, ids in batches:
+        vals = []
+        for rid in ids:
+            vals.append(-1 if rid not in last else step - last[rid])
+            last[rid] = step
+        out.append(vals)
     return out
 
 

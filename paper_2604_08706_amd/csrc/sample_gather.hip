@@ -4,7 +4,7 @@
 // (Sec. 3.1; App. B "BufferStructure"); draws are uniform with replacement
 // (Sec. 4); positive-bias retention keeps the freshest (1-delta)N rollouts
 // plus the freshest delta*N correct rollouts older than those (Sec. 5;
-// App. D.3).  The positive-prioritised mixture is an addition (see header).
+// App. D.4).  The positive-prioritised mixture is an addition (see header).
 //
 // Device pipeline (one stream):
 //   [mix/retain only] pos_count -> pos_scan -> pos_compact : ascending list of

@@ -88,7 +88,7 @@ def test_tiny_all_modes_bit_exact(mode, p, delta, layout):
 
 
 def test_paper_worked_example_on_gpu():
-    # App. D.3 example (10 rollouts, N = 8, delta = 0.5): every draw lands in
+    # App. D.4 example (10 rollouts, N = 8, delta = 0.5): every draw lands in
     # the printed buffer and all 8 of its members are drawn
     rbp = require_gpu()
     correct = np.array([0, 1, 1, 0, 1, 1, 0, 1, 0, 0], dtype=np.float32)

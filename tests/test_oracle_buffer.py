@@ -197,3 +197,74 @@ def test_gather_padded_rows():
         assert np.all(g["seq_of_token"][j, :k] == j)
         assert np.all(g["seq_of_token"][j, k:] == -1)
     assert g["n_tokens"] == sum(min(lens[i], 12) for i in idx)
+
+
+# ---- sampling without replacement / unused first (App. E variants) ---------
+
+def test_without_replacement_is_a_subset_of_distinct_slots_and_covers_all():
+    got = ob.sample_without_replacement(seed=3, step=1, n_live=50, n_draw=20)
+    assert len(got) == 20 and len(set(got)) == 20 and got == sorted(got)
+    assert all(0 <= s < 50 for s in got)
+    assert ob.sample_without_replacement(3, 1, 50, 50) == list(range(50))
+    with pytest.raises(ValueError):
+        ob.sample_without_replacement(3, 1, 5, 6)
+
+
+def test_without_replacement_single_draw_is_the_smallest_key():
+    keys = [philox.philox4x64((s, 7, 1, 0), (9, 0))[0] >> 1 for s in range(300)]
+    assert ob.sample_without_replacement(9, 7, 300, 1) == [int(np.argmin(keys))]
+
+
+def test_without_replacement_inclusion_is_uniform():
+    # every slot is in a B-subset with probability B / n: inclusion counts over
+    # many steps follow a uniform multinomial
+    n_live, n_draw, steps = 40, 10, 2000
+    counts = np.zeros(n_live)
+    for step in range(steps):
+        counts[ob.sample_without_replacement(21, step, n_live, n_draw)] += 1
+    assert counts.sum() == n_draw * steps
+    assert stats.chisquare(counts).pvalue > 1e-4
+
+
+def test_unused_first_takes_never_used_records_ahead_of_used_ones():
+    n_live = 60
+    rng = np.random.default_rng(0)
+    use = rng.integers(0, 3, n_live)
+    unused = [s for s in range(n_live) if use[s] == 0]
+    k = len(unused)
+    assert 5 < k < 40
+    # fewer draws than unused records: only unused ones, as a plain
+    # without-replacement draw restricted to them would rank them
+    few = ob.sample_without_replacement(4, 2, n_live, 5, use_count=use)
+    assert set(few) <= set(unused)
+    keys = {s: ob.slot_key(4, 2, s) for s in unused}
+    assert few == sorted(sorted(unused, key=lambda s: (keys[s], s))[:5])
+    # more draws than unused records: all unused ones plus used ones
+    many = ob.sample_without_replacement(4, 2, n_live, k + 7, use_count=use)
+    assert set(unused) <= set(many) and len(many) == k + 7
+    # nothing used (or everything used): the plain draw
+    plain = ob.sample_without_replacement(4, 2, n_live, 13)
+    assert ob.sample_without_replacement(4, 2, n_live, 13, use_count=[0] * n_live) == plain
+    assert ob.sample_without_replacement(4, 2, n_live, 13, use_count=[5] * n_live) == plain
+
+
+# ---- steps since last use (App. D.3) -----------------------------------------
+
+def test_steps_since_last_use_paper_example(golden_dir):
+    with open(os.path.join(golden_dir, "steps_since_last_use_example.json")) as f:
+        ex = json.load(f)
+    assert ob.steps_since_last_use([tuple(b) for b in ex["batches"]]) == ex["expected"]
+
+
+def test_steps_since_last_use_brute_force():
+    # against a scan of the whole sample history for each sample
+    rng = np.random.default_rng(1)
+    batches = [(int(step), list(rng.integers(0, 12, 6))) for step in sorted(
+        rng.choice(100, 15, replace=False))]
+    got = ob.steps_since_last_use(batches)
+    history = []  # (step, rid) of every earlier sample, in order
+    for (step, ids), vals in zip(batches, got):
+        for rid, v in zip(ids, vals):
+            prev = [s for s, r in history if r == rid]
+            assert v == (-1 if not prev else step - prev[-1])
+            history.append((step, rid))
