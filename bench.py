@@ -191,9 +191,12 @@ def aux_stress(iters=20):
     buffer (10^6 records, ~1.8e9 stored tokens in HBM):
       sample+gather: 256 positive-mixture draws (p_pos = 0.5), padded to 8192;
       loss: policy_loss_fwd_bwd over the same draws packed (~4.7e5 tokens).
+      sample_no_replace: the same draws without replacement (per-slot keys and
+      a radix select), padded; note_use: the usage update of 256 draws.
     Algorithmic bytes: gather = 4 B/record reward scan + 4 B per positive slot
     + 20 B record metadata per draw + 8 B read per gathered token + 12 B
-    written per padded position; loss = 16 B per token (logp, old_logp,
+    written per padded position (without replacement: 8 B per record key in
+    place of the reward scan); loss = 16 B per token (logp, old_logp,
     seq_of_token read, dlogp written) + 8 B per sequence."""
     import torch
 
@@ -245,6 +248,42 @@ def aux_stress(iters=20):
                              + 12 * wl.n_draw * wl.l_max for v in n_tok]))
     g_rate = g_bytes / (g_ms / 1e3)
 
+    # without replacement: radix select over the 10^6 per-slot keys, same
+    # layout; then the usage update of the drawn records
+    nr = [rbp.make_sample_cfg(rbp.RB_NO_REPLACE, rbp.RB_LAYOUT_PADDED, 3, i, wl.n_draw,
+                              cur_version=tab.cur_version, l_max=wl.l_max) for i in range(iters)]
+    for c in nr[:3]:
+        rbp.rb_sample_gather(rec, c, out, ws)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for c in nr:
+        rbp.rb_sample_gather(rec, c, out, ws)
+    b.record()
+    torch.cuda.synchronize()
+    nr_ms = a.elapsed_time(b) / iters
+    nr_tok = []
+    for c in nr:
+        rbp.rb_sample_gather(rec, c, out, ws)
+        nr_tok.append(int(out["n_tokens"].item()))
+    nr_bytes = float(np.mean([8 * n + 20 * wl.n_draw + 8 * v + 12 * wl.n_draw * wl.l_max
+                              for v in nr_tok]))
+    uses = torch.zeros(n, dtype=torch.int32, device=dev)
+    last = torch.full((n,), -1, dtype=torch.int64, device=dev)
+    since = torch.empty(wl.n_draw, dtype=torch.int32, device=dev)
+    ws_u = rbp.workspace(rbp.RBP_OP_NOTE_USE, n)
+    rbp.rb_note_use(out["idx"], 0, n, 0, uses, last, since, ws_u)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for i in range(iters):
+        rbp.rb_note_use(out["idx"], 0, n, i + 1, uses, last, since, ws_u)
+    b.record()
+    torch.cuda.synchronize()
+    u_ms = a.elapsed_time(b) / iters
+
     # loss over the draws packed (one micro-batch holding every drawn token)
     c_pk = cfg(0, rbp.RB_LAYOUT_PACKED, max_tokens=wl.n_draw * wl.l_max)
     pk = rbp.alloc_batch(c_pk)
@@ -281,6 +320,11 @@ def aux_stress(iters=20):
                           "bytes": int(g_bytes),
                           "GB/s": round(g_rate / 1e9, 1),
                           "frac_hbm": round(g_rate / PEAK_HBM, 4)},
+        "sample_no_replace": {"layout": "padded [256, 8192]", "ms": round(nr_ms, 4),
+                              "tokens": int(np.mean(nr_tok)), "bytes": int(nr_bytes),
+                              "GB/s": round(nr_bytes / (nr_ms / 1e3) / 1e9, 1),
+                              "frac_hbm": round(nr_bytes / (nr_ms / 1e3) / PEAK_HBM, 4)},
+        "note_use": {"draws": wl.n_draw, "ms": round(u_ms, 4)},
         "loss": {"tokens": T, "ms": round(l_ms, 4), "bytes": l_bytes,
                  "GB/s": round(l_bytes / (l_ms / 1e3) / 1e9, 1),
                  "frac_hbm": round(l_bytes / (l_ms / 1e3) / PEAK_HBM, 4)},

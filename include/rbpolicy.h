@@ -11,6 +11,8 @@
  *
  *   rb_group_advantage   advantages of a freshly generated group     (App. D.2)
  *   rb_sample_gather     draw records and gather their tokens         (Sec. 3.1, 5; App. B, D.4)
+ *   rb_push              append generated groups, FIFO eviction      (App. B, D.2)
+ *   rb_note_use          per-record use counts, steps since last use (App. D.3)
  *   policy_logprob_fwd   log pi(y_t) from hidden states and W         (App. D.2)
  *   policy_loss_fwd_bwd  clipped GRPO loss and d loss / d logp        (App. D.2)
  *   policy_logprob_bwd   d loss / d hidden and d loss / d W           (chain rule of the above)
@@ -70,9 +72,15 @@ enum {
   RB_POS_MIX = 1,    /* per draw, a coin with probability p_pos picks a uniform
                         positive record (reward > 0), else a uniform live record;
                         no positives -> uniform.  Not in the paper.             */
-  RB_POS_RETAIN = 2  /* positive-bias sampling (Sec. 5; App. D.4): uniform over
+  RB_POS_RETAIN = 2, /* positive-bias sampling (Sec. 5; App. D.4): uniform over
                         the freshest n_fresh records plus the freshest
                         n_pos_keep positive records older than those            */
+  RB_NO_REPLACE = 3, /* uniform without replacement (App. E, "No replacement"):
+                        the n_draw slots with the smallest per-slot keys (see
+                        rb_sample_cfg), listed in ascending slot order          */
+  RB_UNUSED_FIRST = 4 /* without replacement, never-used records first (App. E,
+                        "No replacement, at least once"): as RB_NO_REPLACE with
+                        records of use_count 0 ranked ahead of used ones        */
 };
 
 /* ---- batch layouts (rb_sample_cfg.layout) ---------------------------------- */
@@ -88,7 +96,8 @@ enum {
   RBP_OP_LOSS = 3,          /* n = T (also policy_asymre_fwd_bwd)            */
   RBP_OP_LOGPROB_BWD = 4,   /* n = tokens per backward chunk (T for one chunk) */
   RBP_OP_LOSS_SEQ = 5,      /* n = B, sequences of policy_loss_seq_fwd_bwd     */
-  RBP_OP_FUSED = 6          /* n = tokens per policy_fused_fwd_bwd chunk       */
+  RBP_OP_FUSED = 6,         /* n = tokens per policy_fused_fwd_bwd chunk       */
+  RBP_OP_NOTE_USE = 7       /* n = capacity of the record table              */
 };
 
 /*
@@ -110,6 +119,9 @@ typedef struct rb_records {
   const int32_t* arena_tokens;   /* device [arena_size]                            */
   const float* arena_old_logp;   /* device [arena_size]                            */
   int64_t arena_size;            /* every record must lie inside [0, arena_size)   */
+  const int32_t* use_count;      /* device [capacity], samples per row so far
+                                    (rb_note_use); read by RB_UNUSED_FIRST only,
+                                    may be NULL for the other modes               */
 } rb_records;
 
 /*
@@ -118,7 +130,10 @@ typedef struct rb_records {
  * word x0 maps to an index in [0, n) as floor(x0 * n / 2^64), the high half of
  * its second word x1 decides the stratum coin: (x1 >> 32) < p_pos_q32.  A call
  * therefore depends only on (seed, step) and the record table: re-running a
- * step after a restart reproduces it bit for bit.
+ * step after a restart reproduces it bit for bit.  The modes without
+ * replacement give slot s the key x0 >> 1 of the block with counter
+ * (s, step, 1, 0) and the same key (RB_UNUSED_FIRST adds 2^63 when the slot's
+ * use_count is > 0) and take the n_draw smallest (key, slot) pairs.
  */
 typedef struct rb_sample_cfg {
   int32_t mode;          /* RB_UNIFORM / RB_POS_MIX / RB_POS_RETAIN                */
@@ -162,10 +177,12 @@ typedef struct rb_batch {
 /*
  * Draw a training batch from the replay buffer and gather it (Sec. 3.1:
  * sampling does not remove records; Sec. 4: draws are uniform with
- * replacement; Sec. 5 and App. D.4: positive-bias retention).  Draws are
- * kept in draw order, duplicates included.
+ * replacement; Sec. 5 and App. D.4: positive-bias retention; App. E: the
+ * variants without replacement).  Draws are kept in draw order, duplicates
+ * included; the modes without replacement list distinct slots ascending.
  * Errors: RBP_EINVAL for null pointers, n_live outside [1, capacity], n_draw
- *   outside [1, 2^20], an unknown mode/layout, p_pos_q32 > 2^32, negative
+ *   outside [1, 2^20] (or above n_live without replacement), a null
+ *   use_count for RB_UNUSED_FIRST, an unknown mode/layout, p_pos_q32 > 2^32, negative
  *   n_fresh/n_pos_keep, max_tokens < 1 (packed) or l_max < 1 (padded);
  *   RBP_EWORKSPACE if ws_bytes < rbp_workspace_bytes(RBP_OP_SAMPLE_GATHER,
  *   capacity, 0, 0).  Record offsets and lengths are trusted: the caller
@@ -343,6 +360,68 @@ int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
                          float* loss_accum, float* dlogp, float* stats,
                          float* dhidden, float* dW, int accumulate_dW, void* ws,
                          size_t ws_bytes, void* stream);
+
+/*
+ * The record table as rb_push writes it: the rb_records arrays, writable, with
+ * a fixed arena stretch of slot_tokens tokens per row (row r owns
+ * arena[r * slot_tokens, (r + 1) * slot_tokens)), so that a new record always
+ * reuses the storage of the record it evicts.
+ */
+typedef struct rb_ring {
+  int64_t n_live;            /* host; updated by rb_push                           */
+  int64_t capacity;          /* N, rows of every per-record array                  */
+  int64_t head;              /* host; physical row of slot 0, updated by rb_push   */
+  int64_t slot_tokens;       /* arena tokens per row (>= 1)                        */
+  int64_t* arena_off;        /* device [capacity]                                  */
+  int32_t* length;           /* device [capacity]                                  */
+  float* reward;             /* device [capacity]                                  */
+  float* advantage;          /* device [capacity]                                  */
+  int32_t* version;          /* device [capacity]                                  */
+  int32_t* use_count;        /* device [capacity] or NULL: reset to 0 on insert     */
+  int64_t* last_step;        /* device [capacity] or NULL: reset to -1 on insert    */
+  int32_t* arena_tokens;     /* device [capacity * slot_tokens]                    */
+  float* arena_old_logp;     /* device [capacity * slot_tokens]                    */
+} rb_ring;
+
+/*
+ * Append freshly generated groups to the buffer, first in first out (App. B
+ * "BufferStructure": a push into a full buffer evicts the oldest record), and
+ * record each rollout's group advantage as rb_group_advantage computes it
+ * (App. D.2: advantages are fixed at generation).  New record i (0-based, in
+ * the given order) goes to physical row (head + n_live + i) % capacity; then
+ * n_live = min(capacity, n_live + n_new) and head moves past the evicted rows.
+ * group_off device int32 [n_groups + 1] splits the n_new records into groups
+ * (group_off[0] = 0, group_off[n_groups] = n_new); length, reward device
+ * [n_new]; src_off device int64 [n_new]: record i's tokens / behaviour
+ * log-probs are tokens / old_logp[src_off[i] .. + length[i]).  A record longer
+ * than slot_tokens keeps its first slot_tokens tokens (its stored length is
+ * cut to that).  version is stored for every new record.
+ * Errors: RBP_EINVAL (null pointers, n_new outside [1, capacity],
+ *         n_groups < 1, n_live outside [0, capacity], head outside
+ *         [0, capacity), slot_tokens < 1, ddof not 0 or 1, eps < 0).
+ */
+int rb_push(rb_ring* ring, int32_t n_new, int32_t n_groups, const int32_t* group_off,
+            const int32_t* length, const int64_t* src_off, const float* reward,
+            int32_t version, const int32_t* tokens, const float* old_logp,
+            int32_t ddof, float eps, void* stream);
+
+/*
+ * Usage bookkeeping after a batch is drawn (App. D.3, "Steps-since-last-use"):
+ * for draw j in draw order, since[j] = -1 if its record was never used before
+ * ("new"), 0 if an earlier draw of this batch took the same record, else
+ * step - last_step of the record; then every drawn record gets
+ * last_step = step and use_count += its number of draws.  idx device int32
+ * [n_draw] (slots as rb_sample_gather writes them); head, capacity as in the
+ * record table; use_count device int32, last_step device int64 [capacity];
+ * since device int32 [n_draw] (may be NULL).  Steps must not decrease
+ * between calls.
+ * ws device, >= rbp_workspace_bytes(RBP_OP_NOTE_USE, capacity, 0, 0).
+ * Errors: RBP_EINVAL (null pointers, n_draw < 0, head outside [0, capacity),
+ *         step < 0); RBP_EWORKSPACE.
+ */
+int rb_note_use(const int32_t* idx, int64_t n_draw, int64_t head, int64_t capacity,
+                int64_t step, int32_t* use_count, int64_t* last_step, int32_t* since,
+                void* ws, size_t ws_bytes, void* stream);
 
 /* Workspace bytes an operation needs (see RBP_OP_*); 0 for an invalid op. */
 size_t rbp_workspace_bytes(int op, int64_t n, int32_t d, int32_t V);

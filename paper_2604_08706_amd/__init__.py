@@ -15,7 +15,9 @@ from ._binding import (  # noqa: F401
     RB_LAYOUT_PACKED,
     RB_LAYOUT_PADDED,
     RB_POS_MIX,
+    RB_NO_REPLACE,
     RB_POS_RETAIN,
+    RB_UNUSED_FIRST,
     RB_UNIFORM,
     RBP_EHIP,
     RBP_EINVAL,
@@ -26,6 +28,7 @@ from ._binding import (  # noqa: F401
     RBP_OP_LOGPROB_FWD,
     RBP_OP_LOSS,
     RBP_OP_FUSED,
+    RBP_OP_NOTE_USE,
     RBP_OP_LOSS_SEQ,
     RBP_OP_SAMPLE_GATHER,
     RbpError,
@@ -33,6 +36,7 @@ from ._binding import (  # noqa: F401
     lib,
     load_library,
     make_records,
+    make_ring,
     make_sample_cfg,
     policy_logprob_bwd,
     policy_logprob_fwd,
@@ -42,7 +46,10 @@ from ._binding import (  # noqa: F401
     policy_loss_seq_fwd_bwd,
     rb_asymre_coef,
     rb_group_advantage,
+    rb_note_use,
+    rb_push,
     rb_sample_gather,
     rbp_workspace_bytes,
+    ring_records,
     workspace,
 )

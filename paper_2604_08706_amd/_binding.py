@@ -23,6 +23,8 @@ RBP_EHIP = -4
 RB_UNIFORM = 0
 RB_POS_MIX = 1
 RB_POS_RETAIN = 2
+RB_NO_REPLACE = 3
+RB_UNUSED_FIRST = 4
 RB_LAYOUT_PACKED = 0
 RB_LAYOUT_PADDED = 1
 
@@ -32,12 +34,13 @@ RBP_OP_LOSS = 3
 RBP_OP_LOGPROB_BWD = 4
 RBP_OP_LOSS_SEQ = 5
 RBP_OP_FUSED = 6
+RBP_OP_NOTE_USE = 7
 
 EXPORTED = (
     "rb_sample_gather", "rb_group_advantage", "policy_logprob_fwd",
     "policy_loss_fwd_bwd", "policy_logprob_bwd", "rbp_workspace_bytes",
     "rbp_status_string", "rbp_last_error", "policy_loss_seq_fwd_bwd", "rb_asymre_coef",
-    "policy_asymre_fwd_bwd", "policy_fused_fwd_bwd",
+    "policy_asymre_fwd_bwd", "policy_fused_fwd_bwd", "rb_push", "rb_note_use",
 )
 
 
@@ -54,6 +57,19 @@ class RbRecords(ctypes.Structure):
         ("reward", ctypes.c_void_p), ("advantage", ctypes.c_void_p),
         ("version", ctypes.c_void_p), ("arena_tokens", ctypes.c_void_p),
         ("arena_old_logp", ctypes.c_void_p), ("arena_size", ctypes.c_int64),
+        ("use_count", ctypes.c_void_p),
+    ]
+
+
+class RbRing(ctypes.Structure):
+    _fields_ = [
+        ("n_live", ctypes.c_int64), ("capacity", ctypes.c_int64), ("head", ctypes.c_int64),
+        ("slot_tokens", ctypes.c_int64),
+        ("arena_off", ctypes.c_void_p), ("length", ctypes.c_void_p),
+        ("reward", ctypes.c_void_p), ("advantage", ctypes.c_void_p),
+        ("version", ctypes.c_void_p), ("use_count", ctypes.c_void_p),
+        ("last_step", ctypes.c_void_p), ("arena_tokens", ctypes.c_void_p),
+        ("arena_old_logp", ctypes.c_void_p),
     ]
 
 
@@ -102,6 +118,9 @@ def load_library(path=LIB_PATH):
     lib.policy_fused_fwd_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i32, i32, i32, i64,
                                          f32, f32, vp, vp, vp, vp, vp, vp, vp, vp,
                                          ctypes.c_int, vp, sz, vp]
+    lib.rb_push.argtypes = [ctypes.POINTER(RbRing), i32, i32, vp, vp, vp, vp, i32, vp, vp, i32,
+                            f32, vp]
+    lib.rb_note_use.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, sz, vp]
     lib.rbp_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i32]
     lib.rbp_workspace_bytes.restype = sz
     lib.rbp_status_string.argtypes = [ctypes.c_int]
@@ -180,13 +199,15 @@ def rb_group_advantage(reward, group_off, adv, ddof=1, eps=1e-6, stream=None):
 
 
 def make_records(n_live, capacity, head, arena_off, length, reward, advantage, version,
-                 arena_tokens, arena_old_logp):
+                 arena_tokens, arena_old_logp, use_count=None):
     """Build the host-side rb_records struct from device tensors.
 
     The struct keeps references to the tensors, so their memory stays
     allocated for as long as the struct is alive."""
     rec = RbRecords()
-    rec._keep = (arena_off, length, reward, advantage, version, arena_tokens, arena_old_logp)
+    rec._keep = (arena_off, length, reward, advantage, version, arena_tokens, arena_old_logp,
+                 use_count)
+    rec.use_count = _opt(use_count, torch.int32, "use_count", capacity).value
     rec.n_live, rec.capacity, rec.head = int(n_live), int(capacity), int(head)
     rec.arena_off = _dev(arena_off, torch.int64, "arena_off", capacity).value
     rec.length = _dev(length, torch.int32, "length", capacity).value
@@ -368,3 +389,60 @@ def policy_fused_fwd_bwd(hidden, W, tokens, seq_of_token, old_logp, adv, seq_len
                                     _dev(dW, torch.float32, "dW", V * d),
                                     1 if accumulate_dW else 0, wsp, wsb, _stream(stream))
     _check("policy_fused_fwd_bwd", st)
+
+
+def make_ring(capacity, slot_tokens, device="cuda", counters=True):
+    """Allocate an empty ring record table (rb_ring) with torch; returns the
+    struct, which keeps its tensors in ``ring.t``."""
+    cap, st = int(capacity), int(slot_tokens)
+    t = {
+        "arena_off": torch.zeros(cap, dtype=torch.int64, device=device),
+        "length": torch.zeros(cap, dtype=torch.int32, device=device),
+        "reward": torch.zeros(cap, dtype=torch.float32, device=device),
+        "advantage": torch.zeros(cap, dtype=torch.float32, device=device),
+        "version": torch.zeros(cap, dtype=torch.int32, device=device),
+        "use_count": torch.zeros(cap, dtype=torch.int32, device=device) if counters else None,
+        "last_step": torch.full((cap,), -1, dtype=torch.int64, device=device)
+        if counters else None,
+        "arena_tokens": torch.zeros(cap * st, dtype=torch.int32, device=device),
+        "arena_old_logp": torch.zeros(cap * st, dtype=torch.float32, device=device),
+    }
+    ring = RbRing()
+    ring.t = t
+    ring.n_live, ring.capacity, ring.head, ring.slot_tokens = 0, cap, 0, st
+    for k, v in t.items():
+        setattr(ring, k, 0 if v is None else v.data_ptr())
+    return ring
+
+
+def ring_records(ring):
+    """rb_records view of a ring (for rb_sample_gather)."""
+    t = ring.t
+    return make_records(max(ring.n_live, 1), ring.capacity, ring.head, t["arena_off"],
+                        t["length"], t["reward"], t["advantage"], t["version"],
+                        t["arena_tokens"], t["arena_old_logp"], t["use_count"])
+
+
+def rb_push(ring, group_off, length, src_off, reward, version, tokens, old_logp, ddof=1,
+            eps=1e-6, stream=None):
+    n_new = length.numel()
+    n_groups = group_off.numel() - 1
+    st = lib().rb_push(ctypes.byref(ring), n_new, n_groups,
+                       _dev(group_off, torch.int32, "group_off", n_groups + 1),
+                       _dev(length, torch.int32, "length", n_new),
+                       _dev(src_off, torch.int64, "src_off", n_new),
+                       _dev(reward, torch.float32, "reward", n_new), int(version),
+                       _dev(tokens, torch.int32, "tokens"),
+                       _dev(old_logp, torch.float32, "old_logp"), int(ddof), float(eps),
+                       _stream(stream))
+    _check("rb_push", st)
+
+
+def rb_note_use(idx, head, capacity, step, use_count, last_step, since, ws, stream=None):
+    n = idx.numel()
+    wsp, wsb = _ws(ws)
+    st = lib().rb_note_use(_dev(idx, torch.int32, "idx", n), n, int(head), int(capacity),
+                           int(step), _dev(use_count, torch.int32, "use_count", capacity),
+                           _dev(last_step, torch.int64, "last_step", capacity),
+                           _opt(since, torch.int32, "since", n), wsp, wsb, _stream(stream))
+    _check("rb_note_use", st)

@@ -12,6 +12,7 @@
 // order and then summed over blocks by one small block in block order, so the
 // result is bitwise reproducible.
 
+#include "group_advantage.h"
 #include "rbp_internal.h"
 
 namespace {
@@ -25,24 +26,8 @@ __global__ void __launch_bounds__(64) group_advantage_kernel(
     int32_t n_groups, int32_t ddof, float eps, float* __restrict__ adv) {
   const int32_t g = blockIdx.x * 64 + threadIdx.x;
   if (g >= n_groups) return;
-  const int32_t lo = group_off[g], hi = group_off[g + 1];
-  const int32_t n = hi - lo;
-  if (n <= 0) return;
-  float sum = 0.0f;
-  for (int32_t i = lo; i < hi; ++i) sum += reward[i];
-  const float mean = sum / (float)n;
-  float ss = 0.0f;
-  for (int32_t i = lo; i < hi; ++i) {
-    const float dv = reward[i] - mean;
-    ss = fmaf(dv, dv, ss);
-  }
-  if (ss == 0.0f || n - ddof <= 0) {
-    for (int32_t i = lo; i < hi; ++i) adv[i] = 0.0f;
-    return;
-  }
-  const float sd = __fsqrt_rn(ss / (float)(n - ddof));
-  const float denom = sd + eps;
-  for (int32_t i = lo; i < hi; ++i) adv[i] = (reward[i] - mean) / denom;
+  rbp::group_advantage(reward, group_off[g], group_off[g + 1], ddof, eps,
+                       [&](int32_t i, float a) { adv[i] = a; });
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

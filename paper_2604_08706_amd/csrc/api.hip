@@ -39,6 +39,7 @@ extern "C" size_t rbp_workspace_bytes(int op, int64_t n, int32_t d, int32_t V) {
     case RBP_OP_LOGPROB_BWD: return rbp::logprob_bwd_ws(n, d, V < 1 ? 1 : V);
     case RBP_OP_LOSS_SEQ: return rbp::loss_seq_ws(n);
     case RBP_OP_FUSED: return rbp::fused_ws(n, d, V);
+    case RBP_OP_NOTE_USE: return rbp::note_use_ws(n);
     default: return 0;
   }
 }

@@ -40,6 +40,7 @@ size_t loss_ws(int64_t T);
 size_t loss_seq_ws(int64_t B);
 size_t logprob_bwd_ws(int64_t Tc, int32_t d, int32_t V);
 size_t fused_ws(int64_t Tc, int32_t d, int32_t V);
+size_t note_use_ws(int64_t capacity);
 
 // The two products of the log-prob backward for one chunk of Tn tokens, from
 // dz^T (bf16 [round256(V)][ldGt], columns Tn..round256(Tn) zero):

@@ -9,6 +9,10 @@
 // Device pipeline (one stream):
 //   [mix/retain only] pos_count -> pos_scan -> pos_compact : ascending list of
 //       positive slots (slot = FIFO position, 0 = oldest) in the workspace;
+//   [without replacement] slot_key -> 8 x (select_hist -> select_digit) ->
+//       sel_count -> sel_scan -> sel_compact : an MSD radix select finds the
+//       n_draw-th smallest 64-bit slot key K exactly, then the slots with a key
+//       below K (and the first ties in slot order) are listed ascending;
 //   draw     : one thread per draw; Philox4x64-10 block -> slot; per-draw
 //              outputs; block scan of lengths -> cu_seqlens, n_tokens;
 //   gather   : one thread per output position; coalesced copies from the
@@ -128,6 +132,138 @@ __global__ void __launch_bounds__(kCountThreads) pos_compact_kernel(
     if (f[i]) pos_list[at++] = (int32_t)(s0 + i);
 }
 
+// ---- selection without replacement -----------------------------------------
+
+// Key of slot s: the top 63 bits of word 0 of the Philox block with counter
+// (s, step, 1, 0); for never-used-first, bit 63 set when the slot was used.
+__global__ void __launch_bounds__(256) slot_key_kernel(uint64_t seed, uint64_t step,
+                                                       int64_t n_live, int64_t head, int64_t cap,
+                                                       const int32_t* __restrict__ use_count,
+                                                       uint64_t* __restrict__ keys) {
+  for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < n_live;
+       s += (int64_t)gridDim.x * 256) {
+    uint64_t k = philox4x64_10((uint64_t)s, step, 1, 0, seed, 0).x0 >> 1;
+    if (use_count != nullptr && use_count[phys_row(s, head, cap)] > 0) k |= 1ull << 63;
+    keys[s] = k;
+  }
+}
+
+// Radix-select state: the key digits fixed so far, how many keys still to be
+// taken among those sharing them, and the histogram of the next digit.
+struct SelState {
+  uint64_t prefix;
+  int64_t need;
+  uint32_t hist[256];
+};
+
+__global__ void __launch_bounds__(256) select_init_kernel(SelState* st, int64_t n_draw) {
+  st->hist[threadIdx.x] = 0u;
+  if (threadIdx.x == 0) {
+    st->prefix = 0;
+    st->need = n_draw;
+  }
+}
+
+// Histogram of digit `pass` (bits 56 - 8 pass .. +8, most significant first)
+// over the keys whose higher digits equal the prefix.  Integer atomics: the
+// counts do not depend on the order of the additions.
+__global__ void __launch_bounds__(256) select_hist_kernel(const uint64_t* __restrict__ keys,
+                                                          int64_t n, int pass,
+                                                          SelState* __restrict__ st) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0u;
+  __syncthreads();
+  const int shift = 56 - 8 * pass;
+  const uint64_t hi = pass == 0 ? 0 : st->prefix >> (shift + 8);
+  for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < n;
+       s += (int64_t)gridDim.x * 256) {
+    const uint64_t k = keys[s];
+    if (pass == 0 || (k >> (shift + 8)) == hi) atomicAdd(&h[(k >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  if (h[threadIdx.x] != 0u) atomicAdd(&st->hist[threadIdx.x], h[threadIdx.x]);
+}
+
+// The digit holding the need-th smallest remaining key; clears the histogram.
+__global__ void __launch_bounds__(256) select_digit_kernel(int pass, SelState* __restrict__ st) {
+  if (threadIdx.x == 0) {
+    int64_t cum = 0;
+    int d = 0;
+    for (; d < 255; ++d) {
+      if (cum + (int64_t)st->hist[d] >= st->need) break;
+      cum += st->hist[d];
+    }
+    st->need -= cum;
+    st->prefix |= (uint64_t)d << (56 - 8 * pass);
+  }
+  __syncthreads();
+  st->hist[threadIdx.x] = 0u;
+}
+
+// Per slot, (key < K) in the low 32 bits and (key == K) in the high 32 bits:
+// one int64 whose block sums carry both counts.
+__device__ __forceinline__ int64_t sel_flags(uint64_t k, uint64_t K) {
+  return (k < K ? 1 : 0) + (k == K ? (int64_t(1) << 32) : 0);
+}
+
+__global__ void __launch_bounds__(kCountThreads) sel_count_kernel(
+    const uint64_t* __restrict__ keys, int64_t n, const SelState* __restrict__ st,
+    int64_t* __restrict__ counts) {
+  __shared__ int64_t lds[kCountThreads / 64];
+  const uint64_t K = st->prefix;
+  const int64_t s0 = (int64_t)blockIdx.x * kSlotsPerBlock + threadIdx.x * 4;
+  int64_t c = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (s0 + i < n) c += sel_flags(keys[s0 + i], K);
+  int64_t total;
+  block_exclusive_scan<kCountThreads>(c, &total, lds);
+  if (threadIdx.x == 0) counts[blockIdx.x] = total;
+}
+
+__global__ void __launch_bounds__(1024) sel_scan_kernel(const int64_t* __restrict__ counts,
+                                                        int64_t* __restrict__ offsets,
+                                                        int64_t nb) {
+  __shared__ int64_t lds[1024 / 64];
+  int64_t carry = 0;
+  for (int64_t base = 0; base < nb; base += 1024) {
+    const int64_t i = base + threadIdx.x;
+    const int64_t v = i < nb ? counts[i] : 0;
+    int64_t total;
+    const int64_t ex = block_exclusive_scan<1024>(v, &total, lds);
+    if (i < nb) offsets[i] = carry + ex;
+    carry += total;
+  }
+}
+
+// A slot with key < K goes to position (# keys < K before it) + min(# ties
+// before it, need); a tie is taken while fewer than `need` ties precede it.
+__global__ void __launch_bounds__(kCountThreads) sel_compact_kernel(
+    const uint64_t* __restrict__ keys, int64_t n, const SelState* __restrict__ st,
+    const int64_t* __restrict__ offsets, int32_t* __restrict__ sel) {
+  __shared__ int64_t lds[kCountThreads / 64];
+  const uint64_t K = st->prefix;
+  const int64_t need = st->need;
+  const int64_t s0 = (int64_t)blockIdx.x * kSlotsPerBlock + threadIdx.x * 4;
+  int64_t f[4], c = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[i] = s0 + i < n ? sel_flags(keys[s0 + i], K) : 0;
+    c += f[i];
+  }
+  int64_t total;
+  int64_t at = offsets[blockIdx.x] + block_exclusive_scan<kCountThreads>(c, &total, lds);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t less = at & 0xffffffffll, ties = at >> 32;
+    if (f[i] == 1)
+      sel[less + (ties < need ? ties : need)] = (int32_t)(s0 + i);
+    else if (f[i] != 0 && ties < need)
+      sel[less + ties] = (int32_t)(s0 + i);
+    at += f[i];
+  }
+}
+
 struct DrawParams {
   int32_t mode, layout;
   uint64_t seed, step, p_q32;
@@ -145,7 +281,7 @@ __global__ void __launch_bounds__(kDrawThreads) draw_kernel(
     int32_t* __restrict__ cu_seqlens, int64_t* __restrict__ n_tokens,
     int64_t* __restrict__ stream_total) {
   __shared__ int64_t lds[kDrawThreads / 64];
-  const int64_t n_pos = (p.mode == RB_UNIFORM) ? 0 : meta[0];
+  const int64_t n_pos = (p.mode == RB_POS_MIX || p.mode == RB_POS_RETAIN) ? meta[0] : 0;
   // retained set: the newest `keep` positives older than the fresh part, then
   // the fresh part [first_fresh, n_live)
   const int64_t keep = n_pos < p.n_pos_keep ? n_pos : p.n_pos_keep;
@@ -165,6 +301,8 @@ __global__ void __launch_bounds__(kDrawThreads) draw_kernel(
           slot = pos_list[__umul64hi(b.x0, (uint64_t)n_pos)];
         else
           slot = (int64_t)__umul64hi(b.x0, (uint64_t)p.n_live);
+      } else if (p.mode == RB_NO_REPLACE || p.mode == RB_UNUSED_FIRST) {
+        slot = pos_list[j];  // the selected slots, ascending
       } else {
         if (n_set <= 0) {
           slot = 0;
@@ -295,6 +433,10 @@ size_t rbp::sample_gather_ws(int64_t capacity) {
   c.take<int32_t>(nb);
   c.take<int32_t>(capacity < 1 ? 1 : capacity);
   c.take<int64_t>(4);
+  c.take<uint64_t>(capacity < 1 ? 1 : capacity);
+  c.take<int64_t>(nb);
+  c.take<int64_t>(nb);
+  c.take<SelState>(1);
   return align_up(c.used, 256);
 }
 
@@ -313,8 +455,14 @@ extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
   RBP_REQUIRE(rec->arena_off && rec->length && rec->reward && rec->advantage &&
                   rec->version && rec->arena_tokens && rec->arena_old_logp,
               RBP_EINVAL, "rb_sample_gather: null record array");
-  RBP_REQUIRE(cfg->mode == RB_UNIFORM || cfg->mode == RB_POS_MIX || cfg->mode == RB_POS_RETAIN,
-              RBP_EINVAL, "rb_sample_gather: unknown mode %d", cfg->mode);
+  RBP_REQUIRE(cfg->mode >= RB_UNIFORM && cfg->mode <= RB_UNUSED_FIRST, RBP_EINVAL,
+              "rb_sample_gather: unknown mode %d", cfg->mode);
+  const bool no_replace = cfg->mode == RB_NO_REPLACE || cfg->mode == RB_UNUSED_FIRST;
+  RBP_REQUIRE(!no_replace || cfg->n_draw <= rec->n_live, RBP_EINVAL,
+              "rb_sample_gather: %lld draws without replacement from %lld records",
+              (long long)cfg->n_draw, (long long)rec->n_live);
+  RBP_REQUIRE(cfg->mode != RB_UNUSED_FIRST || rec->use_count != nullptr, RBP_EINVAL,
+              "rb_sample_gather: RB_UNUSED_FIRST needs use_count");
   RBP_REQUIRE(cfg->layout == RB_LAYOUT_PACKED || cfg->layout == RB_LAYOUT_PADDED, RBP_EINVAL,
               "rb_sample_gather: unknown layout %d", cfg->layout);
   RBP_REQUIRE(cfg->n_draw >= 1 && cfg->n_draw <= (1 << 20), RBP_EINVAL,
@@ -344,6 +492,10 @@ extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
   int32_t* offsets = c.take<int32_t>(nb_cap);
   int32_t* pos_list = c.take<int32_t>(rec->capacity);
   int64_t* meta = c.take<int64_t>(4);
+  uint64_t* keys = c.take<uint64_t>(rec->capacity);
+  int64_t* sel_counts = c.take<int64_t>(nb_cap);
+  int64_t* sel_offsets = c.take<int64_t>(nb_cap);
+  SelState* sel_state = c.take<SelState>(1);
 
   DrawParams p{};
   p.mode = cfg->mode;
@@ -363,7 +515,26 @@ extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
   p.token_begin = cfg->token_begin;
   p.l_max = cfg->l_max;
 
-  if (cfg->mode != RB_UNIFORM) {
+  if (no_replace) {
+    const int64_t n = rec->n_live;
+    int64_t kb = rbp::ceil_div(n, 256);
+    if (kb > 4096) kb = 4096;
+    hipLaunchKernelGGL(slot_key_kernel, dim3(kb), dim3(256), 0, s, cfg->seed, cfg->step, n,
+                       rec->head, rec->capacity,
+                       cfg->mode == RB_UNUSED_FIRST ? rec->use_count : nullptr, keys);
+    hipLaunchKernelGGL(select_init_kernel, dim3(1), dim3(256), 0, s, sel_state, cfg->n_draw);
+    for (int pass = 0; pass < 8; ++pass) {
+      hipLaunchKernelGGL(select_hist_kernel, dim3(kb), dim3(256), 0, s, keys, n, pass,
+                         sel_state);
+      hipLaunchKernelGGL(select_digit_kernel, dim3(1), dim3(256), 0, s, pass, sel_state);
+    }
+    const int64_t nb = rbp::ceil_div(n, kSlotsPerBlock);
+    hipLaunchKernelGGL(sel_count_kernel, dim3(nb), dim3(kCountThreads), 0, s, keys, n, sel_state,
+                       sel_counts);
+    hipLaunchKernelGGL(sel_scan_kernel, dim3(1), dim3(1024), 0, s, sel_counts, sel_offsets, nb);
+    hipLaunchKernelGGL(sel_compact_kernel, dim3(nb), dim3(kCountThreads), 0, s, keys, n,
+                       sel_state, sel_offsets, pos_list);
+  } else if (cfg->mode != RB_UNIFORM) {
     // positives over all live slots (mixture) or over the non-fresh ones (retention)
     const int64_t n_range = cfg->mode == RB_POS_MIX ? rec->n_live : p.first_fresh;
     const int64_t nb = rbp::ceil_div(n_range > 0 ? n_range : 1, kSlotsPerBlock);

@@ -1,0 +1,173 @@
+"""GPU parity of the buffer maintenance calls against the oracle: sampling
+without replacement and never-used-first (bit-exact slots), steps since last
+use and use counts (exact), and FIFO insertion with advantages at insert
+(records, arena contents and ring bookkeeping exact; advantages rtol 1e-5)."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import buffer as ob
+from oracle.advantage import group_advantage
+
+from gpu_util import require_gpu, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _records(rbp, n_live, cap, head, seed, use=None):
+    """A ring of n_live records with 1..8 tokens each; use = per-slot counts."""
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(1, 9, n_live).astype(np.int32)
+    offs = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+    phys = (head + np.arange(n_live)) % cap
+
+    def ring(vals, dtype, junk):
+        a = np.full(cap, junk, dtype=dtype)
+        a[phys] = vals
+        return torch.from_numpy(a).cuda()
+
+    t = {
+        "off": ring(offs, np.int64, 0), "len": ring(lens, np.int32, 1),
+        "rew": ring(rng.random(n_live).astype(np.float32), np.float32, 0.0),
+        "adv": ring(rng.standard_normal(n_live).astype(np.float32), np.float32, 0.0),
+        "ver": ring(np.zeros(n_live, np.int32), np.int32, 0),
+        "tok": torch.from_numpy(rng.integers(0, 1000, int(lens.sum())).astype(np.int32)).cuda(),
+        "old": torch.from_numpy(rng.random(int(lens.sum())).astype(np.float32)).cuda(),
+        "use": None if use is None else ring(np.asarray(use, np.int32), np.int32, 99),
+    }
+    rec = rbp.make_records(n_live, cap, head, t["off"], t["len"], t["rew"], t["adv"], t["ver"],
+                           t["tok"], t["old"], t["use"])
+    return rec, t, lens, offs
+
+
+def _draw(rbp, rec, cap, mode, seed, step, n_draw):
+    cfg = rbp.make_sample_cfg(mode, rbp.RB_LAYOUT_PACKED, seed, step, n_draw,
+                              max_tokens=8 * n_draw)
+    out = rbp.alloc_batch(cfg)
+    print(f"[buffer] mode={mode} n_live={rec.n_live} n_draw={n_draw} step={step}", flush=True)
+    rbp.rb_sample_gather(rec, cfg, out, rbp.workspace(rbp.RBP_OP_SAMPLE_GATHER, cap))
+    torch.cuda.synchronize()
+    return {k: to_np(v) for k, v in out.items()}
+
+
+@pytest.mark.parametrize("n_live,cap,head,n_draw", [
+    (1, 1, 0, 1), (37, 50, 45, 10), (37, 37, 3, 37), (1000, 1500, 1234, 1),
+    (5000, 5000, 17, 300), (100_000, 120_000, 99_999, 1024)])
+def test_without_replacement_matches_oracle(n_live, cap, head, n_draw):
+    rbp = require_gpu()
+    rec, t, lens, offs = _records(rbp, n_live, cap, head, n_live)
+    for step in (0, 5):
+        got = _draw(rbp, rec, cap, rbp.RB_NO_REPLACE, 11, step, n_draw)
+        want = ob.sample_without_replacement(11, step, n_live, n_draw)
+        assert np.array_equal(got["idx"], want)
+        g = ob.gather(want, offs, lens, np.zeros(n_live), np.zeros(n_live), to_np(t["tok"]),
+                      to_np(t["old"]), 10, ob.LAYOUT_PACKED, max_tokens=8 * n_draw)
+        assert np.array_equal(got["tokens"], g["tokens"])
+        assert np.array_equal(got["cu_seqlens"], g["cu_seqlens"])
+
+
+@pytest.mark.parametrize("frac_used", [0.0, 0.3, 0.9, 1.0])
+def test_unused_first_matches_oracle(frac_used):
+    rbp = require_gpu()
+    n_live, cap, head = 3000, 4096, 4000
+    rng = np.random.default_rng(int(frac_used * 10))
+    use = np.where(rng.random(n_live) < frac_used, rng.integers(1, 5, n_live), 0)
+    rec, *_ = _records(rbp, n_live, cap, head, 7, use=use)
+    for n_draw in (1, 100, 2500):
+        got = _draw(rbp, rec, cap, rbp.RB_UNUSED_FIRST, 3, 2, n_draw)
+        want = ob.sample_without_replacement(3, 2, n_live, n_draw, use_count=use)
+        assert np.array_equal(got["idx"], want)
+
+
+def test_without_replacement_rejects_bad_requests():
+    rbp = require_gpu()
+    rec, *_ = _records(rbp, 10, 10, 0, 1)
+    with pytest.raises(rbp.RbpError):
+        _draw(rbp, rec, 10, rbp.RB_NO_REPLACE, 1, 0, 11)
+    with pytest.raises(rbp.RbpError):
+        _draw(rbp, rec, 10, rbp.RB_UNUSED_FIRST, 1, 0, 3)  # no use_count
+
+
+def test_note_use_matches_steps_since_last_use():
+    rbp = require_gpu()
+    cap, head, n_live = 64, 50, 60
+    use = torch.zeros(cap, dtype=torch.int32, device="cuda")
+    last = torch.full((cap,), -1, dtype=torch.int64, device="cuda")
+    ws = rbp.workspace(rbp.RBP_OP_NOTE_USE, cap)
+    rng = np.random.default_rng(5)
+    batches, counts = [], np.zeros(n_live, dtype=np.int64)
+    for step in (0, 1, 3, 4, 9, 10, 10):
+        idx = rng.integers(0, n_live, 40).astype(np.int32)  # with replacement: repeats
+        since = torch.empty(40, dtype=torch.int32, device="cuda")
+        rbp.rb_note_use(torch.from_numpy(idx).cuda(), head, cap, step, use, last, since, ws)
+        torch.cuda.synchronize()
+        batches.append((step, idx.tolist()))
+        want = ob.steps_since_last_use(batches)[-1]
+        assert np.array_equal(to_np(since), want), step
+        np.add.at(counts, idx, 1)
+    phys = (head + np.arange(n_live)) % cap
+    assert np.array_equal(to_np(use)[phys], counts)
+    last_want = {}
+    for step, ids in batches:
+        for s in ids:
+            last_want[s] = step
+    assert all(to_np(last)[phys[s]] == (last_want.get(s, -1)) for s in range(n_live))
+
+
+def test_push_is_fifo_with_advantages_at_insert():
+    rbp = require_gpu()
+    cap, slot = 10, 6
+    ring = rbp.make_ring(cap, slot)
+    fifo = ob.FifoBuffer(cap)
+    rng = np.random.default_rng(3)
+    version = 0
+    for sizes in ([4, 4], [3], [4, 2, 4], [1], [5, 5], [2]):
+        version += 1
+        n = sum(sizes)
+        goff = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+        lens = rng.integers(1, 9, n).astype(np.int32)  # some longer than the slot
+        src = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+        rew = (rng.random(n) < 0.5).astype(np.float32)
+        tok = rng.integers(0, 500, int(lens.sum())).astype(np.int32)
+        old = rng.random(int(lens.sum())).astype(np.float32)
+        ring.t["use_count"].fill_(7)  # rows written by the push must be reset
+        print(f"[buffer] push {sizes}", flush=True)
+        rbp.rb_push(ring, torch.from_numpy(goff).cuda(), torch.from_numpy(lens).cuda(),
+                    torch.from_numpy(src).cuda(), torch.from_numpy(rew).cuda(), version,
+                    torch.from_numpy(tok).cuda(), torch.from_numpy(old).cuda())
+        torch.cuda.synchronize()
+        adv = group_advantage(rew, goff)
+        for i in range(n):
+            k = min(int(lens[i]), slot)
+            fifo.push({"len": k, "rew": rew[i], "adv": adv[i], "ver": version,
+                       "tok": tok[src[i]:src[i] + k], "old": old[src[i]:src[i] + k]})
+        assert ring.n_live == len(fifo)
+        t = {k: (None if v is None else to_np(v)) for k, v in ring.t.items()}
+        for s, want in enumerate(fifo.records):
+            r = (ring.head + s) % cap
+            assert t["length"][r] == want["len"] and t["version"][r] == want["ver"]
+            assert t["reward"][r] == want["rew"]
+            assert abs(t["advantage"][r] - want["adv"]) <= 1e-5 * abs(want["adv"]) + 1e-6
+            o = t["arena_off"][r]
+            assert o == r * slot
+            assert np.array_equal(t["arena_tokens"][o:o + want["len"]], want["tok"])
+            assert np.array_equal(t["arena_old_logp"][o:o + want["len"]], want["old"])
+        written = (ring.head + len(fifo) - n + np.arange(n)) % cap
+        assert np.all(t["use_count"][written] == 0) and np.all(t["last_step"][written] == -1)
+    # the filled ring feeds the sampler: a uniform draw gathers the FIFO records
+    rec = rbp.ring_records(ring)
+    cfg = rbp.make_sample_cfg(rbp.RB_UNIFORM, rbp.RB_LAYOUT_PACKED, 2, 0, 6, max_tokens=64)
+    out = rbp.alloc_batch(cfg)
+    rbp.rb_sample_gather(rec, cfg, out, rbp.workspace(rbp.RBP_OP_SAMPLE_GATHER, cap))
+    torch.cuda.synchronize()
+    idx = ob.sample_indices([0.0] * cap, ob.RB_UNIFORM, 2, 0, 6)
+    assert np.array_equal(to_np(out["idx"]), idx)
+    want_tok = np.concatenate([fifo.records[s]["tok"] for s in idx])
+    assert np.array_equal(to_np(out["tokens"])[:len(want_tok)], want_tok)
+    with pytest.raises(rbp.RbpError):
+        rbp.rb_push(ring, torch.tensor([0, 11], dtype=torch.int32, device="cuda"),
+                    torch.ones(11, dtype=torch.int32, device="cuda"),
+                    torch.zeros(11, dtype=torch.int64, device="cuda"),
+                    torch.zeros(11, device="cuda"), 0,
+                    torch.zeros(1, dtype=torch.int32, device="cuda"), torch.zeros(1, device="cuda"))
