@@ -37,13 +37,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # 1.0).  Only valid for the sources the counters were read on.
 TRAFFIC_SOURCES = ("logprob.hip", "logits_epilogue.h", "gemm_core.h", "gemm_dma.h")
 TRAFFIC = {
-    "sources_sha256": "e294450e0a07a15b59a31e2bcb60ef1b2e933ee15a5d505613f2fad2673d0fbb",
-    "fetch_bytes": {"logits_lse_partial_kernel": 27484116608,   # 13420347 KiB x 2.0
-                    "lse_merge_kernel": 373010553},             # 182139 KiB x 2.0
-    "write_bytes": {"logits_lse_partial_kernel": 116942797,     # 114202 KiB
-                    "lse_merge_kernel": 265267},                # 259.1 KiB
+    "sources_sha256": "78fe1fefd605393ebd78c43c51d252cc5728c461881cf170f09db4aafbb85c65",
+    "fetch_bytes": {"logits_lse_partial_kernel": 27462468267,   # 13409408 KiB x 2.0
+                    "lse_merge_kernel": 372858197},             # 182060 KiB x 2.0
+    "write_bytes": {"logits_lse_partial_kernel": 116926805,     # 114186 KiB
+                    "lse_merge_kernel": 264875},                # 258.7 KiB
 }
-
 
 def parse():
     ap = argparse.ArgumentParser()
