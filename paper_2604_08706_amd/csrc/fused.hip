@@ -66,8 +66,8 @@ __device__ __forceinline__ void q_pack(const f32x16& acc, float ls, int mi, int 
     const float z = acc[rg * 4 + i];
     q[i] = exp2_hw(fmaf(z, kLog2e, -ls));
     if constexpr (!kFull)
-      q[i] = __uint_as_float(select_neg(GL::row_off(mi, rg * 4 + i) - lim,
-                                        __float_as_uint(q[i]), 0u));
+      q[i] = __uint_as_float(select_below(GL::row_off(mi, rg * 4 + i), lim,
+                                          __float_as_uint(q[i]), 0u));
     S += q[i];
     E = fmaf(q[i], z, E);
   }

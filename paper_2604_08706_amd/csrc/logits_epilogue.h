@@ -38,14 +38,17 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
-// (a & mask) | (b & ~mask) with mask = all ones where x < 0: written as two
-// vector bit instructions in assembly, because the compiler would otherwise
-// turn the sign test into a compare whose lane mask lives in scalar registers
-// (64 of them live at once overflow the scalar file); volatile so that the
-// masked values are recomputed where used rather than kept live.
-__device__ __forceinline__ uint32_t select_neg(int32_t x, uint32_t a, uint32_t b) {
+// a where off < lim, else b, as (a & mask) | (b & ~mask) with mask = all ones
+// where off - lim < 0: three vector instructions in assembly.  A plain
+// compare would become a lane mask in scalar registers (64 of them live at
+// once overflow the scalar file), and a plain subtraction would be computed
+// once and kept live for every later use (64 values per pass over a tile);
+// volatile, so that every use forms its own difference and mask.
+__device__ __forceinline__ uint32_t select_below(int off, int32_t lim, uint32_t a, uint32_t b) {
+  int32_t d;
   uint32_t m, r;
-  asm volatile("v_ashrrev_i32 %0, 31, %1" : "=v"(m) : "v"(x));
+  asm volatile("v_sub_u32 %0, %1, %2" : "=v"(d) : "i"(off), "v"(lim));
+  asm volatile("v_ashrrev_i32 %0, 31, %1" : "=v"(m) : "v"(d));
   asm volatile("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(a), "v"(b));
   return r;
 }
@@ -56,7 +59,7 @@ __device__ __forceinline__ uint32_t select_neg(int32_t x, uint32_t a, uint32_t b
 template <bool kFull>
 __device__ __forceinline__ float logit_or_ninf(float v, int off, int32_t lim) {
   if constexpr (kFull) return v;
-  return __uint_as_float(select_neg(off - lim, __float_as_uint(v), 0xff800000u));
+  return __uint_as_float(select_below(off, lim, __float_as_uint(v), 0xff800000u));
 }
 
 // Per token column of this wave's 128 x 64 block: max and sum exp(z - max)
@@ -179,8 +182,8 @@ __device__ __forceinline__ void dz_pack(const f32x16& acc, float ls, float dl, i
   for (int i = 0; i < 4; ++i) {
     g[i] = -dl * exp2_hw(fmaf(acc[rg * 4 + i], kLog2e, -ls));
     if constexpr (!kFull)  // rows past the vocabulary hold zeros
-      g[i] = __uint_as_float(select_neg(GL::row_off(mi, rg * 4 + i) - lim,
-                                        __float_as_uint(g[i]), 0u));
+      g[i] = __uint_as_float(select_below(GL::row_off(mi, rg * 4 + i), lim,
+                                          __float_as_uint(g[i]), 0u));
   }
   P0 = pack_bf16x2(g[0], g[1]);
   P1 = pack_bf16x2(g[2], g[3]);
