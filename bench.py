@@ -44,6 +44,293 @@ TRAFFIC = {
                     "lse_merge_kernel": 264192},                # 258.0 KiB
 }
 
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="head7b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=3072,
+                    help="tokens of the bounded sample the CPU oracle is timed on")
+    ap.add_argument("--no-aux", action="store_true",
+                    help="skip the HBM-rate measurement of sample+gather and loss on the "
+                         "10^6-record stress buffer")
+    ap.add_argument("--no-fused", action="store_true",
+                    help="skip the separately reported single-pass policy_fused_fwd_bwd leg")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB three "
+                         "times (calibrates the HBM byte counters) and exit")
+    return ap.parse_args()
+
+
+def copy_probe(mib):
+    """A plain copy of known size, for scaling FETCH_SIZE / WRITE_SIZE."""
+    import torch
+
+    n = mib << 18  # float32 elements
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4}))
+
+
+def sources_sha256():
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, "paper_2604_08706_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_bytes():
+    """HBM bytes per forward call, or None once the kernel sources differ
+    from the ones the counters were read on."""
+    if TRAFFIC is None or TRAFFIC["sources_sha256"] != sources_sha256():
+        return None
+    return sum(TRAFFIC["fetch_bytes"].values()) + sum(TRAFFIC["write_bytes"].values())
+
+
+def setup(wl, seed=0):
+    import torch
+
+    import paper_2604_08706_amd as rbp
+    from paper_2604_08706_amd import workloads as wlm
+
+    dev = "cuda"
+    T = wl.max_tokens
+    tab = wlm.record_table(wl, seed)
+    total = int(tab.length.sum())
+    S = {}
+    S["rewards"] = torch.from_numpy(tab.reward).to(dev)
+    S["group_off"] = torch.from_numpy(tab.group_off).to(dev)
+    S["adv_rec"] = torch.zeros(len(tab.length), dtype=torch.float32, device=dev)
+    S["len_rec"] = torch.from_numpy(tab.length.astype(np.int32)).to(dev)
+    S["off_rec"] = torch.from_numpy(tab.arena_off).to(dev)
+    S["ver_rec"] = torch.from_numpy(tab.version).to(dev)
+    S["arena_tok"] = wlm.arena_tokens(total, wl.V, seed, device=dev)
+    S["arena_old"] = torch.zeros(total, dtype=torch.float32, device=dev)
+    S["rec"] = rbp.make_records(len(tab.length), len(tab.length), 0, S["off_rec"], S["len_rec"],
+                                S["rewards"], S["adv_rec"], S["ver_rec"], S["arena_tok"],
+                                S["arena_old"])
+    hidden, W, _ = wlm.head(T, wl.d, wl.V, seed, device=dev)
+    S["hidden"], S["W"] = hidden, W
+    S["dW"] = torch.zeros((wl.V, wl.d), dtype=torch.float32, device=dev)
+    S["dh"] = torch.empty((T, wl.d), dtype=torch.float32, device=dev)
+    S["logp"] = torch.empty(T, device=dev)
+    S["lse"] = torch.empty(T, device=dev)
+    S["dlogp"] = torch.empty(T, device=dev)
+    S["loss"] = torch.zeros(1, device=dev)
+    S["stats"] = torch.zeros(4, device=dev)
+    S["ws_sample"] = rbp.workspace(rbp.RBP_OP_SAMPLE_GATHER, len(tab.length))
+    S["ws_fwd"] = rbp.workspace(rbp.RBP_OP_LOGPROB_FWD, T, wl.d, wl.V)
+    S["ws_loss"] = rbp.workspace(rbp.RBP_OP_LOSS, T)
+    S["ws_bwd"] = rbp.workspace(rbp.RBP_OP_LOGPROB_BWD, T, wl.d, wl.V)
+    S["T"] = T
+    S["tab"] = tab
+    return S
+
+
+def cfg_for(rbp, wl, step, seed=0):
+    return rbp.make_sample_cfg(rbp.RB_UNIFORM, rbp.RB_LAYOUT_PACKED, seed, step, wl.n_draw,
+                               cur_version=10, max_tokens=wl.max_tokens, token_begin=0)
+
+
+def align_old_logp(rbp, wl, S, steps, noise_sd, seed=0):
+    """Untimed: store behaviour log-probs for the tokens each step will draw,
+    as the current policy's log-probs plus staleness noise (a replayed,
+    slightly stale rollout)."""
+    import torch
+
+    from paper_2604_08706_amd import workloads as wlm
+
+    for k in steps:
+        cfg = cfg_for(rbp, wl, k, seed)
+        out = rbp.alloc_batch(cfg)
+        rbp.rb_sample_gather(S["rec"], cfg, out, S["ws_sample"])
+        rbp.policy_logprob_fwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"],
+                               S["logp"], S["lse"], S["ws_fwd"])
+        seq = out["seq_of_token"].long()
+        ok = seq >= 0
+        pos = torch.arange(S["T"], device="cuda")
+        start = out["cu_seqlens"].long()[seq.clamp(min=0)]
+        src = S["off_rec"][out["idx"].long()[seq.clamp(min=0)]] + (pos - start)
+        noise = wlm.normal(S["T"], noise_sd, 1000 + k, device="cuda")
+        S["arena_old"][src[ok]] = (S["logp"] + noise)[ok]
+    torch.cuda.synchronize()
+
+
+def run_step(rbp, wl, S, step, out, ev=None):
+    rbp.rb_group_advantage(S["rewards"], S["group_off"], S["adv_rec"])
+    rbp.rb_sample_gather(S["rec"], cfg_for(rbp, wl, step), out, S["ws_sample"])
+    if ev is not None:
+        ev[0].record()
+    rbp.policy_logprob_fwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"], S["logp"],
+                           S["lse"], S["ws_fwd"])
+    if ev is not None:
+        ev[1].record()
+    rbp.policy_loss_fwd_bwd(S["logp"], out["old_logp"], out["seq_of_token"], out["adv"],
+                            out["len"], wl.n_draw, S["loss"], S["dlogp"], S["stats"],
+                            S["ws_loss"])
+    if ev is not None:
+        ev[2].record()
+    rbp.policy_logprob_bwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"], S["lse"],
+                           S["dlogp"], S["dh"], S["dW"], S["ws_bwd"], accumulate_dW=True)
+    if ev is not None:
+        ev[3].record()
+
+
+def aux_stress(iters=20):
+    """HBM rate of the two memory-bound steps on the long-sequence stress
+    buffer (10^6 records, ~1.8e9 stored tokens in HBM):
+      sample+gather: 256 positive-mixture draws (p_pos = 0.5), padded to 8192;
+      loss: policy_loss_fwd_bwd over the same draws packed (~4.7e5 tokens).
+      sample_no_replace: the same draws without replacement (per-slot keys and
+      a radix select), padded; note_use: the usage update of 256 draws.
+    Algorithmic bytes: gather = 4 B/record reward scan + 4 B per positive slot
+    + 20 B record metadata per draw + 8 B read per gathered token + 12 B
+    written per padded position (without replacement: 8 B per record key in
+    place of the reward scan); loss = 16 B per token (logp, old_logp,
+    seq_of_token read, dlogp written) + 8 B per sequence."""
+    import torch
+
+    import paper_2604_08706_amd as rbp
+    from paper_2604_08706_amd import workloads as wlm
+
+    dev = "cuda"
+    wl = wlm.WORKLOADS["stress"]
+    tab = wlm.record_table(wl, 3)
+    n = len(tab.length)
+    total = int(tab.length.sum())
+    tok = wlm.arena_tokens(total, wl.V, 3, device=dev)
+    old = wlm.normal(total, 1.0, 4, device=dev)
+    adv = wlm.normal(n, 1.0, 5, device=dev)
+    keep = (torch.from_numpy(tab.arena_off).to(dev),
+            torch.from_numpy(tab.length.astype(np.int32)).to(dev),
+            torch.from_numpy(tab.reward).to(dev), adv, torch.from_numpy(tab.version).to(dev))
+    rec = rbp.make_records(n, n, 0, *keep, tok, old)
+    p_q32 = int(wl.p_pos * 2.0 ** 32)  # floor(p_pos * 2^32), the sampler's coin threshold
+    n_pos = int((tab.reward > 0).sum())
+    ws = rbp.workspace(rbp.RBP_OP_SAMPLE_GATHER, n)
+
+    def cfg(step, layout, **kw):
+        return rbp.make_sample_cfg(rbp.RB_POS_MIX, layout, 3, step, wl.n_draw, p_pos_q32=p_q32,
+                                   cur_version=tab.cur_version, **kw)
+
+    c_pad = cfg(0, rbp.RB_LAYOUT_PADDED, l_max=wl.l_max)
+    out = rbp.alloc_batch(c_pad)
+    for k in range(3):
+        rbp.rb_sample_gather(rec, cfg(100 + k, rbp.RB_LAYOUT_PADDED, l_max=wl.l_max), out, ws)
+    cfgs = [cfg(i, rbp.RB_LAYOUT_PADDED, l_max=wl.l_max) for i in range(iters)]
+    # The calls take less GPU time than the host needs to issue them: a spin
+    # kernel ahead of the timed region lets all of them queue, so the events
+    # measure the GPU executing them back to back.
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for c in cfgs:
+        rbp.rb_sample_gather(rec, c, out, ws)
+    b.record()
+    torch.cuda.synchronize()
+    g_ms = a.elapsed_time(b) / iters
+    n_tok = []  # valid tokens per call, from an untimed repeat (draws depend on the step only)
+    for c in cfgs:
+        rbp.rb_sample_gather(rec, c, out, ws)
+        n_tok.append(int(out["n_tokens"].item()))
+    g_bytes = float(np.mean([4 * n + 4 * n_pos + 20 * wl.n_draw + 8 * v
+                             + 12 * wl.n_draw * wl.l_max for v in n_tok]))
+    g_rate = g_bytes / (g_ms / 1e3)
+
+    # without replacement: radix select over the 10^6 per-slot keys, same
+    # layout; then the usage update of the drawn records
+    nr = [rbp.make_sample_cfg(rbp.RB_NO_REPLACE, rbp.RB_LAYOUT_PADDED, 3, i, wl.n_draw,
+                              cur_version=tab.cur_version, l_max=wl.l_max) for i in range(iters)]
+    for c in nr[:3]:
+        rbp.rb_sample_gather(rec, c, out, ws)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for c in nr:
+        rbp.rb_sample_gather(rec, c, out, ws)
+    b.record()
+    torch.cuda.synchronize()
+    nr_ms = a.elapsed_time(b) / iters
+    nr_tok = []
+    for c in nr:
+        rbp.rb_sample_gather(rec, c, out, ws)
+        nr_tok.append(int(out["n_tokens"].item()))
+    nr_bytes = float(np.mean([8 * n + 20 * wl.n_draw + 8 * v + 12 * wl.n_draw * wl.l_max
+                              for v in nr_tok]))
+    uses = torch.zeros(n, dtype=torch.int32, device=dev)
+    last = torch.full((n,), -1, dtype=torch.int64, device=dev)
+    since = torch.empty(wl.n_draw, dtype=torch.int32, device=dev)
+    ws_u = rbp.workspace(rbp.RBP_OP_NOTE_USE, n)
+    rbp.rb_note_use(out["idx"], 0, n, 0, uses, last, since, ws_u)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for i in range(iters):
+        rbp.rb_note_use(out["idx"], 0, n, i + 1, uses, last, since, ws_u)
+    b.record()
+    torch.cuda.synchronize()
+    u_ms = a.elapsed_time(b) / iters
+
+    # loss over the draws packed (one micro-batch holding every drawn token)
+    c_pk = cfg(0, rbp.RB_LAYOUT_PACKED, max_tokens=wl.n_draw * wl.l_max)
+    pk = rbp.alloc_batch(c_pk)
+    rbp.rb_sample_gather(rec, c_pk, pk, ws)
+    T = int(pk["n_tokens"].item())
+    old_t = pk["old_logp"][:T]
+    logp = old_t + wlm.normal(T, 0.05, 6, device=dev)
+    seq = pk["seq_of_token"][:T]
+    dlogp = torch.empty(T, device=dev)
+    loss = torch.zeros(1, device=dev)
+    stats = torch.zeros(4, device=dev)
+    ws_l = rbp.workspace(rbp.RBP_OP_LOSS, T)
+    for _ in range(3):
+        rbp.policy_loss_fwd_bwd(logp, old_t, seq, pk["adv"], pk["len"], wl.n_draw, loss, dlogp,
+                                stats, ws_l)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(iters):
+        rbp.policy_loss_fwd_bwd(logp, old_t, seq, pk["adv"], pk["len"], wl.n_draw, loss, dlogp,
+                                stats, ws_l)
+    b.record()
+    torch.cuda.synchronize()
+    l_ms = a.elapsed_time(b) / iters
+    l_bytes = 16 * T + 8 * wl.n_draw
+    del tok, old, keep, rec
+    torch.cuda.empty_cache()
+    return {
+        "workload": "stress: 10^6 records, 256 positive-mixture draws (p_pos 0.5), "
+                    "log-normal lengths capped at 8192",
+        "sample_gather": {"layout": "padded [256, 8192]", "ms": round(g_ms, 4),
+                          "tokens": int(np.mean(n_tok)),
+                          "bytes": int(g_bytes),
+                          "GB/s": round(g_rate / 1e9, 1),
+                          "frac_hbm": round(g_rate / PEAK_HBM, 4)},
+        "sample_no_replace": {"layout": "padded [256, 8192]", "ms": round(nr_ms, 4),
+                              "tokens": int(np.mean(nr_tok)), "bytes": int(nr_bytes),
+                              "GB/s": round(nr_bytes / (nr_ms / 1e3) / 1e9, 1),
+                              "frac_hbm": round(nr_bytes / (nr_ms / 1e3) / PEAK_HBM, 4)},
+        "note_use": {"draws": wl.n_draw, "ms": round(u_ms, 4)},
+        "loss": {"tokens": T, "ms": round(l_ms, 4), "bytes": l_bytes,
+                 "GB/s": round(l_bytes / (l_ms / 1e3) / 1e9, 1),
+                 "frac_hbm": round(l_bytes / (l_ms / 1e3) / PEAK_HBM, 4)},
+    }
+
+
 def cpu_baseline(wl, n_tokens, seed=0):
     """The oracle (fp64 numpy) timed on a bounded sample of the same workload:
     the buffer draw and gather, then log-probs, loss and backward over the
