@@ -436,7 +436,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
-              "data-parallel path is a design note, not part of this build", file=sys.stderr)
+              "data-parallel path is described in the design notes, not implemented", file=sys.stderr)
         sys.exit(2)
     import torch
 

@@ -60,7 +60,7 @@ extern "C" {
 enum {
   RBP_OK = 0,
   RBP_EINVAL = -1,       /* a null pointer, a size out of range, a bad enum     */
-  RBP_EUNSUPPORTED = -2, /* a shape this build does not handle (e.g. d % 8)     */
+  RBP_EUNSUPPORTED = -2, /* a shape the kernels do not handle (e.g. d % 8)      */
   RBP_EWORKSPACE = -3,   /* workspace too small (see rbp_workspace_bytes)       */
   RBP_EHIP = -4          /* a HIP launch failed                                 */
 };

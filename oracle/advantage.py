@@ -7,7 +7,7 @@ gets A_i = (r_i - mean of the group's rewards) / (std of the group's rewards),
 computed at generation time and stored with the rollout (not recomputed when
 the rollout is replayed).
 
-Readings (R5): the paper says only "std".  The standard deviation uses ``ddof``
+The paper says only "std".  The standard deviation uses ``ddof``
 (default 1, the sample estimate), ``eps`` (default 1e-6) is added to it, and a
 group whose rewards are all equal (std exactly 0, which includes G = 1) gets
 A = 0 exactly.

@@ -9,14 +9,14 @@ Paper passages followed:
   (first in, first out); sampling does not remove entries.
 * Sec. 4 (synchronous analysis) and App. C.1: a minibatch of B draws is taken
   uniformly from the buffer *with replacement*; the pseudo-code's library call
-  samples without replacement -- this build follows the analysis (reading R7).
+  samples without replacement -- the analysis is followed here.
 * Sec. 5 ("Further optimization") and App. D.4 ("Positive-bias sampling"): with
   coefficient delta the buffer keeps the freshest (1-delta)N rollouts and, among
   the rollouts not in that fresh part, the freshest delta*N correct ones; the
   sampler draws uniformly over what is kept.  delta = 0 is plain uniform.
   Pinned by the worked example of App. D.4, which the rule reproduces at
-  delta = 0.5 (the example prints 0.75; reading R8).
-* Positive-prioritised mixture (p_pos): not in the paper (reading R9).  A coin
+  delta = 0.5 (the example prints 0.75).
+* Positive-prioritised mixture (p_pos): not in the paper.  A coin
   with probability p_pos picks the positive stratum, otherwise the draw is over
   all live records; with no positives the draw falls back to all records.
 
@@ -25,7 +25,7 @@ Paper passages followed:
   the same after first taking records never used before.  Defined here as the
   B records with the smallest per-record random keys (a uniformly random
   B-subset), listed in slot order; "at least once" ranks never-used records
-  ahead of used ones (reading R17).
+  ahead of used ones.
 * Steps-since-last-use (App. D.3, "Metrics"): samples are ordered batch by
   batch, in a random order inside a batch (here: draw order); a sample of a
   rollout seen for the first time is "new" (-1 here), any later one gets the

@@ -8,16 +8,16 @@ the current policy's probability of the rollout to the probability recorded
 when the rollout was generated, A the rollout's group advantage (stored at
 generation), eps_low = eps_high = 0.2 and no KL term.
 
-Readings (each listed in the design notes):
+Where the paper leaves a choice open:
 
-* R1 -- the ratio is taken per token, rho_t = exp(logp_t - old_logp_t), and
+* ratio level -- the ratio is taken per token, rho_t = exp(logp_t - old_logp_t), and
   each sequence contributes the mean of its token terms (the GRPO form the
   paper cites); a whole-sequence ratio is a different objective.
-* R2 -- sequence i is weighted 1 / (n_seq * len_i): len_i is its full length
+* normalisation -- sequence i is weighted 1 / (n_seq * len_i): len_i is its full length
   (also when a micro-batch holds only part of it), n_seq the number of sampled
   sequences in the optimizer batch (duplicated draws count twice).
-* R3 -- the paper maximises J; ``loss = -J`` and all gradients are of ``loss``.
-* R4 -- the gradient of a token term is rho*A when the unclipped branch is
+* sign -- the paper maximises J; ``loss = -J`` and all gradients are of ``loss``.
+* clip gradient -- the gradient of a token term is rho*A when the unclipped branch is
   taken or the ratio lies inside [1 - eps_low, 1 + eps_high] (closed), and 0
   when the clipped branch is taken strictly outside it:
   act_t = 0 iff (A > 0 and rho > 1 + eps_high) or (A < 0 and rho < 1 - eps_low).
@@ -85,10 +85,10 @@ def grpo_loss(logp, old_logp, seq_of_token, adv, seq_len, n_seq, eps_low=0.2,
 # rollouts of the optimizer batch (as for GRPO); no ratio, no clip, no
 # per-token length normalisation (log pi is a sum over the rollout's tokens).
 #
-# Sequence-ratio GRPO (R1's alternative reading, R16): rho_i =
+# Sequence-ratio GRPO (the printed formula taken literally): rho_i =
 # pi(z_i|q) / pi_old(z_i|q) = exp(sum_{t in i} (logp_t - old_logp_t)),
 # J = (1/n_seq) sum_i min(rho_i A_i, clip(rho_i, 1 - eps_low, 1 + eps_high) A_i),
-# with the clip-gradient rule of R4 applied to rho_i.  The sum runs over the
+# with the clip-gradient rule above applied to rho_i.  The sum runs over the
 # whole rollout, so a call must hold complete sequences (given by cu_seqlens).
 
 

@@ -13,7 +13,7 @@ Pinned by: the published known-answer vector for counter = key = 0, and by
 numpy's independent implementation (``numpy.random.Philox`` is Philox4x64-10)
 on random keys and counters (tests/test_oracle_philox.py).
 
-Derived draws (this build's definition; the paper fixes none of it):
+Derived draws (defined here; the paper fixes none of it):
 
 * draw ``j`` of sampling step ``step`` under ``seed`` reads the block
   ``philox(counter=(j, step, 0, 0), key=(seed, 0))`` -> four 64-bit words

@@ -56,7 +56,8 @@ def _loss_case(T, B, seed, noise, margin=1e-3):
     seq[rng.random(T) < 0.05] = -1   # some padding inside the batch
     logp = (-rng.random(T) * 12.0).astype(np.float32)
     old = (logp + rng.normal(0, noise, T)).astype(np.float32)
-    # keep every ratio >= margin away from the clip boundaries (reading R4)
+    # keep every ratio >= margin away from the clip boundaries, where fp32 and
+    # fp64 log-probs (within ~1e-6) could take different branches
     rho = np.exp(logp.astype(np.float64) - old.astype(np.float64))
     near = (np.abs(rho - 0.8) < margin) | (np.abs(rho - 1.2) < margin)
     old[near] -= np.float32(5 * margin)

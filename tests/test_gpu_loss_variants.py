@@ -76,7 +76,8 @@ def test_seq_ratio_loss_matches_oracle(B, mean_len, noise):
     logp = (-rng.random(T) * 8).astype(np.float32)
     old = (logp + rng.normal(0, noise, T)).astype(np.float32)
     adv = rng.standard_normal(B).astype(np.float32)
-    # keep every sequence ratio away from the clip boundaries (reading R4)
+    # keep every sequence ratio away from the clip boundaries, where fp32 and
+    # fp64 could take different branches
     s = np.array([np.sum(logp[cu[i]:cu[i + 1]].astype(np.float64) - old[cu[i]:cu[i + 1]])
                   for i in range(B)])
     for i in range(B):

@@ -33,7 +33,7 @@ def test_paper_worked_example_positive_bias(golden_dir):
 
 
 def test_worked_example_at_printed_delta_differs():
-    # reading R8: at delta = 0.75 the stated rule does not give the printed set
+    # at the printed delta = 0.75 the stated rule does not give the printed set
     correct = [False, True, True, False, True, True, False, True, False, False]
     rewards = [1.0 if c else 0.0 for c in correct]
     kept = ob.retained_set(rewards, *ob.retain_split(8, 0.75))
@@ -107,7 +107,7 @@ def test_pos_mix_p0_equals_uniform_and_p1_only_positives():
 
 
 def test_pos_mix_fraction_chi_square():
-    # expected positive fraction p + (1 - p) f_pos (reading R9)
+    # expected positive fraction p + (1 - p) f_pos
     rng = np.random.default_rng(4)
     rewards = (rng.random(1000) < 0.3).astype(float)
     f_pos = rewards.mean()
