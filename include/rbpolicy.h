@@ -395,7 +395,9 @@ typedef struct rb_ring {
  * [n_new]; src_off device int64 [n_new]: record i's tokens / behaviour
  * log-probs are tokens / old_logp[src_off[i] .. + length[i]).  A record longer
  * than slot_tokens keeps its first slot_tokens tokens (its stored length is
- * cut to that).  version is stored for every new record.
+ * cut to that).  version is stored for every new record.  The device-side
+ * group_off, length and src_off are trusted (not read on the host): offsets
+ * outside the given arrays are the caller's error.
  * Errors: RBP_EINVAL (null pointers, n_new outside [1, capacity],
  *         n_groups < 1, n_live outside [0, capacity], head outside
  *         [0, capacity), slot_tokens < 1, ddof not 0 or 1, eps < 0).
@@ -411,8 +413,8 @@ int rb_push(rb_ring* ring, int32_t n_new, int32_t n_groups, const int32_t* group
  * ("new"), 0 if an earlier draw of this batch took the same record, else
  * step - last_step of the record; then every drawn record gets
  * last_step = step and use_count += its number of draws.  idx device int32
- * [n_draw] (slots as rb_sample_gather writes them); head, capacity as in the
- * record table; use_count device int32, last_step device int64 [capacity];
+ * [n_draw] (slots as rb_sample_gather writes them, trusted to lie below the
+ * table's n_live); head, capacity as in the record table; use_count device int32, last_step device int64 [capacity];
  * since device int32 [n_draw] (may be NULL).  Steps must not decrease
  * between calls.
  * ws device, >= rbp_workspace_bytes(RBP_OP_NOTE_USE, capacity, 0, 0).

@@ -416,9 +416,12 @@ def make_ring(capacity, slot_tokens, device="cuda", counters=True):
 
 
 def ring_records(ring):
-    """rb_records view of a ring (for rb_sample_gather)."""
+    """rb_records view of a ring (for rb_sample_gather); the ring must hold at
+    least one record."""
+    if ring.n_live < 1:
+        raise ValueError("ring_records: the ring is empty")
     t = ring.t
-    return make_records(max(ring.n_live, 1), ring.capacity, ring.head, t["arena_off"],
+    return make_records(ring.n_live, ring.capacity, ring.head, t["arena_off"],
                         t["length"], t["reward"], t["advantage"], t["version"],
                         t["arena_tokens"], t["arena_old_logp"], t["use_count"])
 
