@@ -375,7 +375,35 @@ def cpu_baseline(wl, n_tokens, seed=0):
             "kind": "oracle",
             "sample": f"{n_tokens} tokens of one {wl.max_tokens}-token micro-batch at "
                       f"d={wl.d}, V={wl.V} (sample+gather, advantages, log-probs, loss, "
-                      f"backward in fp64 numpy); {dt:.1f} s"}
+                      f"backward in fp64 numpy); {dt:.1f} s",
+            "stress_sample_gather": cpu_sampler_stress()}
+
+
+def cpu_sampler_stress(seed=3):
+    """The oracle's positive-mixture draw and padded gather on the 10^6-record
+    stress buffer (the GPU's sample_gather line in memory_bound_steps), with
+    the same algorithmic bytes.  The token arena is allocated as zeros (mapped
+    lazily), so only the drawn records' stretches are touched."""
+    from oracle import buffer as ob
+    from paper_2604_08706_amd import workloads as wlm
+
+    wl = wlm.WORKLOADS["stress"]
+    tab = wlm.record_table(wl, seed)
+    n = len(tab.length)
+    total = int(tab.length.sum())
+    tok = np.zeros(total, dtype=np.int32)
+    old = np.zeros(total, dtype=np.float32)
+    p_q32 = int(wl.p_pos * 2.0 ** 32)
+    t0 = time.perf_counter()
+    idx = ob.sample_indices(tab.reward, ob.RB_POS_MIX, seed, 0, wl.n_draw, p_q32=p_q32)
+    g = ob.gather(idx, tab.arena_off, tab.length, np.zeros(n), tab.version, tok, old,
+                  tab.cur_version, ob.LAYOUT_PADDED, l_max=wl.l_max)
+    dt = time.perf_counter() - t0
+    n_pos = int((tab.reward > 0).sum())
+    nbytes = 4 * n + 4 * n_pos + 20 * wl.n_draw + 8 * g["n_tokens"] + 12 * wl.n_draw * wl.l_max
+    return {"ms": round(dt * 1e3, 1), "tokens": int(g["n_tokens"]),
+            "GB/s": round(nbytes / dt / 1e9, 4), "cores": 1,
+            "sample": f"{wl.n_draw} draws from {n} records, padded [{wl.n_draw}, {wl.l_max}]"}
 
 
 def run_step_fused(rbp, wl, S, step, out, ev=None):
