@@ -33,7 +33,9 @@
  *   - Tensors are dense, row-major and contiguous.  bf16 tensors are passed as
  *     uint16_t bit patterns (IEEE binary32 truncated to its upper 16 bits).
  *   - The caller owns and allocates every buffer, workspace included; the
- *     library never allocates, frees or synchronises.  Size the workspace with
+ *     library never allocates memory, frees or synchronises (one exception,
+ *     policy_fused_fwd_bwd, owns a stream and two events per device; see
+ *     there).  Size the workspace with
  *     rbp_workspace_bytes().  Workspace contents are scratch between calls.
  *   - All device work is enqueued on `stream` (a hipStream_t; NULL = the null
  *     stream) and is asynchronous to the host.
@@ -335,6 +337,12 @@ int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
  * exp(z - max) for every vocabulary entry as bf16 in the workspace (2 V bytes
  * per token; it does materialise a T x V array, which policy_logprob_fwd
  * never does).  dz is rounded to bf16 twice instead of once.
+ * Overlap: on its first call on a device the entry creates one stream of
+ * default priority and two events there, kept until the process ends; it
+ * runs the second half of its HBM-bound rescale on that stream beside the
+ * first half of the dW product, ordered against `stream` by the events, so
+ * all its work is complete in `stream` order when later work on `stream`
+ * runs.
  * Arguments: hidden, W, tokens, seq_of_token as in policy_logprob_fwd
  * (seq_of_token required); old_logp, adv, seq_len, B, n_seq_total, eps_low,
  * eps_high, loss_accum, stats as in policy_loss_fwd_bwd (loss_accum and stats

@@ -25,6 +25,8 @@
 // the workspace).  dz is rounded to bf16 twice (q, then the scaled value)
 // instead of once.
 
+#include <mutex>
+
 #include "logits_epilogue.h"
 #include "rbp_internal.h"
 
@@ -274,12 +276,13 @@ __global__ void __launch_bounds__(256) grad_scale_kernel(
     uint16_t* __restrict__ Qt, int64_t ldQ, int64_t T256, const float* __restrict__ pM,
     int64_t ldp, const float* __restrict__ lse, const float* __restrict__ logp,
     const float* __restrict__ dlogp, const int32_t* __restrict__ tokens,
-    const int32_t* __restrict__ seq, int64_t Tn, int32_t V) {
+    const int32_t* __restrict__ seq, int64_t Tn, int32_t V, int32_t group0) {
   const int64_t tb = (int64_t)blockIdx.x * kScaleTokens + threadIdx.x * 8;
-  const int32_t v0 = (int32_t)blockIdx.y * 128;
+  const int32_t group = group0 + (int32_t)blockIdx.y;  // 128-row vocabulary group
+  const int32_t v0 = group * 128;
   const int32_t rows = V - v0 < 128 ? V - v0 : 128;
   if (tb >= T256 || rows <= 0) return;
-  const float* m = pM + (int64_t)blockIdx.y * ldp + tb;
+  const float* m = pM + (int64_t)group * ldp + tb;
   float c[8], gy[8];
   int32_t y[8];
 #pragma unroll
@@ -334,6 +337,55 @@ FusedWs carve_fused(void* base, int64_t Tc, int32_t d, int32_t V) {
   return w;
 }
 
+// A second stream per device, owned by the library (created on the first call
+// on that device, default priority, kept for the life of the process), and
+// two events that order it against the caller's stream.  It lets the second
+// half of the in-place rescale (HBM-bound) run beside the first half of the
+// dW product (MFMA-bound); both fit on a CU at once (dW: one 512-thread
+// workgroup, 128 KiB of LDS, ~200 VGPRs per lane; rescale: 40 VGPRs, no LDS).
+struct SideStream {
+  hipStream_t stream = nullptr;
+  hipEvent_t head_done = nullptr, tail_done = nullptr;
+  std::mutex lock;  // serialises event record / wait pairs of concurrent calls
+  bool ready = false;
+};
+SideStream g_side[64];
+
+SideStream* side_stream() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  SideStream& ss = g_side[dev];
+  std::lock_guard<std::mutex> g(ss.lock);
+  if (!ss.ready) {
+    if (hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&ss.head_done, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&ss.tail_done, hipEventDisableTiming) != hipSuccess)
+      return nullptr;
+    ss.ready = true;
+  }
+  return &ss;
+}
+
+// Vocabulary tiles of the first dW part: a multiple of the tiles that make
+// whole rounds of the persistent grid (tiles_d * tv0 % n_cu == 0), nearest
+// half the vocabulary; 0 when no such split exists.
+int64_t head_tiles(int64_t tiles_d, int64_t tiles_v, int n_cu) {
+  int64_t a = tiles_d, b = n_cu;
+  while (b != 0) {
+    const int64_t r = a % b;
+    a = b;
+    b = r;
+  }
+  const int64_t step = n_cu / a;
+  int64_t best = 0;
+  for (int64_t t = step; t < tiles_v; t += step) {
+    const int64_t dist = t > tiles_v / 2 ? t - tiles_v / 2 : tiles_v / 2 - t;
+    const int64_t bdist = best > tiles_v / 2 ? best - tiles_v / 2 : tiles_v / 2 - best;
+    if (best == 0 || dist < bdist) best = t;
+  }
+  return best;
+}
+
 }  // namespace
 
 size_t rbp::fused_ws(int64_t Tc, int32_t d, int32_t V) {
@@ -386,6 +438,7 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
               "policy_fused_fwd_bwd: workspace of %zu bytes holds no 256-token chunk (needs %zu)",
               ws_bytes, rbp::fused_ws(256, d, V));
   const FusedWs w = carve_fused(ws, Tc, d, V);
+  SideStream* side = side_stream();
   const int64_t Vp = round256(V), tiles_v = Vp / 256;
   const int n_cu = device_cus();
   for (int64_t t0 = 0; t0 < T; t0 += Tc) {
@@ -405,12 +458,50 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
                                        n_seq_total, eps_low, eps_high, loss_accum, dlogp + t0,
                                        stats, w.loss, w.loss_bytes, stream);
     if (st != RBP_OK) return st;
-    hipLaunchKernelGGL(grad_scale_kernel,
-                       dim3(rbp::ceil_div(T256, kScaleTokens), (unsigned)(Vp / 128)), dim3(256), 0,
-                       s, w.Qt, Tc, T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0, tokens + t0,
-                       sq, Tn, V);
-    rbp::launch_grad_products(Hc, W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, dW,
-                              (accumulate_dW || t0 > 0) ? 1 : 0, s);
+    const int acc = (accumulate_dW || t0 > 0) ? 1 : 0;
+    const unsigned gx = (unsigned)rbp::ceil_div(T256, kScaleTokens);
+    const int64_t tv0 = side ? head_tiles(rbp::ceil_div(d, 256), tiles_v, n_cu) : 0;
+    if (tv0 > 0) {
+      // rescale rows [0, 256 tv0); then, on the side stream, the rest while
+      // dW runs over the first tv0 vocabulary tiles; dW of the rest and
+      // dhidden once both halves are done
+      const int32_t g0 = (int32_t)(tv0 * 2);  // 128-row groups in the head
+      hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)g0), dim3(256), 0, s, w.Qt, Tc,
+                         T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0, tokens + t0, sq, Tn, V,
+                         0);
+      hipError_t e;
+      {
+        std::lock_guard<std::mutex> g(side->lock);
+        e = hipEventRecord(side->head_done, s);
+        if (e == hipSuccess) e = hipStreamWaitEvent(side->stream, side->head_done, 0);
+        if (e == hipSuccess) {
+          hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)(Vp / 128 - g0)), dim3(256),
+                             0, side->stream, w.Qt, Tc, T256, w.pM, Tc, lse + t0, logp + t0,
+                             dlogp + t0, tokens + t0, sq, Tn, V, g0);
+          e = hipGetLastError();
+        }
+        if (e == hipSuccess) e = hipEventRecord(side->tail_done, side->stream);
+      }
+      rbp::launch_dweight(Hc, w.Qt, Tc, Tn, d, V, dW, acc, 0, tv0, s);
+      // waits for the latest rescale tail on the side stream: this call's, or
+      // a later one of a concurrent call (which then comes after it)
+      if (e == hipSuccess) e = hipStreamWaitEvent(s, side->tail_done, 0);
+      if (e != hipSuccess) {
+        // no side-stream work may outlive a failed call
+        (void)hipStreamSynchronize(side->stream);
+        rbp::set_error("policy_fused_fwd_bwd: ordering the side stream failed: %s",
+                       hipGetErrorString(e));
+        return RBP_EHIP;
+      }
+      rbp::launch_dweight(Hc, w.Qt, Tc, Tn, d, V, dW, acc, tv0, tiles_v, s);
+      rbp::launch_dhidden(W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, s);
+    } else {
+      hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)(Vp / 128)), dim3(256), 0, s,
+                         w.Qt, Tc, T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0, tokens + t0,
+                         sq, Tn, V, 0);
+      rbp::launch_grad_products(Hc, W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, dW,
+                                acc, s);
+    }
   }
   RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
   return RBP_OK;

@@ -253,10 +253,11 @@ RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
 
 // Backward step 3: dW[v][m] (+)= sum_t H[t][m] dz[t][v], with A = H read
 // MN-major (m contiguous, k = token) and B = dz^T K-major (rows v, k = token).
+// The launch covers the vocabulary tiles [tn_off, tn_off + tiles_n).
 RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
                                       const uint16_t* __restrict__ Gt, int64_t ldGt, int64_t Tn,
                                       int32_t d, int32_t V, float* __restrict__ dW, int accumulate,
-                                      int64_t tiles_m, int64_t tiles_n) {
+                                      int64_t tiles_m, int64_t tiles_n, int64_t tn_off) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int64_t T8 = (Tn + 7) / 8 * 8;  // dz^T columns Tn..T8 hold zeros
   const Operand A{Hc, d, d, Tn};        // (m = hidden unit, k = token): H[t][m]
@@ -264,7 +265,7 @@ RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
   auto tile_of = [&](int32_t vid) {
     int32_t tm, tn;
     map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
-    return Tile{tm * 256, tn * 256, 0, (int32_t)Tn};
+    return Tile{tm * 256, (tn + (int32_t)tn_off) * 256, 0, (int32_t)Tn};
   };
   auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
     const Tile tile = tile_of(vid);
@@ -373,21 +374,21 @@ extern "C" int policy_logprob_fwd(const uint16_t* hidden, const uint16_t* W,
   return RBP_OK;
 }
 
-void rbp::launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint16_t* Gt,
-                               int64_t ldGt, int64_t Tn, int32_t d, int32_t V, float* dhidden_c,
-                               float* dh_half, float* dW, int accumulate, hipStream_t s) {
-  const int64_t tiles_d = rbp::ceil_div(d, 256), tiles_v = round256(V) / 256;
-  if (Tn == 0) {
-    if (!accumulate) {
-      const int64_t n = (int64_t)V * d;
-      int64_t blocks = rbp::ceil_div(n, 256);
-      if (blocks > 65536) blocks = 65536;
-      hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, s, dW, n);
-    }
-    return;
-  }
+void rbp::launch_dweight(const uint16_t* Hc, const uint16_t* Gt, int64_t ldGt, int64_t Tn,
+                         int32_t d, int32_t V, float* dW, int accumulate, int64_t tn_begin,
+                         int64_t tn_end, hipStream_t s) {
+  const int64_t tiles_d = rbp::ceil_div(d, 256);
+  if (tn_end <= tn_begin) return;
+  hipLaunchKernelGGL(dweight_kernel,
+                     dim3(rbp::gemm::stream_grid(tiles_d * (tn_end - tn_begin), device_cus())),
+                     dim3(GL::kThreads), 0, s, Hc, Gt, ldGt, Tn, d, V, dW, accumulate, tiles_d,
+                     tn_end - tn_begin, tn_begin);
+}
+
+void rbp::launch_dhidden(const uint16_t* W, const uint16_t* Gt, int64_t ldGt, int64_t Tn,
+                         int32_t d, int32_t V, float* dhidden_c, float* dh_half, hipStream_t s) {
   const int n_cu = device_cus();
-  const int64_t tiles_t = rbp::ceil_div(Tn, 256);
+  const int64_t tiles_d = rbp::ceil_div(d, 256), tiles_t = rbp::ceil_div(Tn, 256);
   // dhidden in two K halves when one pass would give each CU only a few
   // tiles (the last, partly empty round would then cost a large share)
   const int64_t tiles_dh = tiles_d * tiles_t;
@@ -402,9 +403,22 @@ void rbp::launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint
     if (blocks > 8192) blocks = 8192;
     hipLaunchKernelGGL(add_f32_kernel, dim3(blocks), dim3(256), 0, s, dhidden_c, dh_half, n4);
   }
-  hipLaunchKernelGGL(dweight_kernel, dim3(rbp::gemm::stream_grid(tiles_d * tiles_v, n_cu)),
-                     dim3(GL::kThreads), 0, s, Hc, Gt, ldGt, Tn, d, V, dW, accumulate, tiles_d,
-                     tiles_v);
+}
+
+void rbp::launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint16_t* Gt,
+                               int64_t ldGt, int64_t Tn, int32_t d, int32_t V, float* dhidden_c,
+                               float* dh_half, float* dW, int accumulate, hipStream_t s) {
+  if (Tn == 0) {
+    if (!accumulate) {
+      const int64_t n = (int64_t)V * d;
+      int64_t blocks = rbp::ceil_div(n, 256);
+      if (blocks > 65536) blocks = 65536;
+      hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, s, dW, n);
+    }
+    return;
+  }
+  launch_dhidden(W, Gt, ldGt, Tn, d, V, dhidden_c, dh_half, s);
+  launch_dweight(Hc, Gt, ldGt, Tn, d, V, dW, accumulate, 0, round256(V) / 256, s);
 }
 
 extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,

@@ -49,6 +49,13 @@ size_t note_use_ws(int64_t capacity);
 void launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint16_t* Gt,
                           int64_t ldGt, int64_t Tn, int32_t d, int32_t V, float* dhidden_c,
                           float* dh_half, float* dW, int accumulate, hipStream_t s);
+// Its two parts: dW rows of the vocabulary tiles [tn_begin, tn_end) (256 rows
+// each), and dhidden (with its split-K sum).
+void launch_dweight(const uint16_t* Hc, const uint16_t* Gt, int64_t ldGt, int64_t Tn, int32_t d,
+                    int32_t V, float* dW, int accumulate, int64_t tn_begin, int64_t tn_end,
+                    hipStream_t s);
+void launch_dhidden(const uint16_t* W, const uint16_t* Gt, int64_t ldGt, int64_t Tn, int32_t d,
+                    int32_t V, float* dhidden_c, float* dh_half, hipStream_t s);
 
 }  // namespace rbp
 
