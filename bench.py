@@ -35,13 +35,13 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # read for a plain copy of known size (--copy-probe-mib: a 1 GiB copy reads
 # 524302 KiB of FETCH_SIZE, factor 2.0, and 1048576 KiB of WRITE_SIZE, factor
 # 1.0).  Only valid for the sources the counters were read on.
-TRAFFIC_SOURCES = ("logprob.hip", "logits_epilogue.h", "gemm_core.h", "gemm_dma.h")
+TRAFFIC_SOURCES = ("logprob_fwd.hip", "logits_epilogue.h", "gemm_core.h", "gemm_dma.h")
 TRAFFIC = {
-    "sources_sha256": "033a9c3d1a50806a1905286fc4f838a4dfa2ee97ad8d9719a4e9a8e7dd99744b",
-    "fetch_bytes": {"logits_lse_partial_kernel": 27354198699,   # 13356542 KiB x 2.0
-                    "lse_merge_kernel": 373326507},             # 182288 KiB x 2.0
-    "write_bytes": {"logits_lse_partial_kernel": 117253461,     # 114505 KiB
-                    "lse_merge_kernel": 264192},                # 258.0 KiB
+    "sources_sha256": "68f56381a8d242e03d64188a366a6dd74babf5ebe4fb7abdd64aa5e495fd5bd2",
+    "fetch_bytes": {"logits_lse_partial_kernel": 26987301547,   # 13177393 KiB x 2.0
+                    "lse_merge_kernel": 373289643},             # 182270 KiB x 2.0
+    "write_bytes": {"logits_lse_partial_kernel": 117858304,     # 115096 KiB
+                    "lse_merge_kernel": 265216},                # 259.0 KiB
 }
 
 

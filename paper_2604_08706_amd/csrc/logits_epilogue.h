@@ -1,4 +1,5 @@
-// Device helpers shared by the log-prob products (logprob.hip, fused.hip):
+// Device helpers shared by the log-prob products (logprob_fwd.hip,
+// logprob_bwd.hip, fused.hip):
 // the 8-wave tile grid, exponentials, per-column (max, sum exp) reductions of
 // a 256 x 256 logit tile, wave reductions, the target-logit dot product and the
 // transposing bf16 store of a tile into a vocabulary-major [v][t] array.
