@@ -204,3 +204,44 @@ def test_fused_reproducible_empty_and_bad_args():
                                  a["dh"], a["dW"],
                                  torch.empty(16, dtype=torch.uint8, device="cuda"))
     assert e.value.status == rbp.RBP_EWORKSPACE
+
+
+def test_fused_concurrent_calls_on_two_streams():
+    """Two host threads run the single pass on their own streams at once (the
+    library's side stream and events are shared between them); every result
+    must equal the same call made alone."""
+    import threading
+
+    rbp = require_gpu()
+    T, d, V = 2048, 512, 70000  # large enough that the overlapped path runs
+    cases = []
+    for seed in (31, 32):
+        (hidden, W, tokens, seq, lens, *_r) = _case(T, d, V, 0.02, seed, device="cuda")
+        old, adv = _r[-2], _r[-1]
+        cases.append((rbp, hidden, W, tokens, torch.from_numpy(seq).cuda(),
+                      torch.from_numpy(old).cuda(), torch.from_numpy(adv).cuda(),
+                      torch.from_numpy(lens).cuda(), len(lens)))
+    alone = [_run(*c) for c in cases]
+    results = [[None] * 3 for _ in cases]
+    errors = []
+
+    def worker(i):
+        try:
+            st = torch.cuda.Stream()
+            with torch.cuda.stream(st):
+                for k in range(3):
+                    results[i][k] = _run(*cases[i])
+        except Exception as e:  # reported by the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for i in range(2):
+        for k in range(3):
+            for key in ("logp", "lse", "entropy", "dlogp", "dh", "dW"):
+                assert torch.equal(results[i][k][key], alone[i][key]), (i, k, key)
