@@ -366,9 +366,11 @@ SideStream* side_stream() {
   return &ss;
 }
 
-// Vocabulary tiles of the first dW part: a multiple of the tiles that make
-// whole rounds of the persistent grid (tiles_d * tv0 % n_cu == 0), nearest
-// half the vocabulary; 0 when no such split exists.
+// Vocabulary tiles of the first dW part: the smallest multiple of the tiles
+// that make whole rounds of the persistent grid (tiles_d * tv0 % n_cu == 0)
+// that is at least a fifth of the vocabulary -- the rescale of the rest, run
+// beside it, then still finishes within it -- and leaves some tiles over; 0
+// when no such split exists.
 int64_t head_tiles(int64_t tiles_d, int64_t tiles_v, int n_cu) {
   int64_t a = tiles_d, b = n_cu;
   while (b != 0) {
@@ -377,13 +379,9 @@ int64_t head_tiles(int64_t tiles_d, int64_t tiles_v, int n_cu) {
     b = r;
   }
   const int64_t step = n_cu / a;
-  int64_t best = 0;
-  for (int64_t t = step; t < tiles_v; t += step) {
-    const int64_t dist = t > tiles_v / 2 ? t - tiles_v / 2 : tiles_v / 2 - t;
-    const int64_t bdist = best > tiles_v / 2 ? best - tiles_v / 2 : tiles_v / 2 - best;
-    if (best == 0 || dist < bdist) best = t;
-  }
-  return best;
+  for (int64_t t = step; t < tiles_v; t += step)
+    if (5 * t >= tiles_v) return t;
+  return 0;
 }
 
 }  // namespace
