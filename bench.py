@@ -59,6 +59,10 @@ def parse():
                          "10^6-record stress buffer")
     ap.add_argument("--no-fused", action="store_true",
                     help="skip the separately reported single-pass policy_fused_fwd_bwd leg")
+    ap.add_argument("--blas-probe", action="store_true",
+                    help="only time the vendor library's plain bf16 GEMM on the forward's "
+                         "shape (W [V, d] x hidden^T [d, T], torch.mm) as a practical "
+                         "ceiling, print one JSON line and exit")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB three "
                          "times (calibrates the HBM byte counters) and exit")
@@ -77,6 +81,35 @@ def copy_probe(mib):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4}))
+
+
+def blas_probe(steps=10, warmup=3):
+    """Z^T = W H^T in bf16 through torch.mm (hipBLASLt) at the 7B head shape:
+    the same 2*T*d*V flop as the forward product, with no log-sum-exp, both
+    operands contiguous.  A measurement of the vendor GEMM, not a product path."""
+    import torch
+
+    from paper_2604_08706_amd import workloads as wlm
+
+    wl = wlm.WORKLOADS["head7b"]
+    T = wl.max_tokens
+    hidden, W, _ = wlm.head(T, wl.d, wl.V, 0, device="cuda")
+    ht = hidden.t().contiguous()
+    out = torch.empty((wl.V, T), dtype=torch.bfloat16, device="cuda")
+    for _ in range(warmup):
+        torch.mm(W, ht, out=out)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        torch.mm(W, ht, out=out)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    flop = 2.0 * T * wl.d * wl.V
+    print(json.dumps({"probe": "torch.mm bf16 [V, d] x [d, T]", "T": T, "d": wl.d, "V": wl.V,
+                      "ms": round(ms, 3), "TFLOP/s": round(flop / (ms / 1e3) / 1e12, 1),
+                      "frac_peak": round(flop / (ms / 1e3) / PEAK_BF16, 4)}), flush=True)
 
 
 def sources_sha256():
@@ -461,6 +494,9 @@ def main():
     args = parse()
     if args.copy_probe_mib:
         copy_probe(args.copy_probe_mib)
+        return
+    if args.blas_probe:
+        blas_probe()
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
