@@ -99,13 +99,13 @@ def test_fused_small_shapes(T, d, V, w_sd):
     _check(out, h64, W64, y, seq, lens, want_logp, want_lse, old, adv, n_seq)
 
 
-def test_fused_real_vocab_chunked_and_accumulating():
+@pytest.mark.parametrize("name,T", [("head05b", 700), ("head15b", 300)])
+def test_fused_real_vocab_chunked_and_accumulating(name, T):
     """Real vocabulary (151936: a V tail), then 256-token chunks with dW
     accumulation and no entropy output."""
     rbp = require_gpu()
-    wl = wlm.WORKLOADS["head05b"]
-    T = 700
-    print(f"[fused] head05b T={T}", flush=True)
+    wl = wlm.WORKLOADS[name]
+    print(f"[fused] {name} T={T}", flush=True)
     (hidden, W, tokens, seq, lens, h64, W64, y, want_logp, want_lse, old,
      adv) = _case(T, wl.d, wl.V, 0.02, 21, device="cuda")
     n_seq = len(lens)
@@ -153,7 +153,8 @@ def test_fused_head7b_full_size_sampled_rows():
     assert np.abs(to_np(out["lse"])[check_rows] - want_lse).max() < ATOL
     want_H = entropy(h64, W64)
     assert np.abs(to_np(out["entropy"])[check_rows] - want_H).max() < ATOL
-    assert np.all(to_np(out["logp"])[mask_rows] == 0)
+    for key in ("logp", "lse", "entropy"):
+        assert np.all(to_np(out[key])[mask_rows] == 0), key
     k = len(rows)
     _, dl_rows, _ = grpo_loss(want_logp[:k], old[rows], seq[rows], adv, lens, n_seq)
     dl = to_np(out["dlogp"])
