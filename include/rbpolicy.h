@@ -399,8 +399,8 @@ typedef struct rb_ring {
  * the given order) goes to physical row (head + n_live + i) % capacity; then
  * n_live = min(capacity, n_live + n_new) and head moves past the evicted rows.
  * group_off device int32 [n_groups + 1] splits the n_new records into groups
- * (group_off[0] = 0, group_off[n_groups] = n_new); length, reward device
- * [n_new]; src_off device int64 [n_new]: record i's tokens / behaviour
+ * (group_off[0] = 0, group_off[n_groups] = n_new); length (each >= 1),
+ * reward device [n_new]; src_off device int64 [n_new]: record i's tokens / behaviour
  * log-probs are tokens / old_logp[src_off[i] .. + length[i]).  A record longer
  * than slot_tokens keeps its first slot_tokens tokens (its stored length is
  * cut to that).  version is stored for every new record.  The device-side
