@@ -246,3 +246,66 @@ def test_fused_concurrent_calls_on_two_streams():
         for k in range(3):
             for key in ("logp", "lse", "entropy", "dlogp", "dh", "dW"):
                 assert torch.equal(results[i][k][key], alone[i][key]), (i, k, key)
+
+
+def test_fused_three_chunks_with_sequences_across_chunk_boundaries():
+    """T = 49152 at the 7B head with a workspace for 16384 tokens: three
+    chunks, dW accumulated across them.  Four short sequences carry the only
+    nonzero advantages, two of them straddling a chunk boundary, so dlogp,
+    dhidden and dW involve their rows alone."""
+    rbp = require_gpu()
+    wl = wlm.WORKLOADS["head7b"]
+    T, Tc = 3 * 16384, 16384
+    print("[fused] head7b three chunks", flush=True)
+    hidden, W, tokens = wlm.head(T, wl.d, wl.V, seed=5, device="cuda")
+    L = 64
+    lens = np.full(T // L, L, dtype=np.int32)
+    seq = np.repeat(np.arange(len(lens)), lens).astype(np.int32)
+    # sequences re-cut so that two of them cross the chunk boundaries
+    starts = [100, Tc - 5, 2 * Tc - 9, T - 12]
+    sizes = [9, 11, 17, 12]
+    seq[:] = -1
+    for i, (a, n) in enumerate(zip(starts, sizes)):
+        seq[a:a + n] = i
+    n_seq = 64
+    lens = np.zeros(n_seq, dtype=np.int32)
+    lens[:4] = sizes
+    lens[4:] = 1  # sequences with no tokens in this batch
+    adv = np.zeros(n_seq, dtype=np.float32)
+    adv[:4] = [0.8, -1.1, 0.5, -0.3]
+    rows = np.concatenate([np.arange(a, a + n) for a, n in zip(starts, sizes)])
+    h64 = hidden[torch.from_numpy(rows).cuda()].cpu().to(torch.float64).numpy()
+    W64 = bf16_to_f64(W)
+    y = to_np(tokens)[rows]
+    want_logp, want_lse = logprob_rows(h64, W64, y, range(len(rows)))
+    rng = np.random.default_rng(2)
+    old = np.zeros(T, dtype=np.float32)
+    old[rows] = (want_logp + rng.normal(0, 0.1, len(rows))).astype(np.float32)
+    dW0 = wlm.normal((wl.V, wl.d), 1e-4, 9, device="cuda")
+    out = _run(rbp, hidden, W, tokens, torch.from_numpy(seq).cuda(), torch.from_numpy(old).cuda(),
+               torch.from_numpy(adv).cuda(), torch.from_numpy(lens).cuda(), n_seq, ws_tokens=Tc,
+               dW0=dW0)
+    assert np.abs(to_np(out["logp"])[rows] - want_logp).max() < ATOL
+    assert np.abs(to_np(out["lse"])[rows] - want_lse).max() < ATOL
+    assert np.abs(to_np(out["entropy"])[rows] - entropy(h64, W64)).max() < ATOL
+    _, dl_rows, _ = grpo_loss(want_logp, old[rows], seq[rows], adv, lens, n_seq)
+    dl = to_np(out["dlogp"])
+    assert rel_l2(dl[rows], dl_rows) < RTOL
+    others = np.ones(T, dtype=bool)
+    others[rows] = False
+    assert np.all(dl[others] == 0) and np.all(to_np(out["dh"])[others] == 0)
+    dz = dz_rows(h64, W64, y, want_lse, dl_rows, range(len(rows)))
+    want_dh = dhidden_rows(h64, W64, y, want_lse, dl_rows, range(len(rows)), dz=dz)
+    assert rel_l2(to_np(out["dh"])[rows], want_dh) < RTOL
+    num = den = 0.0
+    for v0 in range(0, wl.V, 16384):
+        v1 = min(v0 + 16384, wl.V)
+        want = dW_from_rows(h64, W64, y, want_lse, dl_rows, range(len(rows)), v0, v1, dz=dz)
+        # the accumulated gradient alone (the initial dW would dominate a norm)
+        got = (out["dW"][v0:v1].cpu().numpy().astype(np.float64)
+               - dW0[v0:v1].cpu().numpy().astype(np.float64))
+        num += ((got - want) ** 2).sum()
+        den += (want ** 2).sum()
+    assert np.sqrt(num / den) < RTOL
+    del hidden, W, out, dW0
+    torch.cuda.empty_cache()
