@@ -37,11 +37,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # 1.0).  Only valid for the sources the counters were read on.
 TRAFFIC_SOURCES = ("logprob_fwd.hip", "logits_epilogue.h", "gemm_core.h", "gemm_dma.h")
 TRAFFIC = {
-    "sources_sha256": "68f56381a8d242e03d64188a366a6dd74babf5ebe4fb7abdd64aa5e495fd5bd2",
-    "fetch_bytes": {"logits_lse_partial_kernel": 26987301547,   # 13177393 KiB x 2.0
-                    "lse_merge_kernel": 373289643},             # 182270 KiB x 2.0
-    "write_bytes": {"logits_lse_partial_kernel": 117858304,     # 115096 KiB
-                    "lse_merge_kernel": 265216},                # 259.0 KiB
+    "sources_sha256": "74be3da0398d2c050fc75bbdc4a6edc2e8c77e272754abee17e5e653457de83f",
+    "fetch_bytes": {"logits_lse_partial_kernel": 28308226048,   # 13822376 KiB x 2.0
+                    "lse_merge_kernel": 391094955},             # 190964 KiB x 2.0
+    "write_bytes": {"logits_lse_partial_kernel": 155713536,     # 152064 KiB
+                    "lse_merge_kernel": 328363},                # 320.7 KiB
 }
 
 

@@ -70,9 +70,9 @@ def test_status_strings_and_workspace_sizes():
         152064 * 16384 * 2 + 16384 * 3584 * 4
     assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_BWD, 1, 64, 1000) == \
         1024 * 256 * 2 + 256 * 64 * 4
-    # forward workspace: one (max, sum) pair per token and 256-wide vocab tile
-    assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_FWD, 100, 64, 513) == \
-        ((100 * 3 * 8 + 255) // 256) * 256
+    # forward workspace: one (max, sum) pair per 128-row half of each vocab
+    # tile and token (tokens rounded up to 256)
+    assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_FWD, 100, 64, 513) == 256 * 6 * 8
     assert lib.rbp_workspace_bytes(b.RBP_OP_LOSS, 10, 0, 0) > 0
     # fused workspace: exp(z - max) bf16 [Vp, Tc], (max, sum, sum z) fp32
     # [Vp / 128, Tc] each, the dhidden K half and the loss pass's sums
