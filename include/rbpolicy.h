@@ -38,7 +38,8 @@
  *     there).  Size the workspace with
  *     rbp_workspace_bytes().  Workspace contents are scratch between calls.
  *   - All device work is enqueued on `stream` (a hipStream_t; NULL = the null
- *     stream) and is asynchronous to the host.
+ *     stream; policy_fused_fwd_bwd also uses its side stream, ordered against
+ *     `stream` by events) and is asynchronous to the host.
  *   - Return value: RBP_OK (0) or a negative RBP_E* code.  Arguments are checked
  *     on the host before anything is enqueued; on an error nothing is enqueued,
  *     except RBP_EHIP, which reports a failed launch (outputs then undefined).
@@ -46,7 +47,9 @@
  *   - Results are bitwise reproducible for identical inputs (no floating-point
  *     atomics; every reduction runs in a fixed order).
  *   - No exception crosses this interface.  The library holds no mutable global
- *     state except the thread-local error text.
+ *     state except the thread-local error text and, per device, the side
+ *     stream and events of policy_fused_fwd_bwd (created on first use, guarded
+ *     by a lock, kept until the process ends).
  */
 #ifndef RBPOLICY_H
 #define RBPOLICY_H
@@ -138,7 +141,8 @@ typedef struct rb_records {
  * use_count is > 0) and take the n_draw smallest (key, slot) pairs.
  */
 typedef struct rb_sample_cfg {
-  int32_t mode;          /* RB_UNIFORM / RB_POS_MIX / RB_POS_RETAIN                */
+  int32_t mode;          /* RB_UNIFORM, RB_POS_MIX, RB_POS_RETAIN, RB_NO_REPLACE,
+                            RB_UNUSED_FIRST                                        */
   int32_t layout;        /* RB_LAYOUT_PACKED / RB_LAYOUT_PADDED                    */
   uint64_t seed;
   uint64_t step;
