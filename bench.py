@@ -225,7 +225,11 @@ def aux_stress(iters=20):
       sample+gather: 256 positive-mixture draws (p_pos = 0.5), padded to 8192;
       loss: policy_loss_fwd_bwd over the same draws packed (~4.7e5 tokens).
       sample_no_replace: the same draws without replacement (per-slot keys and
-      a radix select), padded; note_use: the usage update of 256 draws.
+      a radix select), padded; note_use: the usage update of 256 draws;
+      loss_seq_ratio, loss_asymre: the objective variants over the loss's
+      tokens (12 B per token: logp, old_logp or seq id read, dlogp written);
+      push: FIFO insertion of 1024 rollouts (16 B per token: tokens and
+      behaviour log-probs read and written, 40 B per record).
     Algorithmic bytes: gather = 4 B/record reward scan + 4 B per positive slot
     + 20 B record metadata per draw + 8 B read per gathered token + 12 B
     written per padded position (without replacement: 8 B per record key in
@@ -343,7 +347,46 @@ def aux_stress(iters=20):
     torch.cuda.synchronize()
     l_ms = a.elapsed_time(b) / iters
     l_bytes = 16 * T + 8 * wl.n_draw
-    del tok, old, keep, rec
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        torch.cuda._sleep(20_000_000)
+        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ea.record()
+        for _ in range(iters):
+            fn()
+        eb.record()
+        torch.cuda.synchronize()
+        return ea.elapsed_time(eb) / iters
+
+    # the objective variants over the same tokens: whole-sequence ratio (the
+    # draws as complete sequences) and AsymRE (stored coefficients)
+    ws_s = rbp.workspace(rbp.RBP_OP_LOSS_SEQ, wl.n_draw)
+    s_ms = timed(lambda: rbp.policy_loss_seq_fwd_bwd(logp, old_t, pk["cu_seqlens"], pk["adv"],
+                                                     wl.n_draw, loss, dlogp, stats, ws_s))
+    s_bytes = 12 * T + 8 * wl.n_draw
+    st2 = torch.zeros(2, device=dev)
+    a_ms = timed(lambda: rbp.policy_asymre_fwd_bwd(logp, seq, pk["adv"], wl.n_draw, loss, dlogp,
+                                                   st2, ws_l))
+    a_bytes = 12 * T + 4 * wl.n_draw
+
+    # FIFO insertion of 128 groups of 8 rollouts (the stress length mix) into
+    # a 65536-row ring with 8192 arena tokens per row
+    ring = rbp.make_ring(65536, 8192, device=dev)
+    n_new = 1024
+    lens = pk["len"].repeat(n_new // wl.n_draw + 1)[:n_new].contiguous()
+    src = torch.zeros(n_new, dtype=torch.int64, device=dev)
+    src[1:] = torch.cumsum(lens[:-1].long(), 0)
+    tot = int(lens.sum().item())
+    new_tok = torch.randint(0, wl.V, (tot,), dtype=torch.int32, device=dev)
+    new_old = torch.randn(tot, device=dev)
+    goff = torch.arange(0, n_new + 1, 8, dtype=torch.int32, device=dev)
+    rew = (torch.rand(n_new, device=dev) < 0.4).float()
+    p_ms = timed(lambda: rbp.rb_push(ring, goff, lens, src, rew, 1, new_tok, new_old))
+    p_bytes = 16 * tot + 40 * n_new
+    del tok, old, keep, rec, ring
     torch.cuda.empty_cache()
     return {
         "workload": "stress: 10^6 records, 256 positive-mixture draws (p_pos 0.5), "
@@ -358,6 +401,12 @@ def aux_stress(iters=20):
                               "GB/s": round(nr_bytes / (nr_ms / 1e3) / 1e9, 1),
                               "frac_hbm": round(nr_bytes / (nr_ms / 1e3) / PEAK_HBM, 4)},
         "note_use": {"draws": wl.n_draw, "ms": round(u_ms, 4)},
+        "loss_seq_ratio": {"tokens": T, "ms": round(s_ms, 4), "bytes": s_bytes,
+                           "GB/s": round(s_bytes / (s_ms / 1e3) / 1e9, 1)},
+        "loss_asymre": {"tokens": T, "ms": round(a_ms, 4), "bytes": a_bytes,
+                        "GB/s": round(a_bytes / (a_ms / 1e3) / 1e9, 1)},
+        "push": {"records": n_new, "tokens": tot, "ms": round(p_ms, 4), "bytes": p_bytes,
+                 "GB/s": round(p_bytes / (p_ms / 1e3) / 1e9, 1)},
         "loss": {"tokens": T, "ms": round(l_ms, 4), "bytes": l_bytes,
                  "GB/s": round(l_bytes / (l_ms / 1e3) / 1e9, 1),
                  "frac_hbm": round(l_bytes / (l_ms / 1e3) / PEAK_HBM, 4)},

@@ -9,14 +9,19 @@
 // Device pipeline (one stream):
 //   [mix/retain only] pos_count -> pos_scan -> pos_compact : ascending list of
 //       positive slots (slot = FIFO position, 0 = oldest) in the workspace;
-//   [without replacement] slot_key -> 8 x (select_hist -> select_digit) ->
-//       sel_count -> sel_scan -> sel_compact : an MSD radix select finds the
-//       n_draw-th smallest 64-bit slot key K exactly, then the slots with a key
-//       below K (and the first ties in slot order) are listed ascending;
+//   [without replacement] slot_key -> select_top -> select_cand ->
+//       select_rest -> sel_count -> sel_scan -> sel_compact : an MSD radix
+//       select (8-bit digits) finds the n_draw-th smallest 64-bit slot key K
+//       exactly -- the top digit from per-block histograms of every key, the
+//       seven lower ones by one block over the keys that share the top digit
+//       -- then the slots with a key below K (and the first ties in slot
+//       order) are listed ascending;
 //   draw     : one thread per draw; Philox4x64-10 block -> slot; per-draw
-//              outputs; block scan of lengths -> cu_seqlens, n_tokens;
-//   gather   : one thread per output position; coalesced copies from the
-//              token arena.
+//              outputs; scan of lengths -> cu_seqlens, n_tokens (one block
+//              up to 1024 draws, else draw_rows -> draw_scan -> draw_cu);
+//   gather   : one block column per draw (packed: the part of its sequence
+//              inside the window; padded: its l_max row); coalesced copies
+//              from the token arena.
 // Everything is integer work or a bit-exact copy of stored floats.
 
 #include "rbp_internal.h"
@@ -25,7 +30,9 @@ namespace {
 
 constexpr int kSlotsPerBlock = 1024;  // compaction granule
 constexpr int kCountThreads = 256;    // 4 slots per thread
-constexpr int kDrawThreads = 1024;
+constexpr int kDrawThreads = 1024;  // single-block draw pass, up to this many draws
+constexpr int kRowThreads = 256;    // draws per block beyond that
+constexpr int kMaxRowBlocks = (1 << 20) / kRowThreads;
 
 // ---- Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11) ----------------------
 struct Block4 {
@@ -134,70 +141,229 @@ __global__ void __launch_bounds__(kCountThreads) pos_compact_kernel(
 
 // ---- selection without replacement -----------------------------------------
 
-// Key of slot s: the top 63 bits of word 0 of the Philox block with counter
-// (s, step, 1, 0); for never-used-first, bit 63 set when the slot was used.
-__global__ void __launch_bounds__(256) slot_key_kernel(uint64_t seed, uint64_t step,
-                                                       int64_t n_live, int64_t head, int64_t cap,
-                                                       const int32_t* __restrict__ use_count,
-                                                       uint64_t* __restrict__ keys) {
-  for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < n_live;
-       s += (int64_t)gridDim.x * 256) {
-    uint64_t k = philox4x64_10((uint64_t)s, step, 1, 0, seed, 0).x0 >> 1;
-    if (use_count != nullptr && use_count[phys_row(s, head, cap)] > 0) k |= 1ull << 63;
-    keys[s] = k;
-  }
-}
+constexpr int kKeyBlocks = 256;   // key kernel blocks (at most): key segments; a power of 2
+constexpr int kKeyThreads = 1024;
+constexpr int kTopThreads = 1024;
+constexpr int kRestThreads = 1024;
+constexpr int kRestRegKeys = 16;  // candidates per thread held in registers
 
-// Radix-select state: the key digits fixed so far, how many keys still to be
-// taken among those sharing them, and the histogram of the next digit.
+// Radix-select state: the key digits fixed so far and how many keys still to
+// be taken among those sharing them.
 struct SelState {
   uint64_t prefix;
   int64_t need;
-  uint32_t hist[256];
 };
 
-__global__ void __launch_bounds__(256) select_init_kernel(SelState* st, int64_t n_draw) {
-  st->hist[threadIdx.x] = 0u;
-  if (threadIdx.x == 0) {
-    st->prefix = 0;
-    st->need = n_draw;
-  }
+// Key segment b of n keys split over n_seg blocks: [b * per, min(n, (b+1) * per)).
+__device__ __forceinline__ int64_t seg_len(int64_t n, int64_t n_seg) {
+  return (n + n_seg - 1) / n_seg;
 }
 
-// Histogram of digit `pass` (bits 56 - 8 pass .. +8, most significant first)
-// over the keys whose higher digits equal the prefix.  Integer atomics: the
-// counts do not depend on the order of the additions.
-__global__ void __launch_bounds__(256) select_hist_kernel(const uint64_t* __restrict__ keys,
-                                                          int64_t n, int pass,
-                                                          SelState* __restrict__ st) {
+// Key of slot s: the top 63 bits of word 0 of the Philox block with counter
+// (s, step, 1, 0); for never-used-first, bit 63 set when the slot was used.
+// Block b keys segment b and writes the histogram of the top digit (bits
+// 56..63) of its keys to row b of `top_hist`: no global atomics, so the 256
+// bins are not contended by every block.
+__global__ void __launch_bounds__(kKeyThreads) slot_key_kernel(
+    uint64_t seed, uint64_t step, int64_t n_live, int64_t head, int64_t cap,
+    const int32_t* __restrict__ use_count, uint64_t* __restrict__ keys,
+    uint32_t* __restrict__ top_hist) {
   __shared__ uint32_t h[256];
-  h[threadIdx.x] = 0u;
+  if (threadIdx.x < 256) h[threadIdx.x] = 0u;
   __syncthreads();
-  const int shift = 56 - 8 * pass;
-  const uint64_t hi = pass == 0 ? 0 : st->prefix >> (shift + 8);
-  for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < n;
-       s += (int64_t)gridDim.x * 256) {
-    const uint64_t k = keys[s];
-    if (pass == 0 || (k >> (shift + 8)) == hi) atomicAdd(&h[(k >> shift) & 255u], 1u);
+  const int64_t per = seg_len(n_live, gridDim.x);
+  const int64_t lo = (int64_t)blockIdx.x * per;
+  const int64_t hi = lo + per < n_live ? lo + per : n_live;
+  for (int64_t s = lo + threadIdx.x; s < hi; s += kKeyThreads) {
+    uint64_t k = philox4x64_10((uint64_t)s, step, 1, 0, seed, 0).x0 >> 1;
+    if (use_count != nullptr && use_count[phys_row(s, head, cap)] > 0) k |= 1ull << 63;
+    keys[s] = k;
+    atomicAdd(&h[k >> 56], 1u);
   }
   __syncthreads();
-  if (h[threadIdx.x] != 0u) atomicAdd(&st->hist[threadIdx.x], h[threadIdx.x]);
+  if (threadIdx.x < 256) top_hist[blockIdx.x * 256 + threadIdx.x] = h[threadIdx.x];
 }
 
-// The digit holding the need-th smallest remaining key; clears the histogram.
-__global__ void __launch_bounds__(256) select_digit_kernel(int pass, SelState* __restrict__ st) {
-  if (threadIdx.x == 0) {
-    int64_t cum = 0;
-    int d = 0;
-    for (; d < 255; ++d) {
-      if (cum + (int64_t)st->hist[d] >= st->need) break;
-      cum += st->hist[d];
-    }
-    st->need -= cum;
-    st->prefix |= (uint64_t)d << (56 - 8 * pass);
+// Bin t of the block holding the need-th smallest remaining key: the one
+// thread whose exclusive prefix is below `need` and inclusive prefix reaches
+// it (empty bins never qualify).
+__device__ __forceinline__ bool holds_need(int64_t excl, int64_t count, int64_t need) {
+  return excl < need && need <= excl + count;
+}
+
+// One block: sums the per-segment top-digit histograms (four threads per
+// bin) and picks the top digit.
+__global__ void __launch_bounds__(kTopThreads) select_top_kernel(
+    const uint32_t* __restrict__ top_hist, int32_t n_seg, int64_t n_draw,
+    SelState* __restrict__ st) {
+  __shared__ uint32_t part[kTopThreads / 256][256];
+  __shared__ int64_t lds[kTopThreads / 64];
+  const int bin = threadIdx.x & 255, q = threadIdx.x >> 8;
+  uint32_t c = 0u;
+#pragma unroll 8
+  for (int32_t b = q; b < n_seg; b += kTopThreads / 256) c += top_hist[b * 256 + bin];
+  part[q][bin] = c;
+  __syncthreads();
+  int64_t v = 0;
+  if (threadIdx.x < 256)
+    for (int i = 0; i < kTopThreads / 256; ++i) v += part[i][bin];
+  int64_t total;
+  const int64_t excl = block_exclusive_scan<kTopThreads>(v, &total, lds);
+  if (threadIdx.x < 256 && holds_need(excl, v, n_draw)) {
+    st->prefix = (uint64_t)bin << 56;
+    st->need = n_draw - excl;
+  }
+}
+
+// Block b lists the keys of segment b whose top digit is the selected one at
+// the start of the segment's stretch of `cand` (order free: only their digit
+// histograms are taken), and their number in cand_cnt[b].  One LDS atomic per
+// wave, no global ones.
+__global__ void __launch_bounds__(kKeyThreads) select_cand_kernel(
+    const uint64_t* __restrict__ keys, int64_t n, const SelState* __restrict__ st,
+    uint64_t* __restrict__ cand, uint32_t* __restrict__ cand_cnt) {
+  __shared__ uint32_t cnt;
+  if (threadIdx.x == 0) cnt = 0u;
+  __syncthreads();
+  const uint64_t top = st->prefix >> 56;
+  const int lane = threadIdx.x & 63;
+  const int64_t per = seg_len(n, gridDim.x);
+  const int64_t lo = (int64_t)blockIdx.x * per;
+  const int64_t hi = lo + per < n ? lo + per : n;
+  for (int64_t base = lo; base < hi; base += kKeyThreads) {
+    const int64_t s = base + threadIdx.x;
+    const uint64_t k = s < hi ? keys[s] : 0ull;
+    const bool take = s < hi && (k >> 56) == top;
+    const uint64_t m = __ballot(take);
+    if (m == 0ull) continue;
+    uint32_t at = 0u;
+    if (lane == 0) at = atomicAdd(&cnt, (uint32_t)__popcll(m));
+    at = __shfl(at, 0, 64);
+    if (take) cand[lo + at + __popcll(m & ((1ull << lane) - 1ull))] = k;
   }
   __syncthreads();
-  st->hist[threadIdx.x] = 0u;
+  if (threadIdx.x == 0) cand_cnt[blockIdx.x] = cnt;
+}
+
+// One block: the lower digits, most significant first, over the candidates
+// only (the first kRestThreads * kRestRegKeys of them held in registers, any
+// further ones re-read each pass), until at most kRestThreads keys share the
+// prefix; those are then ranked directly, each thread counting the survivors
+// below and up to its own.  Integer counts only: the result does not depend
+// on the order of any addition.  Leaves the exact need-th smallest key in
+// `prefix` and the number of its ties still to be taken in `need`.
+__global__ void __launch_bounds__(kRestThreads) select_rest_kernel(
+    const uint64_t* __restrict__ cand, const uint32_t* __restrict__ cand_cnt, int32_t n_seg,
+    int64_t n, SelState* __restrict__ st) {
+  __shared__ uint32_t h[256];
+  __shared__ int64_t lds[kRestThreads / 64];
+  __shared__ int64_t seg_start[kKeyBlocks + 1];
+  __shared__ uint64_t surv[kRestThreads];
+  __shared__ uint64_t s_prefix;
+  __shared__ int64_t s_need, s_match;
+  __shared__ uint32_t s_surv;
+  const int64_t c = threadIdx.x < n_seg ? (int64_t)cand_cnt[threadIdx.x] : 0;
+  int64_t nc;
+  const int64_t excl = block_exclusive_scan<kRestThreads>(c, &nc, lds);
+  if (threadIdx.x < n_seg) seg_start[threadIdx.x] = excl;
+  if (threadIdx.x == 0) {
+    seg_start[n_seg] = nc;
+    s_surv = 0u;
+  }
+  __syncthreads();
+  const int64_t per = seg_len(n, n_seg);
+  // candidate i (< nc) sits at entry i - seg_start[b] of segment b, the last
+  // segment starting at or before i
+  // (a fixed eight halvings over n_seg <= kKeyBlocks = 256 starts, so the
+  // searches of a thread's candidates interleave)
+  auto cand_pos = [&](int64_t i) {
+    int lo = 0;
+#pragma unroll
+    for (int step = kKeyBlocks / 2; step > 0; step >>= 1) {
+      const int m = lo + step;
+      if (m < n_seg && seg_start[m] <= i) lo = m;
+    }
+    return lo * per + (i - seg_start[lo]);
+  };
+  // positions first, then all the loads together (nc >= 1: the selected
+  // bucket holds the need-th key; indices past it re-read the last one)
+  int64_t at[kRestRegKeys];
+#pragma unroll
+  for (int u = 0; u < kRestRegKeys; ++u) {
+    const int64_t i = threadIdx.x + (int64_t)u * kRestThreads;
+    at[u] = cand_pos(i < nc ? i : nc - 1);
+  }
+  uint64_t reg[kRestRegKeys];
+#pragma unroll
+  for (int u = 0; u < kRestRegKeys; ++u) reg[u] = cand[at[u]];
+  // calls f(k) for every candidate k
+  auto each_cand = [&](auto&& f) {
+#pragma unroll
+    for (int u = 0; u < kRestRegKeys; ++u)
+      if (threadIdx.x + (int64_t)u * kRestThreads < nc) f(reg[u]);
+    for (int64_t i = threadIdx.x + (int64_t)kRestRegKeys * kRestThreads; i < nc;
+         i += kRestThreads)
+      f(cand[cand_pos(i)]);
+  };
+  uint64_t prefix = st->prefix;
+  int64_t need = st->need;
+  int64_t n_match = nc;  // keys sharing the digits fixed so far
+  int shift = 56;        // the prefix fixes the bits from `shift` up
+  while (shift > 0 && n_match > kRestThreads) {
+    shift -= 8;
+    if (threadIdx.x < 256) h[threadIdx.x] = 0u;
+    __syncthreads();
+    const uint64_t hi = prefix >> (shift + 8);
+    each_cand([&](uint64_t k) {
+      if ((k >> (shift + 8)) == hi) atomicAdd(&h[(k >> shift) & 255u], 1u);
+    });
+    __syncthreads();
+    const int64_t v = threadIdx.x < 256 ? (int64_t)h[threadIdx.x] : 0;
+    int64_t total;
+    const int64_t ex = block_exclusive_scan<kRestThreads>(v, &total, lds);
+    if (threadIdx.x < 256 && holds_need(ex, v, need)) {
+      s_prefix = prefix | ((uint64_t)threadIdx.x << shift);
+      s_need = need - ex;
+      s_match = v;
+    }
+    __syncthreads();
+    prefix = s_prefix;
+    need = s_need;
+    n_match = s_match;
+  }
+  if (shift > 0) {
+    // at most kRestThreads survivors: list them (order free), then the one
+    // with `need - 1` survivors strictly below it and at least `need` up to
+    // it is the key; equal keys all write the same values
+    const uint64_t hi = prefix >> shift;
+    each_cand([&](uint64_t k) {
+      if ((k >> shift) == hi) {
+        const uint32_t i = atomicAdd(&s_surv, 1u);  // < n_match <= kRestThreads
+        if (i < kRestThreads) surv[i] = k;
+      }
+    });
+    __syncthreads();
+    if (threadIdx.x < n_match) {
+      const uint64_t mine = surv[threadIdx.x];
+      int64_t less = 0, leq = 0;
+      for (int64_t i = 0; i < n_match; ++i) {
+        const uint64_t o = surv[i];
+        less += o < mine;
+        leq += o <= mine;
+      }
+      if (less < need && need <= leq) {
+        s_prefix = mine;
+        s_need = need - less;
+      }
+    }
+    __syncthreads();
+    prefix = s_prefix;
+    need = s_need;
+  }
+  if (threadIdx.x == 0) {
+    st->prefix = prefix;
+    st->need = need;
+  }
 }
 
 // Per slot, (key < K) in the low 32 bits and (key == K) in the high 32 bits:
@@ -273,6 +439,75 @@ struct DrawParams {
   int64_t max_tokens, token_begin, l_max;
 };
 
+// Per-call constants of the draws: the positives listed by the count/scan
+// pass, the retained positives and the size of the retained set.
+struct DrawSet {
+  int64_t n_pos, keep, n_set;
+};
+
+__device__ __forceinline__ DrawSet draw_set(const DrawParams& p,
+                                            const int64_t* __restrict__ meta) {
+  DrawSet d;
+  d.n_pos = (p.mode == RB_POS_MIX || p.mode == RB_POS_RETAIN) ? meta[0] : 0;
+  // retained set: the newest `keep` positives older than the fresh part, then
+  // the fresh part [first_fresh, n_live)
+  d.keep = d.n_pos < p.n_pos_keep ? d.n_pos : p.n_pos_keep;
+  d.n_set = d.keep + (p.n_live - p.first_fresh);
+  return d;
+}
+
+// Slot of draw j: the Philox4x64-10 block with counter (j, step, 0, 0) picks
+// it (or the j-th selected slot without replacement).
+__device__ __forceinline__ int64_t draw_slot(const DrawParams& p, const DrawSet& d,
+                                             const int32_t* __restrict__ pos_list, int64_t j) {
+  if (p.mode == RB_NO_REPLACE || p.mode == RB_UNUSED_FIRST) return pos_list[j];
+  const Block4 b = philox4x64_10((uint64_t)j, p.step, 0, 0, p.seed, 0);
+  if (p.mode == RB_UNIFORM) return (int64_t)__umul64hi(b.x0, (uint64_t)p.n_live);
+  if (p.mode == RB_POS_MIX) {
+    if (d.n_pos > 0 && (b.x1 >> 32) < p.p_q32) return pos_list[__umul64hi(b.x0, (uint64_t)d.n_pos)];
+    return (int64_t)__umul64hi(b.x0, (uint64_t)p.n_live);
+  }
+  if (d.n_set <= 0) return 0;
+  const int64_t i = (int64_t)__umul64hi(b.x0, (uint64_t)d.n_set);
+  return i < d.keep ? pos_list[d.n_pos - d.keep + i] : p.first_fresh + (i - d.keep);
+}
+
+// Per-draw outputs of draw j; returns its contribution to the stream (full
+// length packed, min(length, l_max) padded).
+__device__ __forceinline__ int64_t draw_one(const DrawParams& p, const DrawSet& d,
+                                            const int32_t* __restrict__ pos_list,
+                                            const int32_t* __restrict__ length,
+                                            const float* __restrict__ advantage,
+                                            const int32_t* __restrict__ version, int64_t j,
+                                            int32_t* __restrict__ out_idx,
+                                            float* __restrict__ out_adv,
+                                            int32_t* __restrict__ out_len,
+                                            int32_t* __restrict__ out_age) {
+  const int64_t slot = draw_slot(p, d, pos_list, j);
+  const int64_t r = phys_row(slot, p.head, p.cap);
+  const int64_t len = length[r];
+  out_idx[j] = (int32_t)slot;
+  out_adv[j] = advantage[r];
+  out_len[j] = (int32_t)len;
+  out_age[j] = p.cur_version - version[r];
+  return p.layout == RB_LAYOUT_PACKED ? len : (len < p.l_max ? len : p.l_max);
+}
+
+__device__ __forceinline__ void write_totals(const DrawParams& p, int64_t sum,
+                                             int64_t* __restrict__ n_tokens,
+                                             int64_t* __restrict__ stream_total) {
+  if (p.layout == RB_LAYOUT_PACKED) {
+    int64_t v = sum - p.token_begin;
+    v = v < 0 ? 0 : (v > p.max_tokens ? p.max_tokens : v);
+    *n_tokens = v;
+  } else {
+    *n_tokens = sum;
+  }
+  *stream_total = sum;
+}
+
+// Up to kDrawThreads draws: one block, one draw per thread, block scan of the
+// lengths -> cu_seqlens, n_tokens.
 __global__ void __launch_bounds__(kDrawThreads) draw_kernel(
     DrawParams p, const int64_t* __restrict__ meta, const int32_t* __restrict__ pos_list,
     const int32_t* __restrict__ length, const float* __restrict__ advantage,
@@ -281,94 +516,105 @@ __global__ void __launch_bounds__(kDrawThreads) draw_kernel(
     int32_t* __restrict__ cu_seqlens, int64_t* __restrict__ n_tokens,
     int64_t* __restrict__ stream_total) {
   __shared__ int64_t lds[kDrawThreads / 64];
-  const int64_t n_pos = (p.mode == RB_POS_MIX || p.mode == RB_POS_RETAIN) ? meta[0] : 0;
-  // retained set: the newest `keep` positives older than the fresh part, then
-  // the fresh part [first_fresh, n_live)
-  const int64_t keep = n_pos < p.n_pos_keep ? n_pos : p.n_pos_keep;
-  const int64_t n_set = keep + (p.n_live - p.first_fresh);
-  int64_t carry = 0, valid = 0;
-  if (threadIdx.x == 0) cu_seqlens[0] = 0;
-  for (int64_t base = 0; base < p.n_draw; base += kDrawThreads) {
-    const int64_t j = base + threadIdx.x;
-    int64_t len = 0;
-    if (j < p.n_draw) {
-      const Block4 b = philox4x64_10((uint64_t)j, p.step, 0, 0, p.seed, 0);
-      int64_t slot;
-      if (p.mode == RB_UNIFORM) {
-        slot = (int64_t)__umul64hi(b.x0, (uint64_t)p.n_live);
-      } else if (p.mode == RB_POS_MIX) {
-        if (n_pos > 0 && (b.x1 >> 32) < p.p_q32)
-          slot = pos_list[__umul64hi(b.x0, (uint64_t)n_pos)];
-        else
-          slot = (int64_t)__umul64hi(b.x0, (uint64_t)p.n_live);
-      } else if (p.mode == RB_NO_REPLACE || p.mode == RB_UNUSED_FIRST) {
-        slot = pos_list[j];  // the selected slots, ascending
-      } else {
-        if (n_set <= 0) {
-          slot = 0;
-        } else {
-          const int64_t i = (int64_t)__umul64hi(b.x0, (uint64_t)n_set);
-          slot = i < keep ? pos_list[n_pos - keep + i] : p.first_fresh + (i - keep);
-        }
-      }
-      const int64_t r = phys_row(slot, p.head, p.cap);
-      len = length[r];
-      out_idx[j] = (int32_t)slot;
-      out_adv[j] = advantage[r];
-      out_len[j] = (int32_t)len;
-      out_age[j] = p.cur_version - version[r];
-    }
-    int64_t total;
-    if (p.layout == RB_LAYOUT_PACKED) {
-      const int64_t ex = block_exclusive_scan<kDrawThreads>(len, &total, lds);
-      if (j < p.n_draw) cu_seqlens[j + 1] = (int32_t)(carry + ex + len);
-      carry += total;
-    } else {
-      const int64_t v = len < p.l_max ? len : p.l_max;
-      block_exclusive_scan<kDrawThreads>(v, &total, lds);
-      if (j < p.n_draw) cu_seqlens[j + 1] = (int32_t)((j + 1) * p.l_max);
-      valid += total;
-    }
-  }
-  if (threadIdx.x == 0) {
-    if (p.layout == RB_LAYOUT_PACKED) {
-      int64_t v = carry - p.token_begin;
-      v = v < 0 ? 0 : (v > p.max_tokens ? p.max_tokens : v);
-      *n_tokens = v;
-      *stream_total = carry;
-    } else {
-      *n_tokens = valid;
-      *stream_total = valid;
-    }
-  }
+  const DrawSet d = draw_set(p, meta);
+  const int64_t j = threadIdx.x;
+  const int64_t v = j < p.n_draw ? draw_one(p, d, pos_list, length, advantage, version, j,
+                                            out_idx, out_adv, out_len, out_age)
+                                 : 0;
+  int64_t total;
+  const int64_t ex = block_exclusive_scan<kDrawThreads>(v, &total, lds);
+  if (j == 0) cu_seqlens[0] = 0;
+  if (j < p.n_draw)
+    cu_seqlens[j + 1] = (int32_t)(p.layout == RB_LAYOUT_PACKED ? ex + v : (j + 1) * p.l_max);
+  if (j == 0) write_totals(p, total, n_tokens, stream_total);
 }
 
+// More draws: blocks of kRowThreads draws write the per-draw outputs and
+// their block sums; one block scans the sums; then each block writes its
+// cu_seqlens.  Many blocks keep the scattered record reads spread over the
+// chip.
+__global__ void __launch_bounds__(kRowThreads) draw_rows_kernel(
+    DrawParams p, const int64_t* __restrict__ meta, const int32_t* __restrict__ pos_list,
+    const int32_t* __restrict__ length, const float* __restrict__ advantage,
+    const int32_t* __restrict__ version, int32_t* __restrict__ out_idx,
+    float* __restrict__ out_adv, int32_t* __restrict__ out_len, int32_t* __restrict__ out_age,
+    int64_t* __restrict__ blk_sum) {
+  __shared__ int64_t lds[kRowThreads / 64];
+  const DrawSet d = draw_set(p, meta);
+  const int64_t j = (int64_t)blockIdx.x * kRowThreads + threadIdx.x;
+  const int64_t v = j < p.n_draw ? draw_one(p, d, pos_list, length, advantage, version, j,
+                                            out_idx, out_adv, out_len, out_age)
+                                 : 0;
+  int64_t total;
+  block_exclusive_scan<kRowThreads>(v, &total, lds);
+  if (threadIdx.x == 0) blk_sum[blockIdx.x] = total;
+}
+
+__global__ void __launch_bounds__(1024) draw_scan_kernel(DrawParams p,
+                                                         const int64_t* __restrict__ blk_sum,
+                                                         int64_t* __restrict__ blk_off, int64_t nb,
+                                                         int64_t* __restrict__ n_tokens,
+                                                         int64_t* __restrict__ stream_total) {
+  __shared__ int64_t lds[1024 / 64];
+  int64_t carry = 0;
+  for (int64_t base = 0; base < nb; base += 1024) {
+    const int64_t i = base + threadIdx.x;
+    const int64_t v = i < nb ? blk_sum[i] : 0;
+    int64_t total;
+    const int64_t ex = block_exclusive_scan<1024>(v, &total, lds);
+    if (i < nb) blk_off[i] = carry + ex;
+    carry += total;
+  }
+  if (threadIdx.x == 0) write_totals(p, carry, n_tokens, stream_total);
+}
+
+__global__ void __launch_bounds__(kRowThreads) draw_cu_kernel(
+    DrawParams p, const int32_t* __restrict__ out_len, const int64_t* __restrict__ blk_off,
+    int32_t* __restrict__ cu_seqlens) {
+  __shared__ int64_t lds[kRowThreads / 64];
+  const int64_t j = (int64_t)blockIdx.x * kRowThreads + threadIdx.x;
+  const int64_t v = j < p.n_draw ? (int64_t)out_len[j] : 0;
+  int64_t total;
+  const int64_t ex = block_exclusive_scan<kRowThreads>(v, &total, lds);
+  if (j == 0) cu_seqlens[0] = 0;
+  if (j < p.n_draw)
+    cu_seqlens[j + 1] = (int32_t)(p.layout == RB_LAYOUT_PACKED ? blk_off[blockIdx.x] + ex + v
+                                                               : (j + 1) * p.l_max);
+}
+
+// Block (j, y) copies the tokens of draw j that fall in the window
+// [token_begin, token_begin + max_tokens) of the packed stream, rows y
+// splitting long sequences; every block also takes its share of the window
+// positions past the end of the stream, which are padded.
 __global__ void __launch_bounds__(256) gather_packed_kernel(
-    int64_t n_draw, int64_t head, int64_t cap, int64_t token_begin, int64_t max_tokens,
+    int64_t head, int64_t cap, int64_t token_begin, int64_t max_tokens,
     const int64_t* __restrict__ stream_total, const int32_t* __restrict__ cu_seqlens,
     const int32_t* __restrict__ idx, const int64_t* __restrict__ arena_off,
     const int32_t* __restrict__ arena_tokens, const float* __restrict__ arena_old,
     int32_t* __restrict__ tokens, float* __restrict__ old_logp, int32_t* __restrict__ seq) {
+  const int64_t win_end = token_begin + max_tokens;
   const int64_t total = *stream_total;
-  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < max_tokens;
-       t += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t pos = token_begin + t;
-    if (pos < total) {
-      // largest j with cu_seqlens[j] <= pos (lengths are >= 1)
-      int64_t lo = 0, hi = n_draw;  // invariant: cu[lo] <= pos < cu[hi]
-      while (hi - lo > 1) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (cu_seqlens[mid] <= pos) lo = mid; else hi = mid;
-      }
-      const int64_t src = arena_off[phys_row(idx[lo], head, cap)] + (pos - cu_seqlens[lo]);
-      tokens[t] = arena_tokens[src];
-      old_logp[t] = arena_old[src];
-      seq[t] = (int32_t)lo;
-    } else {
-      tokens[t] = 0;
-      old_logp[t] = 0.0f;
-      seq[t] = -1;
-    }
+  const int64_t n_blk = (int64_t)gridDim.x * gridDim.y;
+  const int64_t blk = (int64_t)blockIdx.x * gridDim.y + blockIdx.y;
+  for (int64_t pos = (total > token_begin ? total : token_begin) + blk * 256 + threadIdx.x;
+       pos < win_end; pos += n_blk * 256) {
+    const int64_t t = pos - token_begin;
+    tokens[t] = 0;
+    old_logp[t] = 0.0f;
+    seq[t] = -1;
+  }
+  const int64_t j = blockIdx.x;
+  const int64_t c0 = cu_seqlens[j], c1 = cu_seqlens[j + 1];
+  const int64_t lo = c0 > token_begin ? c0 : token_begin;
+  const int64_t hi = c1 < win_end ? c1 : win_end;
+  if (lo >= hi) return;
+  const int64_t src = arena_off[phys_row(idx[j], head, cap)] - c0;  // + stream position
+  for (int64_t pos = lo + (int64_t)blockIdx.y * 256 + threadIdx.x; pos < hi;
+       pos += (int64_t)gridDim.y * 256) {
+    const int64_t t = pos - token_begin;
+    tokens[t] = arena_tokens[src + pos];
+    old_logp[t] = arena_old[src + pos];
+    seq[t] = (int32_t)j;
   }
 }
 
@@ -437,6 +683,11 @@ size_t rbp::sample_gather_ws(int64_t capacity) {
   c.take<int64_t>(nb);
   c.take<int64_t>(nb);
   c.take<SelState>(1);
+  c.take<uint32_t>(kKeyBlocks * 256);
+  c.take<uint32_t>(kKeyBlocks);
+  c.take<uint64_t>(capacity < 1 ? 1 : capacity);
+  c.take<int64_t>(kMaxRowBlocks);
+  c.take<int64_t>(kMaxRowBlocks);
   return align_up(c.used, 256);
 }
 
@@ -496,6 +747,11 @@ extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
   int64_t* sel_counts = c.take<int64_t>(nb_cap);
   int64_t* sel_offsets = c.take<int64_t>(nb_cap);
   SelState* sel_state = c.take<SelState>(1);
+  uint32_t* top_hist = c.take<uint32_t>(kKeyBlocks * 256);
+  uint32_t* cand_cnt = c.take<uint32_t>(kKeyBlocks);
+  uint64_t* cand = c.take<uint64_t>(rec->capacity);
+  int64_t* blk_sum = c.take<int64_t>(kMaxRowBlocks);
+  int64_t* blk_off = c.take<int64_t>(kMaxRowBlocks);
 
   DrawParams p{};
   p.mode = cfg->mode;
@@ -517,17 +773,17 @@ extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
 
   if (no_replace) {
     const int64_t n = rec->n_live;
-    int64_t kb = rbp::ceil_div(n, 256);
-    if (kb > 4096) kb = 4096;
-    hipLaunchKernelGGL(slot_key_kernel, dim3(kb), dim3(256), 0, s, cfg->seed, cfg->step, n,
-                       rec->head, rec->capacity,
-                       cfg->mode == RB_UNUSED_FIRST ? rec->use_count : nullptr, keys);
-    hipLaunchKernelGGL(select_init_kernel, dim3(1), dim3(256), 0, s, sel_state, cfg->n_draw);
-    for (int pass = 0; pass < 8; ++pass) {
-      hipLaunchKernelGGL(select_hist_kernel, dim3(kb), dim3(256), 0, s, keys, n, pass,
-                         sel_state);
-      hipLaunchKernelGGL(select_digit_kernel, dim3(1), dim3(256), 0, s, pass, sel_state);
-    }
+    int64_t kb = rbp::ceil_div(n, 2048);
+    if (kb > kKeyBlocks) kb = kKeyBlocks;
+    hipLaunchKernelGGL(slot_key_kernel, dim3(kb), dim3(kKeyThreads), 0, s, cfg->seed, cfg->step,
+                       n, rec->head, rec->capacity,
+                       cfg->mode == RB_UNUSED_FIRST ? rec->use_count : nullptr, keys, top_hist);
+    hipLaunchKernelGGL(select_top_kernel, dim3(1), dim3(kTopThreads), 0, s, top_hist,
+                       (int32_t)kb, cfg->n_draw, sel_state);
+    hipLaunchKernelGGL(select_cand_kernel, dim3(kb), dim3(kKeyThreads), 0, s, keys, n,
+                       sel_state, cand, cand_cnt);
+    hipLaunchKernelGGL(select_rest_kernel, dim3(1), dim3(kRestThreads), 0, s, cand, cand_cnt,
+                       (int32_t)kb, n, sel_state);
     const int64_t nb = rbp::ceil_div(n, kSlotsPerBlock);
     hipLaunchKernelGGL(sel_count_kernel, dim3(nb), dim3(kCountThreads), 0, s, keys, n, sel_state,
                        sel_counts);
@@ -544,13 +800,25 @@ extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
     hipLaunchKernelGGL(pos_compact_kernel, dim3(nb), dim3(kCountThreads), 0, s, rec->reward,
                        rec->head, rec->capacity, n_range, offsets, pos_list);
   }
-  hipLaunchKernelGGL(draw_kernel, dim3(1), dim3(kDrawThreads), 0, s, p, meta, pos_list,
-                     rec->length, rec->advantage, rec->version, out->idx, out->adv, out->len,
-                     out->age, out->cu_seqlens, out->n_tokens, meta + 1);
+  if (cfg->n_draw <= kDrawThreads) {
+    hipLaunchKernelGGL(draw_kernel, dim3(1), dim3(kDrawThreads), 0, s, p, meta, pos_list,
+                       rec->length, rec->advantage, rec->version, out->idx, out->adv, out->len,
+                       out->age, out->cu_seqlens, out->n_tokens, meta + 1);
+  } else {
+    const int64_t nb = rbp::ceil_div(cfg->n_draw, kRowThreads);
+    hipLaunchKernelGGL(draw_rows_kernel, dim3(nb), dim3(kRowThreads), 0, s, p, meta, pos_list,
+                       rec->length, rec->advantage, rec->version, out->idx, out->adv, out->len,
+                       out->age, blk_sum);
+    hipLaunchKernelGGL(draw_scan_kernel, dim3(1), dim3(1024), 0, s, p, blk_sum, blk_off, nb,
+                       out->n_tokens, meta + 1);
+    hipLaunchKernelGGL(draw_cu_kernel, dim3(nb), dim3(kRowThreads), 0, s, p, out->len, blk_off,
+                       out->cu_seqlens);
+  }
   if (cfg->layout == RB_LAYOUT_PACKED) {
-    int64_t blocks = rbp::ceil_div(cfg->max_tokens, 256);
-    if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(gather_packed_kernel, dim3(blocks), dim3(256), 0, s, cfg->n_draw,
+    // about 256 window positions per block
+    int64_t by = rbp::ceil_div(cfg->max_tokens, cfg->n_draw * 256);
+    if (by > 64) by = 64;
+    hipLaunchKernelGGL(gather_packed_kernel, dim3(cfg->n_draw, by), dim3(256), 0, s,
                        rec->head, rec->capacity, cfg->token_begin, cfg->max_tokens, meta + 1,
                        out->cu_seqlens, out->idx, rec->arena_off, rec->arena_tokens,
                        rec->arena_old_logp, out->tokens, out->old_logp, out->seq_of_token);

@@ -80,6 +80,22 @@ def test_unused_first_matches_oracle(frac_used):
         assert np.array_equal(got["idx"], want)
 
 
+@pytest.mark.parametrize("n_draw,n_used", [(700, 0), (12_000, 290_000)])
+def test_without_replacement_large_buffer_matches_oracle(n_draw, n_used):
+    # 300000 records: more than a thousand keys share the selected top digit,
+    # so the select runs digit passes before ranking the survivors; with
+    # 290000 used records the draw spans all unused ones and the smallest used
+    rbp = require_gpu()
+    n_live = 300_000
+    use = np.zeros(n_live, dtype=np.int32)
+    use[:n_used] = 1 + np.arange(n_used) % 3
+    mode = rbp.RB_UNUSED_FIRST if n_used else rbp.RB_NO_REPLACE
+    rec, *_ = _records(rbp, n_live, n_live, 12_345, 4, use=use if n_used else None)
+    got = _draw(rbp, rec, n_live, mode, 5, 1, n_draw)
+    want = ob.sample_without_replacement(5, 1, n_live, n_draw, use_count=use if n_used else None)
+    assert np.array_equal(got["idx"], want)
+
+
 def test_without_replacement_rejects_bad_requests():
     rbp = require_gpu()
     rec, *_ = _records(rbp, 10, 10, 0, 1)

@@ -197,3 +197,55 @@ def test_same_seed_step_reproduces_and_rejects_bad_args():
     with pytest.raises(rbp.RbpError) as e:
         rbp.rb_sample_gather(ring.rec, cfg, rbp.alloc_batch(cfg), small)
     assert e.value.status == rbp.RBP_EWORKSPACE
+
+
+def _small_records(n, seed):
+    """n records of 1..8 tokens, about 30 % positive, versions 0..9."""
+    rng = np.random.default_rng(seed)
+    length = rng.integers(1, 9, n)
+    off = np.concatenate([[0], np.cumsum(length)[:-1]])
+    total = int(length.sum())
+    return dict(length=length, arena_off=off, reward=(rng.random(n) < 0.3).astype(np.float32),
+                adv=rng.standard_normal(n).astype(np.float32), version=rng.integers(0, 10, n),
+                tok=rng.integers(0, 1000, total).astype(np.int32),
+                old=rng.standard_normal(total).astype(np.float32))
+
+
+@pytest.mark.parametrize("mode,layout", [
+    ("uniform", "packed"), ("pos_mix", "padded"), ("pos_retain", "packed")])
+def test_many_draws_carry_the_length_prefix_across_rounds(mode, layout):
+    # 20000 draws: the per-draw pass runs several rounds of 4096 draws and
+    # carries the packed offsets from one round to the next
+    rbp = require_gpu()
+    r = _small_records(3000, 8)
+    ring = DeviceRing(rbp, r["length"], r["arena_off"], r["reward"], r["adv"], r["version"],
+                      r["tok"], r["old"], head=2999, capacity=3500)
+    n_fresh, n_pos_keep = ob.retain_split(3000, 0.25)
+    kw = dict(p_q32=philox.p_to_q32(0.5), n_fresh=n_fresh, n_pos_keep=n_pos_keep)
+    lk = dict(max_tokens=200_000) if layout == "packed" else dict(l_max=8)
+    got = _run(rbp, ring, mode, layout, 6, 2, 20_000, **kw, **lk)
+    idx = ob.sample_indices(r["reward"], MODES[mode], 6, 2, 20_000, **kw)
+    lay = ob.LAYOUT_PACKED if layout == "packed" else ob.LAYOUT_PADDED
+    want = ob.gather(idx, r["arena_off"], r["length"], r["adv"], r["version"], r["tok"],
+                     r["old"], 10, lay, **lk)
+    _compare(got, want)
+
+
+def test_without_replacement_many_draws_match_oracle():
+    # 9000 of 10000 records: the select's bucket holds most keys and the
+    # per-draw pass runs three rounds
+    rbp = require_gpu()
+    r = _small_records(10_000, 9)
+    ring = DeviceRing(rbp, r["length"], r["arena_off"], r["reward"], r["adv"], r["version"],
+                      r["tok"], r["old"], head=77, capacity=10_000)
+    cfg = rbp.make_sample_cfg(rbp.RB_NO_REPLACE, rbp.RB_LAYOUT_PACKED, 5, 1, 9000,
+                              cur_version=10, max_tokens=80_000)
+    out = rbp.alloc_batch(cfg)
+    print("[sampler] no_replace n_live=10000 n_draw=9000", flush=True)
+    rbp.rb_sample_gather(ring.rec, cfg, out, rbp.workspace(rbp.RBP_OP_SAMPLE_GATHER, 10_000))
+    torch.cuda.synchronize()
+    got = {k: to_np(v) for k, v in out.items()}
+    idx = ob.sample_without_replacement(5, 1, 10_000, 9000)
+    want = ob.gather(idx, r["arena_off"], r["length"], r["adv"], r["version"], r["tok"],
+                     r["old"], 10, ob.LAYOUT_PACKED, max_tokens=80_000)
+    _compare(got, want)
