@@ -30,6 +30,8 @@ __global__ void __launch_bounds__(64) group_advantage_kernel(
                        [&](int32_t i, float a) { adv[i] = a; });
 }
 
+constexpr int kSeqThreads = 256;  // threads per sequence of the whole-sequence ratio
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
@@ -209,29 +211,35 @@ __global__ void __launch_bounds__(64) sums_finalize_kernel(const float* __restri
   }
 }
 
-// Whole-sequence ratio: one wave per sequence sums log-ratios over its tokens
-// (lane-strided, fixed butterfly), forms rho_i, the term and the gradient,
-// writes dlogp over the sequence and the per-sequence values into `seqv`
-// ([B][4]: -l_i / n_seq, rho_i, clipped, l_i).
-__global__ void __launch_bounds__(256) seq_ratio_kernel(
+// Whole-sequence ratio: one block per sequence sums log-ratios over its
+// tokens (thread-strided, fixed butterfly per wave, the four wave sums in
+// order), forms rho_i, the term and the gradient, writes dlogp over the
+// sequence and the per-sequence values into `seqv` ([B][4]: -l_i / n_seq,
+// rho_i, clipped, l_i).
+__global__ void __launch_bounds__(kSeqThreads) seq_ratio_kernel(
     const float* __restrict__ logp, const float* __restrict__ old_logp,
-    const int32_t* __restrict__ cu, const float* __restrict__ adv, int32_t B, float inv_nseq,
+    const int32_t* __restrict__ cu, const float* __restrict__ adv, float inv_nseq,
     float eps_low, float eps_high, float* __restrict__ dlogp, float* __restrict__ seqv) {
-  const int32_t i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  __shared__ float red[kSeqThreads / 64];
+  const int32_t i = blockIdx.x;
   const int lane = threadIdx.x & 63;
-  if (i >= B) return;
   const int64_t lo = cu[i], hi = cu[i + 1];
   float s = 0.0f;
-  for (int64_t t = lo + lane; t < hi; t += 64) s += logp[t] - old_logp[t];
+  for (int64_t t = lo + threadIdx.x; t < hi; t += kSeqThreads) s += logp[t] - old_logp[t];
   s = wave_sum(s);
+  if (lane == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  s = red[0];
+#pragma unroll
+  for (int w = 1; w < kSeqThreads / 64; ++w) s += red[w];
   const float rho = expf(s);
   const float A = adv[i];
   const float lo_b = 1.0f - eps_low, hi_b = 1.0f + eps_high;
   const float term = fminf(rho * A, fminf(fmaxf(rho, lo_b), hi_b) * A);
   const bool cut = (A > 0.0f && rho > hi_b) || (A < 0.0f && rho < lo_b);
   const float g = cut ? 0.0f : -A * rho * inv_nseq;
-  for (int64_t t = lo + lane; t < hi; t += 64) dlogp[t] = g;
-  if (lane == 0) {
+  for (int64_t t = lo + threadIdx.x; t < hi; t += kSeqThreads) dlogp[t] = g;
+  if (threadIdx.x == 0) {
     float* v = seqv + (int64_t)i * 4;
     v[0] = -term * inv_nseq;
     v[1] = rho;
@@ -409,8 +417,8 @@ extern "C" int policy_loss_seq_fwd_bwd(const float* logp, const float* old_logp,
   const int64_t nbp = rbp::ceil_div(B, 256);
   float* partials = c.take<float>((size_t)nbp * kNumSums);
   const float inv_nseq = (float)(1.0 / (double)n_seq_total);
-  hipLaunchKernelGGL(seq_ratio_kernel, dim3(rbp::ceil_div(B, 4)), dim3(256), 0, s, logp,
-                     old_logp, cu_seqlens, adv, B, inv_nseq, eps_low, eps_high, dlogp, seqv);
+  hipLaunchKernelGGL(seq_ratio_kernel, dim3(B), dim3(kSeqThreads), 0, s, logp, old_logp,
+                     cu_seqlens, adv, inv_nseq, eps_low, eps_high, dlogp, seqv);
   if (T > 0) {
     int64_t blocks = rbp::ceil_div(T, 256);
     if (blocks > 1024) blocks = 1024;
