@@ -249,3 +249,19 @@ def test_without_replacement_many_draws_match_oracle():
     want = ob.gather(idx, r["arena_off"], r["length"], r["adv"], r["version"], r["tok"],
                      r["old"], 10, ob.LAYOUT_PACKED, max_tokens=80_000)
     _compare(got, want)
+
+
+def test_maximum_draw_count_packed():
+    # n_draw = 2^20, the largest batch the call accepts: 4096 blocks of draws
+    # and a scan over all their sums; the window stops inside the stream
+    rbp = require_gpu()
+    r = _small_records(5000, 10)
+    ring = DeviceRing(rbp, r["length"], r["arena_off"], r["reward"], r["adv"], r["version"],
+                      r["tok"], r["old"], head=4321, capacity=6000)
+    n = 1 << 20
+    lk = dict(max_tokens=3_000_000, token_begin=1_000_000)
+    got = _run(rbp, ring, "uniform", "packed", 12, 3, n, **lk)
+    idx = ob.sample_indices(r["reward"], ob.RB_UNIFORM, 12, 3, n)
+    want = ob.gather(idx, r["arena_off"], r["length"], r["adv"], r["version"], r["tok"],
+                     r["old"], 10, ob.LAYOUT_PACKED, **lk)
+    _compare(got, want)
