@@ -185,3 +185,19 @@ def test_bitwise_reproducible_and_bad_args():
                                torch.empty(T, device="cuda"),
                                torch.empty(16, dtype=torch.uint8, device="cuda"))
     assert e.value.status == rbp.RBP_EWORKSPACE
+
+
+def test_empty_batch():
+    # T = 0: the forward writes nothing; the backward zeroes dW, or leaves an
+    # accumulated dW untouched
+    rbp = require_gpu()
+    d, V = 64, 1000
+    hidden, W, tokens = wlm.head(0, d, V, seed=4, device="cuda")
+    logp, lse = _fwd(rbp, hidden, W, tokens, None)
+    assert logp.numel() == 0 and lse.numel() == 0
+    empty = torch.empty(0, device="cuda")
+    _, dW = _bwd(rbp, hidden, W, tokens, None, empty, empty)
+    assert torch.count_nonzero(dW) == 0
+    dW0 = wlm.normal(V * d, 1.0, 5, device="cuda").view(V, d)
+    _, dW = _bwd(rbp, hidden, W, tokens, None, empty, empty, ws_tokens=1, dW0=dW0)
+    assert torch.equal(dW, dW0)

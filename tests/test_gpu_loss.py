@@ -113,3 +113,18 @@ def test_loss_on_policy_and_determinism():
     want = np.where(seq >= 0, -adv[np.maximum(seq, 0)] / (B * lens[np.maximum(seq, 0)]), 0)
     assert np.allclose(outs[0][1], want, rtol=1e-6, atol=0)
     assert outs[0][2][1] == 0
+
+
+def test_loss_empty_batch_adds_nothing():
+    # T = 0: the accumulated loss and statistics stay as they were
+    rbp = require_gpu()
+    adv = torch.tensor([1.0, -1.0, 0.5], device="cuda")
+    lens = torch.tensor([4, 5, 6], dtype=torch.int32, device="cuda")
+    e = torch.empty(0, device="cuda")
+    ei = torch.empty(0, dtype=torch.int32, device="cuda")
+    loss = torch.full((1,), 0.25, device="cuda")
+    stats = torch.full((4,), 2.0, device="cuda")
+    rbp.policy_loss_fwd_bwd(e, e, ei, adv, lens, 3, loss, e, stats,
+                            rbp.workspace(rbp.RBP_OP_LOSS, 0))
+    torch.cuda.synchronize()
+    assert to_np(loss)[0] == 0.25 and np.all(to_np(stats) == 2.0)
