@@ -26,6 +26,11 @@ Paper passages followed:
   B records with the smallest per-record random keys (a uniformly random
   B-subset), listed in slot order; "at least once" ranks never-used records
   ahead of used ones.
+* Buffer statistics (Sec. 3.2, "Off-Policiness, Diversity, and Compute
+  Efficiency"): off-policiness of a sample = steps since its rollout was
+  generated; replay ratio of a rollout = number of gradient steps that used
+  it over the run, final when the rollout leaves the buffer.  Kept as
+  histograms of those integers.
 * Steps-since-last-use (App. D.3, "Metrics"): samples are ordered batch by
   batch, in a random order inside a batch (here: draw order); a sample of a
   rollout seen for the first time is "new" (-1 here), any later one gets the
@@ -170,6 +175,42 @@ def steps_since_last_use(batches):
             last[rid] = step
         out.append(vals)
     return out
+
+
+def histogram(values, n_bins, lo=0):
+    """Counts of integers in ``n_bins`` bins: value v lands in bin v - lo,
+    values below ``lo`` in the first bin and values past the last bin in the
+    last one.  The buffer statistics of Sec. 3.2 are distributions of small
+    integers: off-policiness (a sample's age in steps), replay ratio (how
+    often a rollout is used) and steps since last use, where lo = -1 gives
+    "new" (-1) the first bin."""
+    if n_bins < 1:
+        raise ValueError("n_bins must be >= 1")
+    h = [0] * n_bins
+    for v in values:
+        h[min(max(int(v) - lo, 0), n_bins - 1)] += 1
+    return h
+
+
+def replay_ratios(capacity, steps):
+    """Replay ratio of each rollout (Sec. 3.2: the number of gradient steps
+    that used it) in a FIFO buffer of ``capacity`` records.
+
+    ``steps``: list of (n_new, draws) in processing order; each step first
+    pushes ``n_new`` fresh rollouts (evicting the oldest ones past the
+    capacity), then uses the records at slots ``draws`` (0 = oldest live
+    record, with repeats counting once per draw).  Returns (use counts of the
+    evicted rollouts in eviction order, use counts of the live ones oldest
+    first)."""
+    live, evicted = [], []
+    for n_new, draws in steps:
+        for _ in range(int(n_new)):
+            if len(live) == capacity:
+                evicted.append(live.pop(0))
+            live.append(0)
+        for s in draws:
+            live[s] += 1
+    return evicted, live
 
 
 def gather(idx, rec_off, rec_len, rec_adv, rec_version, arena_tokens,

@@ -268,3 +268,48 @@ def test_steps_since_last_use_brute_force():
             prev = [s for s, r in history if r == rid]
             assert v == (-1 if not prev else step - prev[-1])
             history.append((step, rid))
+
+
+def test_histogram_bins_by_hand():
+    # since values with "new" = -1 in bin 0; the tail collects 5 and 9
+    assert ob.histogram([-1, 0, 0, 2, 5, 9, -1], 5, lo=-1) == [2, 2, 0, 1, 2]
+    assert ob.histogram([], 3) == [0, 0, 0]
+    assert ob.histogram([3, -4, 1], 1) == [3]
+    vals = np.random.default_rng(0).integers(-3, 40, 1000)
+    h = ob.histogram(vals, 12, lo=-2)
+    assert sum(h) == 1000
+    assert h[0] == int(np.sum(vals <= -2)) and h[-1] == int(np.sum(vals >= 9))
+    assert h[5] == int(np.sum(vals == 3))
+
+
+def test_replay_ratios_by_hand():
+    # capacity 3: push 2, use slot 0 twice and slot 1; push 2 (evicts the first,
+    # used twice), use slots 0 and 2; push 1 (evicts the second, used twice)
+    ev, live = ob.replay_ratios(3, [(2, [0, 0, 1]), (2, [0, 2]), (1, [])])
+    assert ev == [2, 2] and live == [0, 1, 0]
+
+
+def test_replay_ratios_conserve_draws():
+    rng = np.random.default_rng(1)
+    steps, total = [], 0
+    for _ in range(50):
+        n_new = int(rng.integers(0, 6))
+        n_live = min(20, sum(s[0] for s in steps) + n_new)
+        draws = rng.integers(0, n_live, int(rng.integers(0, 9))).tolist() if n_live else []
+        steps.append((n_new, draws))
+        total += len(draws)
+    ev, live = ob.replay_ratios(20, steps)
+    assert sum(ev) + sum(live) == total
+    assert len(ev) + len(live) == sum(s[0] for s in steps) and len(live) == 20
+
+
+def test_replay_ratio_mean_is_batch_over_inserts():
+    # uniform draws with replacement: each record is drawn B/N times per step
+    # in expectation (App. C.1) and stays N/R steps, so its replay ratio has
+    # mean B/R
+    N, R, B = 64, 8, 24
+    rng = np.random.default_rng(2)
+    steps = [(R, rng.integers(0, min(N, R * (k + 1)), B).tolist()) for k in range(4000)]
+    ev, _ = ob.replay_ratios(N, steps)
+    steady = ev[N:]
+    assert abs(np.mean(steady) - B / R) < 0.03
