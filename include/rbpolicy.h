@@ -13,6 +13,7 @@
  *   rb_sample_gather     draw records and gather their tokens         (Sec. 3.1, 5; App. B, D.4)
  *   rb_push              append generated groups, FIFO eviction      (App. B, D.2)
  *   rb_note_use          per-record use counts, steps since last use (App. D.3)
+ *   rb_hist_accumulate   histograms of the buffer statistics         (Sec. 3.2)
  *   policy_logprob_fwd   log pi(y_t) from hidden states and W         (App. D.2)
  *   policy_loss_fwd_bwd  clipped GRPO loss and d loss / d logp        (App. D.2)
  *   policy_logprob_bwd   d loss / d hidden and d loss / d W           (chain rule of the above)
@@ -393,6 +394,10 @@ typedef struct rb_ring {
   int64_t* last_step;        /* device [capacity] or NULL: reset to -1 on insert    */
   int32_t* arena_tokens;     /* device [capacity * slot_tokens]                    */
   float* arena_old_logp;     /* device [capacity * slot_tokens]                    */
+  int64_t* replay_hist;      /* device [replay_bins] or NULL: replay ratios of the
+                                records a push evicts, added to (see rb_push)     */
+  int32_t replay_bins;       /* 1 .. 4096 when replay_hist is set                  */
+  int32_t pad_;
 } rb_ring;
 
 /*
@@ -410,9 +415,15 @@ typedef struct rb_ring {
  * cut to that).  version is stored for every new record.  The device-side
  * group_off, length and src_off are trusted (not read on the host): offsets
  * outside the given arrays are the caller's error.
+ * Replay ratios (Sec. 3.2: the number of gradient steps that used a
+ * rollout): when replay_hist is set, each evicted record's final use_count u
+ * adds 1 to replay_hist[min(u, replay_bins - 1)] before its row is reused
+ * (needs use_count; integer atomics, order-free).
  * Errors: RBP_EINVAL (null pointers, n_new outside [1, capacity],
  *         n_groups < 1, n_live outside [0, capacity], head outside
- *         [0, capacity), slot_tokens < 1, ddof not 0 or 1, eps < 0).
+ *         [0, capacity), slot_tokens < 1, ddof not 0 or 1, eps < 0,
+ *         replay_hist without use_count or with replay_bins outside
+ *         [1, 4096]).
  */
 int rb_push(rb_ring* ring, int32_t n_new, int32_t n_groups, const int32_t* group_off,
             const int32_t* length, const int64_t* src_off, const float* reward,
@@ -436,6 +447,21 @@ int rb_push(rb_ring* ring, int32_t n_new, int32_t n_groups, const int32_t* group
 int rb_note_use(const int32_t* idx, int64_t n_draw, int64_t head, int64_t capacity,
                 int64_t step, int32_t* use_count, int64_t* last_step, int32_t* since,
                 void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Buffer statistics as histograms (Sec. 3.2: the distributions of
+ * off-policiness, replay ratio and steps since last use): value v of
+ * values device int32 [n] adds 1 to hist[min(max(v - lo, 0), n_bins - 1)].
+ * Typical inputs: the age output of rb_sample_gather (off-policiness, lo =
+ * 0), the since output of rb_note_use (lo = -1, so "new" has bin 0), a
+ * use_count array (replay ratios of live records, lo = 0).  hist device
+ * int64 [n_bins], ADDED to; integer atomics, so the counts do not depend on
+ * the order of the additions.
+ * Errors: RBP_EINVAL (n < 0, n_bins outside [1, 4096], null pointers when
+ *         n > 0).
+ */
+int rb_hist_accumulate(const int32_t* values, int64_t n, int32_t lo, int32_t n_bins,
+                       int64_t* hist, void* stream);
 
 /* Workspace bytes an operation needs (see RBP_OP_*); 0 for an invalid op. */
 size_t rbp_workspace_bytes(int op, int64_t n, int32_t d, int32_t V);

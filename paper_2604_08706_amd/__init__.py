@@ -46,6 +46,7 @@ from ._binding import (  # noqa: F401
     policy_loss_seq_fwd_bwd,
     rb_asymre_coef,
     rb_group_advantage,
+    rb_hist_accumulate,
     rb_note_use,
     rb_push,
     rb_sample_gather,

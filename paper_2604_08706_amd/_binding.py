@@ -41,6 +41,7 @@ EXPORTED = (
     "policy_loss_fwd_bwd", "policy_logprob_bwd", "rbp_workspace_bytes",
     "rbp_status_string", "rbp_last_error", "policy_loss_seq_fwd_bwd", "rb_asymre_coef",
     "policy_asymre_fwd_bwd", "policy_fused_fwd_bwd", "rb_push", "rb_note_use",
+    "rb_hist_accumulate",
 )
 
 
@@ -69,7 +70,8 @@ class RbRing(ctypes.Structure):
         ("reward", ctypes.c_void_p), ("advantage", ctypes.c_void_p),
         ("version", ctypes.c_void_p), ("use_count", ctypes.c_void_p),
         ("last_step", ctypes.c_void_p), ("arena_tokens", ctypes.c_void_p),
-        ("arena_old_logp", ctypes.c_void_p),
+        ("arena_old_logp", ctypes.c_void_p), ("replay_hist", ctypes.c_void_p),
+        ("replay_bins", ctypes.c_int32), ("pad_", ctypes.c_int32),
     ]
 
 
@@ -121,6 +123,7 @@ def load_library(path=LIB_PATH):
     lib.rb_push.argtypes = [ctypes.POINTER(RbRing), i32, i32, vp, vp, vp, vp, i32, vp, vp, i32,
                             f32, vp]
     lib.rb_note_use.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, sz, vp]
+    lib.rb_hist_accumulate.argtypes = [vp, i64, i32, i32, vp, vp]
     lib.rbp_workspace_bytes.argtypes = [ctypes.c_int, i64, i32, i32]
     lib.rbp_workspace_bytes.restype = sz
     lib.rbp_status_string.argtypes = [ctypes.c_int]
@@ -391,9 +394,10 @@ def policy_fused_fwd_bwd(hidden, W, tokens, seq_of_token, old_logp, adv, seq_len
     _check("policy_fused_fwd_bwd", st)
 
 
-def make_ring(capacity, slot_tokens, device="cuda", counters=True):
+def make_ring(capacity, slot_tokens, device="cuda", counters=True, replay_bins=0):
     """Allocate an empty ring record table (rb_ring) with torch; returns the
-    struct, which keeps its tensors in ``ring.t``."""
+    struct, which keeps its tensors in ``ring.t``.  replay_bins > 0 (needs
+    counters) adds the histogram of evicted records' replay ratios."""
     cap, st = int(capacity), int(slot_tokens)
     t = {
         "arena_off": torch.zeros(cap, dtype=torch.int64, device=device),
@@ -406,10 +410,13 @@ def make_ring(capacity, slot_tokens, device="cuda", counters=True):
         if counters else None,
         "arena_tokens": torch.zeros(cap * st, dtype=torch.int32, device=device),
         "arena_old_logp": torch.zeros(cap * st, dtype=torch.float32, device=device),
+        "replay_hist": torch.zeros(int(replay_bins), dtype=torch.int64, device=device)
+        if replay_bins > 0 else None,
     }
     ring = RbRing()
     ring.t = t
     ring.n_live, ring.capacity, ring.head, ring.slot_tokens = 0, cap, 0, st
+    ring.replay_bins = int(replay_bins)
     for k, v in t.items():
         setattr(ring, k, 0 if v is None else v.data_ptr())
     return ring
@@ -449,3 +456,10 @@ def rb_note_use(idx, head, capacity, step, use_count, last_step, since, ws, stre
                            _dev(last_step, torch.int64, "last_step", capacity),
                            _opt(since, torch.int32, "since", n), wsp, wsb, _stream(stream))
     _check("rb_note_use", st)
+
+
+def rb_hist_accumulate(values, hist, lo=0, stream=None):
+    n = values.numel()
+    st = lib().rb_hist_accumulate(_dev(values, torch.int32, "values", n), n, int(lo),
+                                  hist.numel(), _dev(hist, torch.int64, "hist"), _stream(stream))
+    _check("rb_hist_accumulate", st)

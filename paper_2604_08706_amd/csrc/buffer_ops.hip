@@ -1,12 +1,15 @@
-// Buffer maintenance: FIFO insertion of generated groups (rb_push) and
-// per-record usage bookkeeping (rb_note_use).
+// Buffer maintenance: FIFO insertion of generated groups (rb_push),
+// per-record usage bookkeeping (rb_note_use) and the histograms of the buffer
+// statistics (rb_hist_accumulate).
 //
 // Paper: the buffer holds the N most recent rollouts; a push into a full
 // buffer evicts the oldest one and sampling never removes (App. B
 // "BufferStructure"); advantages are computed once, when a group is generated
 // (App. D.2).  Steps-since-last-use (App. D.3, "Metrics"): a rollout's first
 // sample is "new", a later one gets the gradient steps since its previous
-// sample, 0 for repeats inside one batch.
+// sample, 0 for repeats inside one batch.  Sec. 3.2 reports the distributions
+// of off-policiness (a sample's age), replay ratio (uses of a rollout over the
+// run) and steps since last use.
 //
 // The record table is a ring: logical slot s is physical row (head + s) %
 // capacity, and row r owns a fixed arena stretch of slot_tokens tokens, so an
@@ -72,6 +75,21 @@ __global__ void __launch_bounds__(256) push_copy_kernel(
   }
 }
 
+// Replay ratio of the records a push evicts (Sec. 3.2): new record i >= first
+// overwrites a row that still holds a live record; its final use count goes
+// to the histogram before push_rows_kernel resets it.
+__global__ void __launch_bounds__(256) push_evict_kernel(int32_t n_new, int64_t first,
+                                                         int64_t base, int64_t cap,
+                                                         const int32_t* __restrict__ uses,
+                                                         int32_t n_bins,
+                                                         int64_t* __restrict__ hist) {
+  const int64_t i = first + (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n_new) return;
+  int32_t u = uses[ring_row(base, i, cap)];
+  u = u < 0 ? 0 : (u > n_bins - 1 ? n_bins - 1 : u);
+  atomicAdd(reinterpret_cast<unsigned long long*>(hist + u), 1ull);
+}
+
 // ---- usage bookkeeping ------------------------------------------------------
 
 __device__ __forceinline__ int64_t drawn_row(const int32_t* __restrict__ idx, int64_t j,
@@ -124,6 +142,27 @@ __global__ void __launch_bounds__(256) use_update_kernel(const int32_t* __restri
   }
 }
 
+// ---- statistics ------------------------------------------------------------
+
+constexpr int kHistMaxBins = 4096;
+
+// Block histogram in LDS, then one integer atomic per non-empty bin.
+__global__ void __launch_bounds__(256) hist_kernel(const int32_t* __restrict__ values, int64_t n,
+                                                   int32_t lo, int32_t n_bins,
+                                                   int64_t* __restrict__ hist) {
+  __shared__ uint32_t h[kHistMaxBins];
+  for (int b = threadIdx.x; b < n_bins; b += 256) h[b] = 0u;
+  __syncthreads();
+  for (int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x; j < n; j += (int64_t)gridDim.x * 256) {
+    int64_t b = (int64_t)values[j] - lo;
+    b = b < 0 ? 0 : (b > n_bins - 1 ? n_bins - 1 : b);
+    atomicAdd(&h[b], 1u);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < n_bins; b += 256)
+    if (h[b] != 0u) atomicAdd(reinterpret_cast<unsigned long long*>(hist + b), (unsigned long long)h[b]);
+}
+
 }  // namespace
 
 size_t rbp::note_use_ws(int64_t capacity) {
@@ -152,10 +191,21 @@ extern "C" int rb_push(rb_ring* ring, int32_t n_new, int32_t n_groups, const int
               RBP_EINVAL, "rb_push: null ring array");
   RBP_REQUIRE(group_off && length && src_off && reward && tokens && old_logp, RBP_EINVAL,
               "rb_push: null input array");
+  RBP_REQUIRE(ring->replay_hist == nullptr ||
+                  (ring->use_count != nullptr && ring->replay_bins >= 1 &&
+                   ring->replay_bins <= kHistMaxBins),
+              RBP_EINVAL, "rb_push: replay_hist needs use_count and 1 <= replay_bins <= %d",
+              kHistMaxBins);
   hipStream_t s = rbp::as_stream(stream);
   // the first free row: just past the newest record
   int64_t base = ring->head + ring->n_live;
   if (base >= cap) base -= cap;
+  // new records from index cap - n_live on overwrite live ones
+  const int64_t first_evict = cap - ring->n_live;
+  if (ring->replay_hist != nullptr && first_evict < n_new)
+    hipLaunchKernelGGL(push_evict_kernel, dim3(rbp::ceil_div(n_new - first_evict, 256)),
+                       dim3(256), 0, s, n_new, first_evict, base, cap, ring->use_count,
+                       ring->replay_bins, ring->replay_hist);
   hipLaunchKernelGGL(push_rows_kernel, dim3(rbp::ceil_div(n_new, 256)), dim3(256), 0, s, n_new,
                      base, cap, ring->slot_tokens, length, reward, version, ring->arena_off,
                      ring->length, ring->reward, ring->version, ring->use_count,
@@ -203,5 +253,21 @@ extern "C" int rb_note_use(const int32_t* idx, int64_t n_draw, int64_t head, int
   hipLaunchKernelGGL(use_update_kernel, dim3(blocks), dim3(256), 0, s, idx, n_draw, head,
                      capacity, step, first, use_count, last_step);
   RBP_CHECK_LAUNCH("rb_note_use");
+  return RBP_OK;
+}
+
+extern "C" int rb_hist_accumulate(const int32_t* values, int64_t n, int32_t lo, int32_t n_bins,
+                                  int64_t* hist, void* stream) {
+  rbp::clear_error();
+  RBP_REQUIRE(n >= 0, RBP_EINVAL, "rb_hist_accumulate: n < 0");
+  RBP_REQUIRE(n_bins >= 1 && n_bins <= kHistMaxBins, RBP_EINVAL,
+              "rb_hist_accumulate: n_bins %d outside [1, %d]", n_bins, kHistMaxBins);
+  if (n == 0) return RBP_OK;
+  RBP_REQUIRE(values && hist, RBP_EINVAL, "rb_hist_accumulate: null pointer");
+  int64_t blocks = rbp::ceil_div(n, 256 * 8);
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(hist_kernel, dim3(blocks), dim3(256), 0, rbp::as_stream(stream), values, n,
+                     lo, n_bins, hist);
+  RBP_CHECK_LAUNCH("rb_hist_accumulate");
   return RBP_OK;
 }

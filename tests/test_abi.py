@@ -106,6 +106,20 @@ def test_invalid_arguments_fail_on_the_host():
     assert lib.rb_group_advantage(null, null, 3, 1, 1e-6, null, null) == b.RBP_EINVAL
     assert lib.rb_group_advantage(ctypes.c_void_p(8), ctypes.c_void_p(8), 3, 2, 1e-6,
                                   ctypes.c_void_p(8), null) == b.RBP_EINVAL
+    assert lib.rb_hist_accumulate(null, 5, 0, 4, null, null) == b.RBP_EINVAL
+    assert lib.rb_hist_accumulate(null, 0, 0, 0, null, null) == b.RBP_EINVAL
+    assert lib.rb_hist_accumulate(null, 0, 0, 4097, null, null) == b.RBP_EINVAL
+    # a replay-ratio histogram needs the use counts
+    ring = b.RbRing()
+    ring.capacity, ring.slot_tokens = 4, 2
+    for f in ("arena_off", "length", "reward", "advantage", "version", "arena_tokens",
+              "arena_old_logp", "replay_hist"):
+        setattr(ring, f, 8)
+    ring.replay_bins = 4
+    d8 = ctypes.c_void_p(8)
+    assert lib.rb_push(ctypes.byref(ring), 2, 1, d8, d8, d8, d8, 0, d8, d8, 1, 1e-6,
+                       null) == b.RBP_EINVAL
+    assert b"replay_hist" in lib.rbp_last_error()
     lib.rbp_status_string(0)
     # a successful call clears the thread's error text
     assert lib.rb_group_advantage(ctypes.c_void_p(8), ctypes.c_void_p(8), 0, 1, 1e-6,

@@ -187,3 +187,70 @@ def test_push_is_fifo_with_advantages_at_insert():
                     torch.zeros(11, dtype=torch.int64, device="cuda"),
                     torch.zeros(11, device="cuda"), 0,
                     torch.zeros(1, dtype=torch.int32, device="cuda"), torch.zeros(1, device="cuda"))
+
+
+@pytest.mark.parametrize("n,n_bins,lo", [(0, 3, 0), (1, 1, 0), (1000, 7, -1), (300_000, 4096, 5),
+                                         (300_000, 33, -1)])
+def test_hist_accumulate_matches_oracle(n, n_bins, lo):
+    rbp = require_gpu()
+    rng = np.random.default_rng(n + n_bins)
+    vals = rng.integers(-3, 5000, n).astype(np.int32)
+    hist = torch.zeros(n_bins, dtype=torch.int64, device="cuda")
+    print(f"[buffer] hist n={n} n_bins={n_bins} lo={lo}", flush=True)
+    for _ in range(2):  # accumulates
+        rbp.rb_hist_accumulate(torch.from_numpy(vals).cuda(), hist, lo)
+    torch.cuda.synchronize()
+    want = 2 * np.array(ob.histogram(vals, n_bins, lo), dtype=np.int64)
+    assert np.array_equal(to_np(hist), want)
+
+
+def test_buffer_statistics_over_a_run():
+    # pushes with evictions, uniform draws and usage updates: the ring's
+    # replay-ratio histogram of evicted records, the live use counts, and the
+    # histograms of ages (off-policiness) and steps since last use
+    rbp = require_gpu()
+    cap, slot, bins = 12, 4, 6
+    ring = rbp.make_ring(cap, slot, replay_bins=bins)
+    ws = rbp.workspace(rbp.RBP_OP_NOTE_USE, cap)
+    rng = np.random.default_rng(9)
+    age_h = torch.zeros(8, dtype=torch.int64, device="cuda")
+    since_h = torch.zeros(6, dtype=torch.int64, device="cuda")
+    steps, ages, sinces, batches, versions = [], [], [], [], []
+    for step in range(14):
+        n_new = int(rng.integers(1, 6))
+        lens = np.full(n_new, 2, dtype=np.int32)
+        goff = np.array([0, n_new], dtype=np.int32)
+        rbp.rb_push(ring, torch.from_numpy(goff).cuda(), torch.from_numpy(lens).cuda(),
+                    torch.arange(n_new, dtype=torch.int64, device="cuda") * 2,
+                    torch.zeros(n_new, device="cuda"), step,
+                    torch.zeros(2 * n_new, dtype=torch.int32, device="cuda"),
+                    torch.zeros(2 * n_new, device="cuda"))
+        versions = (versions + [step] * n_new)[-cap:]
+        n_draw = 7
+        cfg = rbp.make_sample_cfg(rbp.RB_UNIFORM, rbp.RB_LAYOUT_PACKED, 4, step, n_draw,
+                                  cur_version=step, max_tokens=2 * n_draw)
+        out = rbp.alloc_batch(cfg)
+        print(f"[buffer] statistics step={step} n_live={ring.n_live}", flush=True)
+        rbp.rb_sample_gather(rbp.ring_records(ring), cfg, out,
+                             rbp.workspace(rbp.RBP_OP_SAMPLE_GATHER, cap))
+        since = torch.empty(n_draw, dtype=torch.int32, device="cuda")
+        rbp.rb_note_use(out["idx"], ring.head, cap, step, ring.t["use_count"],
+                        ring.t["last_step"], since, ws)
+        rbp.rb_hist_accumulate(out["age"], age_h, 0)
+        rbp.rb_hist_accumulate(since, since_h, -1)
+        torch.cuda.synchronize()
+        draws = ob.sample_indices([0.0] * ring.n_live, ob.RB_UNIFORM, 4, step, n_draw)
+        assert np.array_equal(to_np(out["idx"]), draws)
+        steps.append((n_new, draws))
+        ages += [step - versions[s] for s in draws]
+        # rollout ids: the k-th rollout ever pushed is id k
+        first_id = sum(n for n, _ in steps) - ring.n_live
+        batches.append((step, [first_id + s for s in draws]))
+    evicted, live = ob.replay_ratios(cap, steps)
+    assert len(evicted) > 0
+    assert np.array_equal(to_np(ring.t["replay_hist"]), ob.histogram(evicted, bins))
+    phys = (ring.head + np.arange(ring.n_live)) % cap
+    assert np.array_equal(to_np(ring.t["use_count"])[phys], live)
+    assert np.array_equal(to_np(age_h), ob.histogram(ages, 8))
+    sinces = [v for b in ob.steps_since_last_use(batches) for v in b]
+    assert np.array_equal(to_np(since_h), ob.histogram(sinces, 6, lo=-1))
