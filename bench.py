@@ -228,6 +228,8 @@ def aux_stress(iters=20):
       a radix select), padded; note_use: the usage update of 256 draws;
       loss_seq_ratio, loss_asymre: the objective variants over the loss's
       tokens (12 B per token: logp, old_logp or seq id read, dlogp written);
+      group_advantage: advantages of all 10^6 records in groups of 8 (4 B
+      reward read + 4 B advantage written per record, 4 B per group offset);
       push: FIFO insertion of 1024 rollouts (16 B per token: tokens and
       behaviour log-probs read and written, 40 B per record).
     Algorithmic bytes: gather = 4 B/record reward scan + 4 B per positive slot
@@ -372,6 +374,13 @@ def aux_stress(iters=20):
                                                    st2, ws_l))
     a_bytes = 12 * T + 4 * wl.n_draw
 
+    # group advantages of every record of the buffer (10^6 rewards, groups of 8)
+    rew_all = torch.from_numpy(tab.reward).to(dev)
+    goff_all = torch.from_numpy(tab.group_off).to(dev)
+    adv_all = torch.empty(n, device=dev)
+    v_ms = timed(lambda: rbp.rb_group_advantage(rew_all, goff_all, adv_all))
+    v_bytes = 8 * n + 4 * (len(tab.group_off))
+
     # FIFO insertion of 128 groups of 8 rollouts (the stress length mix) into
     # a 65536-row ring with 8192 arena tokens per row
     ring = rbp.make_ring(65536, 8192, device=dev)
@@ -386,7 +395,7 @@ def aux_stress(iters=20):
     rew = (torch.rand(n_new, device=dev) < 0.4).float()
     p_ms = timed(lambda: rbp.rb_push(ring, goff, lens, src, rew, 1, new_tok, new_old))
     p_bytes = 16 * tot + 40 * n_new
-    del tok, old, keep, rec, ring
+    del tok, old, keep, rec, ring, rew_all, goff_all, adv_all
     torch.cuda.empty_cache()
     return {
         "workload": "stress: 10^6 records, 256 positive-mixture draws (p_pos 0.5), "
@@ -405,6 +414,9 @@ def aux_stress(iters=20):
                            "GB/s": round(s_bytes / (s_ms / 1e3) / 1e9, 1)},
         "loss_asymre": {"tokens": T, "ms": round(a_ms, 4), "bytes": a_bytes,
                         "GB/s": round(a_bytes / (a_ms / 1e3) / 1e9, 1)},
+        "group_advantage": {"records": n, "groups": len(tab.group_off) - 1,
+                            "ms": round(v_ms, 4), "bytes": v_bytes,
+                            "GB/s": round(v_bytes / (v_ms / 1e3) / 1e9, 1)},
         "push": {"records": n_new, "tokens": tot, "ms": round(p_ms, 4), "bytes": p_bytes,
                  "GB/s": round(p_bytes / (p_ms / 1e3) / 1e9, 1)},
         "loss": {"tokens": T, "ms": round(l_ms, 4), "bytes": l_bytes,
