@@ -254,3 +254,30 @@ def test_buffer_statistics_over_a_run():
     assert np.array_equal(to_np(age_h), ob.histogram(ages, 8))
     sinces = [v for b in ob.steps_since_last_use(batches) for v in b]
     assert np.array_equal(to_np(since_h), ob.histogram(sinces, 6, lo=-1))
+
+
+def test_push_of_a_full_capacity_evicts_exactly_the_live_records():
+    # ring of 8 holding 5 used records; a push of 8 overwrites every row and
+    # evicts exactly the 5 (their use counts go to the replay histogram)
+    rbp = require_gpu()
+    cap = 8
+    ring = rbp.make_ring(cap, 2, replay_bins=4)
+    ws = rbp.workspace(rbp.RBP_OP_NOTE_USE, cap)
+
+    def push(n, version):
+        rbp.rb_push(ring, torch.tensor([0, n], dtype=torch.int32, device="cuda"),
+                    torch.ones(n, dtype=torch.int32, device="cuda"),
+                    torch.arange(n, dtype=torch.int64, device="cuda"),
+                    torch.zeros(n, device="cuda"), version,
+                    torch.zeros(n, dtype=torch.int32, device="cuda"), torch.zeros(n, device="cuda"))
+
+    push(5, 0)
+    draws = [0, 0, 0, 1, 1, 4, 4, 4, 4, 4]  # uses 3, 2, 0, 0, 5
+    rbp.rb_note_use(torch.tensor(draws, dtype=torch.int32, device="cuda"), ring.head, cap, 0,
+                    ring.t["use_count"], ring.t["last_step"], None, ws)
+    push(cap, 1)
+    torch.cuda.synchronize()
+    ev, live = ob.replay_ratios(cap, [(5, draws), (cap, [])])
+    assert ev == [3, 2, 0, 0, 5] and ring.n_live == cap
+    assert np.array_equal(to_np(ring.t["replay_hist"]), ob.histogram(ev, 4))
+    assert np.all(to_np(ring.t["use_count"]) == 0) and np.all(to_np(ring.t["version"]) == 1)
