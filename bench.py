@@ -84,9 +84,11 @@ def copy_probe(mib):
 
 
 def blas_probe(steps=10, warmup=3):
-    """Z^T = W H^T in bf16 through torch.mm (hipBLASLt) at the 7B head shape:
-    the same 2*T*d*V flop as the forward product, with no log-sum-exp, both
-    operands contiguous.  A measurement of the vendor GEMM, not a product path."""
+    """The three products of a replay step through torch.mm (hipBLASLt) at the
+    7B head shape, bf16 in and out, every operand contiguous: the forward's
+    Z^T = W H^T, dhidden = dZ W and dW = dZ^T H, each 2*T*d*V flop (no
+    log-sum-exp, no dz epilogue, no accumulation).  A measurement of the
+    vendor GEMM, not a product path."""
     import torch
 
     from paper_2604_08706_amd import workloads as wlm
@@ -95,21 +97,30 @@ def blas_probe(steps=10, warmup=3):
     T = wl.max_tokens
     hidden, W, _ = wlm.head(T, wl.d, wl.V, 0, device="cuda")
     ht = hidden.t().contiguous()
-    out = torch.empty((wl.V, T), dtype=torch.bfloat16, device="cuda")
-    for _ in range(warmup):
-        torch.mm(W, ht, out=out)
-    torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(steps):
-        torch.mm(W, ht, out=out)
-    b.record()
-    torch.cuda.synchronize()
-    ms = a.elapsed_time(b) / steps
+    dz = (torch.randn((T, wl.V), device="cuda") * 1e-3).bfloat16()
+    dzt = dz.t().contiguous()
+    cases = [
+        ("forward Z^T = W H^T: [V, d] x [d, T]", W, ht, (wl.V, T)),
+        ("dhidden = dZ W: [T, V] x [V, d]", dz, W, (T, wl.d)),
+        ("dW = dZ^T H: [V, T] x [T, d]", dzt, hidden, (wl.V, wl.d)),
+    ]
     flop = 2.0 * T * wl.d * wl.V
-    print(json.dumps({"probe": "torch.mm bf16 [V, d] x [d, T]", "T": T, "d": wl.d, "V": wl.V,
-                      "ms": round(ms, 3), "TFLOP/s": round(flop / (ms / 1e3) / 1e12, 1),
-                      "frac_peak": round(flop / (ms / 1e3) / PEAK_BF16, 4)}), flush=True)
+    for name, a_, b_, shape in cases:
+        out = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+        for _ in range(warmup):
+            torch.mm(a_, b_, out=out)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            torch.mm(a_, b_, out=out)
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / steps
+        print(json.dumps({"probe": "torch.mm bf16 " + name, "T": T, "d": wl.d, "V": wl.V,
+                          "ms": round(ms, 3), "TFLOP/s": round(flop / (ms / 1e3) / 1e12, 1),
+                          "frac_peak": round(flop / (ms / 1e3) / PEAK_BF16, 4)}), flush=True)
+        del out
 
 
 def sources_sha256():
