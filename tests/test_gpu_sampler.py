@@ -144,7 +144,8 @@ def test_head7b_micro_batch_is_full():
 
 
 def test_stress_million_records_padded():
-    """10^6 records, ~1.8e9 arena tokens in HBM, 256 mixed draws, padded to 8192."""
+    """10^6 records, ~1.8e9 arena tokens in HBM, 256 mixed draws, padded to
+    8192; then 256 draws without replacement, as the benchmark times them."""
     rbp = require_gpu()
     wl = wlm.WORKLOADS["stress"]
     tab = wlm.record_table(wl, 3)
@@ -158,11 +159,30 @@ def test_stress_million_records_padded():
     got = _run(rbp, ring, "pos_mix", "padded", 3, 11, wl.n_draw, p_q32=p, l_max=wl.l_max)
     idx = ob.sample_indices(tab.reward, ob.RB_POS_MIX, 3, 11, wl.n_draw, p)
     assert np.array_equal(got["idx"], np.array(idx, dtype=np.int32))
-    # oracle gather over a compact arena holding only the drawn records
-    uniq = sorted(set(idx))
+    _compare(got, _compact_gather(idx, tab, tok_d, old_d, adv, wl.l_max))
+    # the benchmark's draw without replacement on the same buffer (seed 3,
+    # step 0, padded): a radix select over all 10^6 slot keys
+    cfg = rbp.make_sample_cfg(rbp.RB_NO_REPLACE, rbp.RB_LAYOUT_PADDED, 3, 0, wl.n_draw,
+                              cur_version=tab.cur_version, l_max=wl.l_max)
+    out = rbp.alloc_batch(cfg)
+    print("[sampler] stress no_replace n_live=10^6 n_draw=256", flush=True)
+    rbp.rb_sample_gather(ring.rec, cfg, out, rbp.workspace(rbp.RBP_OP_SAMPLE_GATHER,
+                                                           ring.capacity))
+    torch.cuda.synchronize()
+    got = {k: to_np(v) for k, v in out.items()}
+    idx = ob.sample_without_replacement(3, 0, len(tab.length), wl.n_draw)
+    assert np.array_equal(got["idx"], np.array(idx, dtype=np.int32))
+    _compare(got, _compact_gather(idx, tab, tok_d, old_d, adv, wl.l_max))
+    del tok_d, old_d, out
+    torch.cuda.empty_cache()
+
+
+def _compact_gather(idx, tab, tok_d, old_d, adv, l_max):
+    """The oracle's padded gather over a compact arena holding only the drawn
+    records (the full arena is too large to copy to the host)."""
     c_off, chunks_t, chunks_o, at = {}, [], [], 0
-    for s in uniq:
-        a, n = int(tab.arena_off[s]), int(min(tab.length[s], wl.l_max))
+    for s in sorted(set(idx)):
+        a, n = int(tab.arena_off[s]), int(min(tab.length[s], l_max))
         chunks_t.append(to_np(tok_d[a:a + n]))
         chunks_o.append(to_np(old_d[a:a + n]))
         c_off[s] = at
@@ -170,11 +190,8 @@ def test_stress_million_records_padded():
     off2 = np.zeros(len(tab.length), dtype=np.int64)
     for s, o in c_off.items():
         off2[s] = o
-    want = ob.gather(idx, off2, tab.length, adv, tab.version, np.concatenate(chunks_t),
-                     np.concatenate(chunks_o), tab.cur_version, ob.LAYOUT_PADDED, l_max=wl.l_max)
-    _compare(got, want)
-    del tok_d, old_d
-    torch.cuda.empty_cache()
+    return ob.gather(idx, off2, tab.length, adv, tab.version, np.concatenate(chunks_t),
+                     np.concatenate(chunks_o), tab.cur_version, ob.LAYOUT_PADDED, l_max=l_max)
 
 
 def test_same_seed_step_reproduces_and_rejects_bad_args():
