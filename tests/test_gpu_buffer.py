@@ -281,3 +281,58 @@ def test_push_of_a_full_capacity_evicts_exactly_the_live_records():
     assert ev == [3, 2, 0, 0, 5] and ring.n_live == cap
     assert np.array_equal(to_np(ring.t["replay_hist"]), ob.histogram(ev, 4))
     assert np.all(to_np(ring.t["use_count"]) == 0) and np.all(to_np(ring.t["version"]) == 1)
+
+
+def test_push_long_records_and_note_use_at_full_capacity():
+    # records of up to 9000 tokens into 8192-token rows: the copy splits each
+    # row over 16 blocks that loop over it, and records past the row are cut
+    rbp = require_gpu()
+    cap, slot = 48, 8192
+    ring = rbp.make_ring(cap, slot)
+    fifo = ob.FifoBuffer(cap)
+    rng = np.random.default_rng(13)
+    for version, n in enumerate((20, 20, 20)):
+        lens = rng.integers(1, 9001, n).astype(np.int32)
+        src = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+        tok = rng.integers(0, 152064, int(lens.sum())).astype(np.int32)
+        old = rng.standard_normal(int(lens.sum())).astype(np.float32)
+        rew = (rng.random(n) < 0.4).astype(np.float32)
+        print(f"[buffer] long push n={n}", flush=True)
+        rbp.rb_push(ring, torch.tensor([0, n // 2, n], dtype=torch.int32, device="cuda"),
+                    torch.from_numpy(lens).cuda(), torch.from_numpy(src).cuda(),
+                    torch.from_numpy(rew).cuda(), version, torch.from_numpy(tok).cuda(),
+                    torch.from_numpy(old).cuda())
+        for i in range(n):
+            k = min(int(lens[i]), slot)
+            fifo.push({"tok": tok[src[i]:src[i] + k], "old": old[src[i]:src[i] + k]})
+    torch.cuda.synchronize()
+    t_tok, t_old = to_np(ring.t["arena_tokens"]), to_np(ring.t["arena_old_logp"])
+    t_len = to_np(ring.t["length"])
+    for s, want in enumerate(fifo.records):
+        r = (ring.head + s) % cap
+        n = len(want["tok"])
+        assert t_len[r] == n
+        assert np.array_equal(t_tok[r * slot:r * slot + n], want["tok"])
+        assert np.array_equal(t_old[r * slot:r * slot + n], want["old"])
+
+    # usage update at the stress buffer's capacity (10^6 rows, 256 draws with
+    # repeats, the head near the end of the ring)
+    cap2, head, n_live = 1_000_000, 999_000, 1_000_000
+    use = torch.zeros(cap2, dtype=torch.int32, device="cuda")
+    last = torch.full((cap2,), -1, dtype=torch.int64, device="cuda")
+    ws = rbp.workspace(rbp.RBP_OP_NOTE_USE, cap2)
+    batches = []
+    for step in (0, 4, 5):
+        idx = rng.integers(0, n_live, 256)
+        idx[:40] = idx[40:80]  # repeats inside the batch
+        since = torch.empty(256, dtype=torch.int32, device="cuda")
+        rbp.rb_note_use(torch.from_numpy(idx.astype(np.int32)).cuda(), head, cap2, step, use,
+                        last, since, ws)
+        torch.cuda.synchronize()
+        batches.append((step, idx.tolist()))
+        assert np.array_equal(to_np(since), ob.steps_since_last_use(batches)[-1])
+    counts = np.zeros(n_live, dtype=np.int64)
+    for _, ids in batches:
+        np.add.at(counts, ids, 1)
+    phys = (head + np.arange(n_live)) % cap2
+    assert np.array_equal(to_np(use)[phys], counts)

@@ -14,7 +14,7 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("G,n_groups,p", [(4, 16, 0.5), (8, 128, 0.4), (8, 4096, 0.3),
-                                          (16, 60, 0.5)])
+                                          (16, 60, 0.5), (8, 125_000, 0.4)])
 def test_group_advantage(G, n_groups, p):
     rbp = require_gpu()
     rng = np.random.default_rng(G * 1000 + n_groups)
