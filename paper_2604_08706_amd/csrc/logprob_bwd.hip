@@ -174,6 +174,31 @@ RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
   };
   auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
     const Tile tile = tile_of(vid);
+    if (accumulate && tile.n0 + 256 <= V && tile.m0 + 256 <= d) {
+      // interior tile: all 16 previous values of a column block are loaded
+      // before any of them is stored back, so the tile waits for memory
+      // twice rather than once per float4
+#pragma unroll
+      for (int ni = 0; ni < GL::NI; ++ni) {
+        float* row = dW + (int64_t)(tile.n0 + GL::col(ni)) * d + tile.m0;
+        float4 o[GL::MI * 4];
+#pragma unroll
+        for (int mi = 0; mi < GL::MI; ++mi)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg)
+            o[mi * 4 + rg] = *reinterpret_cast<const float4*>(row + GL::row(mi, rg * 4));
+#pragma unroll
+        for (int mi = 0; mi < GL::MI; ++mi)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            const float4 a = o[mi * 4 + rg];
+            *reinterpret_cast<float4*>(row + GL::row(mi, rg * 4)) =
+                make_float4(acc[mi][ni][rg * 4 + 0] + a.x, acc[mi][ni][rg * 4 + 1] + a.y,
+                            acc[mi][ni][rg * 4 + 2] + a.z, acc[mi][ni][rg * 4 + 3] + a.w);
+          }
+      }
+      return;
+    }
 #pragma unroll
     for (int ni = 0; ni < GL::NI; ++ni) {
       const int64_t v = tile.n0 + GL::col(ni);
