@@ -342,7 +342,8 @@ FusedWs carve_fused(void* base, int64_t Tc, int32_t d, int32_t V) {
 // two events that order it against the caller's stream.  It lets the second
 // half of the in-place rescale (HBM-bound) run beside the first half of the
 // dW product (MFMA-bound); both fit on a CU at once (dW: one 512-thread
-// workgroup, 128 KiB of LDS, ~200 VGPRs per lane; rescale: 40 VGPRs, no LDS).
+// workgroup, 128 KiB of LDS, 216 VGPRs per lane, two waves per SIMD; rescale:
+// 40 VGPRs, no LDS -- 2 x 216 + 40 <= 512).
 struct SideStream {
   hipStream_t stream = nullptr;
   hipEvent_t head_done = nullptr, tail_done = nullptr;

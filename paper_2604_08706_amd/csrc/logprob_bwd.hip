@@ -175,27 +175,31 @@ RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
   auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
     const Tile tile = tile_of(vid);
     if (accumulate && tile.n0 + 256 <= V && tile.m0 + 256 <= d) {
-      // interior tile: all 16 previous values of a column block are loaded
-      // before any of them is stored back, so the tile waits for memory
-      // twice rather than once per float4
+      // interior tile: the previous values are loaded eight float4 at a time
+      // before any of them is stored back, so the tile waits for memory four
+      // times rather than once per float4.  Eight, not sixteen: the kernel
+      // must stay within 232 VGPRs, so that a 40-VGPR wave of the rescale
+      // that the single pass runs beside it still fits on each SIMD.
 #pragma unroll
       for (int ni = 0; ni < GL::NI; ++ni) {
         float* row = dW + (int64_t)(tile.n0 + GL::col(ni)) * d + tile.m0;
-        float4 o[GL::MI * 4];
 #pragma unroll
-        for (int mi = 0; mi < GL::MI; ++mi)
+        for (int mh = 0; mh < GL::MI; mh += 2) {
+          float4 o[8];
 #pragma unroll
-          for (int rg = 0; rg < 4; ++rg)
-            o[mi * 4 + rg] = *reinterpret_cast<const float4*>(row + GL::row(mi, rg * 4));
+          for (int k = 0; k < 8; ++k)
+            o[k] = *reinterpret_cast<const float4*>(row + GL::row(mh + k / 4, (k % 4) * 4));
 #pragma unroll
-        for (int mi = 0; mi < GL::MI; ++mi)
-#pragma unroll
-          for (int rg = 0; rg < 4; ++rg) {
-            const float4 a = o[mi * 4 + rg];
+          for (int k = 0; k < 8; ++k) {
+            const int mi = mh + k / 4, rg = k % 4;
             *reinterpret_cast<float4*>(row + GL::row(mi, rg * 4)) =
-                make_float4(acc[mi][ni][rg * 4 + 0] + a.x, acc[mi][ni][rg * 4 + 1] + a.y,
-                            acc[mi][ni][rg * 4 + 2] + a.z, acc[mi][ni][rg * 4 + 3] + a.w);
+                make_float4(acc[mi][ni][rg * 4 + 0] + o[k].x, acc[mi][ni][rg * 4 + 1] + o[k].y,
+                            acc[mi][ni][rg * 4 + 2] + o[k].z, acc[mi][ni][rg * 4 + 3] + o[k].w);
           }
+          // keeps the next batch's loads below these stores (the compiler
+          // would otherwise hoist them all and hold 16 float4 at once)
+          asm volatile("" ::: "memory");
+        }
       }
       return;
     }
