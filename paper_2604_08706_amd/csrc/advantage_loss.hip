@@ -21,13 +21,35 @@ constexpr int kLossThreads = 256;
 constexpr int kLossMaxBlocks = 1024;
 constexpr int kNumSums = 5;  // -sum w*l, sum rho, n clipped, n valid, sum l
 
-__global__ void __launch_bounds__(64) group_advantage_kernel(
+constexpr int kAdvGroups = 256;   // groups per block, one thread each
+constexpr int kAdvStage = 4096;   // records a block stages through LDS
+
+// Block b takes groups [256 b, 256 b + 256), whose records form one
+// contiguous range.  When that range fits the stage, it is read into LDS and
+// the advantages written back with coalesced accesses (a thread per group
+// reading its own records from HBM makes a wave's loads 4 G bytes apart);
+// longer ranges take the direct path.  Same arithmetic either way.
+__global__ void __launch_bounds__(kAdvGroups) group_advantage_kernel(
     const float* __restrict__ reward, const int32_t* __restrict__ group_off,
     int32_t n_groups, int32_t ddof, float eps, float* __restrict__ adv) {
-  const int32_t g = blockIdx.x * 64 + threadIdx.x;
-  if (g >= n_groups) return;
-  rbp::group_advantage(reward, group_off[g], group_off[g + 1], ddof, eps,
-                       [&](int32_t i, float a) { adv[i] = a; });
+  __shared__ float r_s[kAdvStage], a_s[kAdvStage];
+  const int32_t g0 = blockIdx.x * kAdvGroups;
+  const int32_t g1 = g0 + kAdvGroups < n_groups ? g0 + kAdvGroups : n_groups;
+  const int32_t g = g0 + threadIdx.x;
+  const int32_t lo = group_off[g0], n = group_off[g1] - lo;
+  if (n > kAdvStage) {
+    if (g < g1)
+      rbp::group_advantage(reward, group_off[g], group_off[g + 1], ddof, eps,
+                           [&](int32_t i, float a) { adv[i] = a; });
+    return;
+  }
+  for (int32_t k = threadIdx.x; k < n; k += kAdvGroups) r_s[k] = reward[lo + k];
+  __syncthreads();
+  if (g < g1)
+    rbp::group_advantage(r_s, group_off[g] - lo, group_off[g + 1] - lo, ddof, eps,
+                         [&](int32_t i, float a) { a_s[i] = a; });
+  __syncthreads();
+  for (int32_t k = threadIdx.x; k < n; k += kAdvGroups) adv[lo + k] = a_s[k];
 }
 
 constexpr int kSeqThreads = 256;  // threads per sequence of the whole-sequence ratio
@@ -309,8 +331,9 @@ extern "C" int rb_group_advantage(const float* reward, const int32_t* group_off,
   RBP_REQUIRE(ddof == 0 || ddof == 1, RBP_EINVAL, "rb_group_advantage: ddof must be 0 or 1");
   RBP_REQUIRE(eps >= 0.0f, RBP_EINVAL, "rb_group_advantage: eps < 0");
   if (n_groups == 0) return RBP_OK;
-  hipLaunchKernelGGL(group_advantage_kernel, dim3((n_groups + 63) / 64), dim3(64), 0,
-                     rbp::as_stream(stream), reward, group_off, n_groups, ddof, eps, adv);
+  hipLaunchKernelGGL(group_advantage_kernel, dim3(rbp::ceil_div(n_groups, kAdvGroups)),
+                     dim3(kAdvGroups), 0, rbp::as_stream(stream), reward, group_off, n_groups,
+                     ddof, eps, adv);
   RBP_CHECK_LAUNCH("rb_group_advantage");
   return RBP_OK;
 }

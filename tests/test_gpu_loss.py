@@ -128,3 +128,18 @@ def test_loss_empty_batch_adds_nothing():
                             rbp.workspace(rbp.RBP_OP_LOSS, 0))
     torch.cuda.synchronize()
     assert to_np(loss)[0] == 0.25 and np.all(to_np(stats) == 2.0)
+
+
+def test_group_advantage_large_groups_take_the_direct_path():
+    # groups of 40..80 records: a block's 256 groups then span more records
+    # than its LDS stage holds, so those blocks read the rewards directly; the
+    # last block holds few groups and is staged
+    rbp = require_gpu()
+    rng = np.random.default_rng(11)
+    sizes = rng.integers(40, 81, 600)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    rewards = (rng.random(int(off[-1])) < 0.5).astype(np.float32)
+    adv = torch.empty(int(off[-1]), dtype=torch.float32, device="cuda")
+    rbp.rb_group_advantage(torch.from_numpy(rewards).cuda(), torch.from_numpy(off).cuda(), adv)
+    want = np.array(group_advantage(rewards, off))
+    assert np.allclose(to_np(adv), want, rtol=1e-5, atol=1e-6)
