@@ -31,9 +31,12 @@ def group_advantage(rewards, group_off, ddof=1, eps=1e-6):
         n = hi - lo
         if n <= 0:
             continue
+        # identical rewards have std 0 by definition; decided on the rewards
+        # themselves, since the fp64 mean of e.g. three 0.7s is not 0.7
+        equal = all(float(rewards[i]) == float(rewards[lo]) for i in range(lo, hi))
         mean = sum(float(rewards[i]) for i in range(lo, hi)) / n
         ss = sum((float(rewards[i]) - mean) ** 2 for i in range(lo, hi))
-        if ss == 0.0 or n - ddof <= 0:
+        if equal or ss == 0.0 or n - ddof <= 0:
             # identical rewards (or no degrees of freedom): no signal
             for i in range(lo, hi):
                 adv[i] = 0.0

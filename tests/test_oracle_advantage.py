@@ -61,3 +61,37 @@ def test_affine_invariance_of_rewards():
     base = group_advantage(r, [0, 16], eps=0.0)
     moved = group_advantage(3.0 * r + 7.0, [0, 16], eps=0.0)
     assert np.allclose(base, moved, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("G", [2, 3, 4, 7, 8, 16])
+@pytest.mark.parametrize("r", [0.7, 0.1, 1.0 / 3.0, -2.5, float(np.float32(0.7))])
+def test_equal_non_binary_rewards_are_exactly_zero(G, r):
+    # identical rewards have std 0 whatever their binary expansion: the fp64
+    # mean of three 0.7s is not 0.7, so the decision cannot rest on the spread
+    assert group_advantage([r] * G, [0, G]) == [0.0] * G
+    assert group_advantage([r] * G, [0, G], ddof=0) == [0.0] * G
+
+
+@pytest.mark.parametrize("G", [2, 4, 8, 16])
+@pytest.mark.parametrize("x, ulps", [(0.7, 1), (0.1, 3), (1.0 / 3.0, 1000), (5.0, 2 ** 20)])
+def test_one_outlier_closed_form(G, x, ulps):
+    # G - 1 rewards x and one x + delta: mean x + delta/G, deviations
+    # -delta/G and delta (G-1)/G, sample std |delta| / sqrt(G).  Evaluated in
+    # exact rationals from the two floats, so eps matters when delta is a few
+    # ulps of x (std ~ 1e-16 against eps = 1e-6).
+    from fractions import Fraction
+    import math as m
+
+    y = float(np.nextafter(np.float32(x), np.float32(np.inf)))  # keep in fp32 range
+    for _ in range(ulps - 1):
+        y = float(np.nextafter(np.float32(y), np.float32(np.inf)))
+    x = float(np.float32(x))
+    delta = Fraction(y) - Fraction(x)
+    eps = 1e-6
+    std = float(abs(delta)) / m.sqrt(G)
+    hi = float(delta * (G - 1) / G) / (std + eps)
+    lo = float(-delta / G) / (std + eps)
+    adv = group_advantage([x] * (G - 1) + [y], [0, G], ddof=1, eps=eps)
+    assert adv[-1] == pytest.approx(hi, rel=1e-9)
+    for a in adv[:-1]:
+        assert a == pytest.approx(lo, rel=1e-9)
