@@ -204,8 +204,9 @@ int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
  * Group-normalised advantage at insert time (App. D.2):
  * A_i = (r_i - mean_g) / (std_g + eps) over group g = [group_off[g],
  * group_off[g+1]); std uses `ddof` (1 = sample estimate); a group whose rewards
- * are all equal (or has no degrees of freedom) gets A = 0.  fp32 arithmetic.
- * reward, group_off, adv: device.  Groups must be non-overlapping, ascending.
+ * are all equal (or has no degrees of freedom) gets A = 0 exactly.  The
+ * mean, std and quotient are formed in fp64 (fp32 inputs sum exactly there),
+ * then A is rounded to fp32.  reward, group_off, adv: device fp32 / int32.  Groups must be non-overlapping, ascending.
  * Errors: RBP_EINVAL for null pointers, n_groups < 0, ddof not 0 or 1, eps < 0.
  */
 int rb_group_advantage(const float* reward, const int32_t* group_off,
@@ -285,7 +286,8 @@ int policy_loss_seq_fwd_bwd(const float* logp, const float* old_logp,
  * (records [group_off[g], group_off[g+1])),
  *   coef_i = reward_i - (mean reward of the group + delta_v),
  * the paper's delta_v being -0.1.  Stored in the record table's advantage
- * slot when training with policy_asymre_fwd_bwd.  reward, coef device fp32;
+ * slot when training with policy_asymre_fwd_bwd.  Formed in fp64, rounded
+ * to fp32 once.  reward, coef device fp32;
  * group_off device int32 [n_groups + 1].
  * Errors: RBP_EINVAL (null pointers, n_groups < 0).
  */

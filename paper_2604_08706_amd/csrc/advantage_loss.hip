@@ -166,10 +166,12 @@ __global__ void __launch_bounds__(64) asymre_coef_kernel(const float* __restrict
   if (g >= n_groups) return;
   const int32_t lo = group_off[g], hi = group_off[g + 1];
   if (hi <= lo) return;
-  float sum = 0.0f;
-  for (int32_t i = lo; i < hi; ++i) sum += reward[i];
-  const float base = sum / (float)(hi - lo) + delta_v;
-  for (int32_t i = lo; i < hi; ++i) coef[i] = reward[i] - base;
+  // fp64 as in the group advantage: the group mean of fp32 rewards is exact,
+  // so equal rewards give coef = -delta_v exactly; one rounding at the end.
+  double sum = 0.0;
+  for (int32_t i = lo; i < hi; ++i) sum += (double)reward[i];
+  const double base = sum / (double)(hi - lo) + (double)delta_v;
+  for (int32_t i = lo; i < hi; ++i) coef[i] = (float)((double)reward[i] - base);
 }
 
 // AsymRE per token: dlogp = -c / n_seq; sums {-sum c logp / n_seq, valid, sum c logp}

@@ -189,6 +189,39 @@ def test_push_is_fifo_with_advantages_at_insert():
                     torch.zeros(1, dtype=torch.int32, device="cuda"), torch.zeros(1, device="cuda"))
 
 
+def test_push_equal_non_binary_groups_store_zero_advantage():
+    # the push computes advantages at insert with the same helper as
+    # rb_group_advantage: groups of equal rewards such as 0.7 store exact zeros
+    rbp = require_gpu()
+    G_list = [4, 8, 16, 4, 8, 16, 8]
+    vals = [0.1, 0.7, 1.0 / 3.0, 0.3, 0.7, 0.1, None]
+    rew = []
+    for G, x in zip(G_list, vals):
+        if x is None:  # one near-equal group: a member one ulp above the rest
+            g = np.full(G, 0.7, dtype=np.float32)
+            g[3] = np.nextafter(g[3], np.float32(np.inf))
+        else:
+            g = np.full(G, x, dtype=np.float32)
+        rew.append(g)
+    rew = np.concatenate(rew)
+    n = len(rew)
+    goff = np.concatenate([[0], np.cumsum(G_list)]).astype(np.int32)
+    lens = np.ones(n, np.int32)
+    ring = rbp.make_ring(n + 5, 2)
+    print(f"[buffer] push of {len(G_list)} equal/near-equal groups", flush=True)
+    rbp.rb_push(ring, torch.from_numpy(goff).cuda(), torch.from_numpy(lens).cuda(),
+                torch.arange(n, dtype=torch.int64, device="cuda"), torch.from_numpy(rew).cuda(),
+                1, torch.zeros(n, dtype=torch.int32, device="cuda"),
+                torch.zeros(n, device="cuda"))
+    torch.cuda.synchronize()
+    got = to_np(ring.t["advantage"])[(ring.head + np.arange(n)) % (n + 5)]
+    want = np.array(group_advantage(rew, goff))
+    k = goff[-2]
+    assert np.all(got[:k] == 0.0) and np.all(want[:k] == 0.0)
+    assert np.all(want[k:] != 0.0)
+    assert np.allclose(got[k:], want[k:], rtol=1e-6, atol=1e-12)
+
+
 @pytest.mark.parametrize("n,n_bins,lo", [(0, 3, 0), (1, 1, 0), (1000, 7, -1), (300_000, 4096, 5),
                                          (300_000, 33, -1)])
 def test_hist_accumulate_matches_oracle(n, n_bins, lo):

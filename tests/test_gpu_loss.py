@@ -47,6 +47,49 @@ def test_group_advantage_ragged_and_real_valued():
     assert np.allclose(to_np(adv), want, rtol=1e-4, atol=1e-5)
 
 
+def _equal_and_near_equal_groups(seed):
+    """Groups of G = 4, 8, 16 rewards: all equal to 0.1, 0.7, 1/3 (not exact in
+    binary, so an fp32 mean leaves r - mean != 0), and near-equal groups with
+    one or two members a few fp32 ulps away."""
+    rng = np.random.default_rng(seed)
+    groups, equal = [], []
+    for G in (4, 8, 16):
+        for x in (0.1, 0.7, 1.0 / 3.0, 0.3, 2.2):
+            groups.append(np.full(G, x, dtype=np.float32))
+            equal.append(True)
+            g = np.full(G, x, dtype=np.float32)
+            for j in rng.choice(G, int(rng.integers(1, 3)), replace=False):
+                step = int(rng.integers(1, 6))
+                for _ in range(step):
+                    g[j] = np.nextafter(g[j], np.float32(np.inf))
+            groups.append(g)
+            equal.append(False)
+    rewards = np.concatenate(groups)
+    off = np.concatenate([[0], np.cumsum([len(g) for g in groups])]).astype(np.int32)
+    return rewards, off, np.array(equal)
+
+
+def test_group_advantage_equal_and_near_equal_non_binary():
+    rbp = require_gpu()
+    rewards, off, equal = _equal_and_near_equal_groups(11)
+    print(f"[advantage] equal/near-equal groups={len(off) - 1}", flush=True)
+    for ddof in (1, 0):
+        adv = torch.full((len(rewards),), 77.0, dtype=torch.float32, device="cuda")
+        rbp.rb_group_advantage(torch.from_numpy(rewards).cuda(), torch.from_numpy(off).cuda(),
+                               adv, ddof=ddof, eps=1e-6)
+        got = to_np(adv)
+        want = np.array(group_advantage(rewards, off, ddof=ddof, eps=1e-6))
+        for g in range(len(off) - 1):
+            a, w = got[off[g]:off[g + 1]], want[off[g]:off[g + 1]]
+            if equal[g]:
+                assert np.all(a == 0.0) and np.all(w == 0.0), (g, a)
+            else:
+                # one fp32 rounding of an fp64 result: well inside rtol 1e-5
+                # (a member that equals the group mean gets 0 on both sides)
+                assert np.any(w != 0.0)
+                assert np.allclose(a, w, rtol=1e-6, atol=1e-12), (g, a, w)
+
+
 def _loss_case(T, B, seed, noise, margin=1e-3):
     rng = np.random.default_rng(seed)
     lens = rng.integers(1, max(2, 2 * T // B), B)
