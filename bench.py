@@ -1,20 +1,27 @@
 """Replayed-token throughput of the replay hot path on one MI355X.
 
 One step = the whole trainer-side path over one replay micro-batch:
-  rb_group_advantage  (advantages of the buffer's groups, as at insert)
-  rb_sample_gather    (uniform draws from a 1024-record FIFO buffer, packed
-                       into a 16384-token micro-batch)
-  policy_logprob_fwd  (hidden [16384, 3584] x W [152064, 3584], bf16 MFMA,
-                       online log-sum-exp)
-  policy_loss_fwd_bwd (clipped GRPO, token ratios, group advantages)
-  policy_logprob_bwd  (dhidden and dW, dW accumulated as over micro-batches)
-Inputs are synthetic (seeded), shaped like Qwen2.5-7B's LM head and the
-paper's rollout length mix; hidden states stand in for the model trunk's
-output.  All inputs are resident in HBM before timing starts.
+  rb_group_advantage    (advantages of the buffer's groups, as at insert)
+  rb_sample_gather      (uniform draws from a 1024-record FIFO buffer, packed
+                         into a 16384-token micro-batch)
+  policy_fused_fwd_bwd  (one pass: logits hidden [16384, 3584] x W [152064,
+                         3584] in bf16 MFMA tiles with the log-sum-exp and
+                         exp(z - M) kept per tile, the clipped GRPO loss with
+                         token ratios and group advantages, and the backward
+                         to dhidden and dW, dW accumulated as over
+                         micro-batches; 6 d V flop per token)
+`value` is this step's throughput.  Reported beside it: the four-call step
+(policy_logprob_fwd + policy_loss_fwd_bwd + policy_logprob_bwd, whose
+backward recomputes the logits: 8 d V flop per token), and both paths with a
+workspace bounded to 4096-token chunks.  Inputs are synthetic (seeded),
+shaped like Qwen2.5-7B's LM head and the paper's rollout length mix; hidden
+states stand in for the model trunk's output.  All inputs are resident in HBM
+before timing starts.
 
 Prints one JSON line (metric: replayed tokens/s; also the fraction of the
-MI355X dense bf16 MFMA peak, a roofline record for the dominant kernel, and
-the CPU oracle timed on a bounded sample).
+MI355X dense bf16 MFMA peak, per-phase times from the call's own events, a
+roofline record for the product that takes the most time per step, and the
+CPU oracle timed on a bounded sample).
 """
 
 import argparse
@@ -29,19 +36,22 @@ PEAK_BF16 = 2.5e15        # MI355X dense bf16 MFMA, FLOP/s
 PEAK_HBM = 8.0e12         # MI355X HBM3E, B/s
 ROOT = os.path.dirname(os.path.abspath(__file__))
 
-# HBM traffic of one policy_logprob_fwd call at the 16384-token micro-batch
-# (d=3584, V=152064): FETCH_SIZE and WRITE_SIZE per dispatch from two
-# rocprofv3 --pmc passes over this script, scaled by what the same counters
-# read for a plain copy of known size (--copy-probe-mib: a 1 GiB copy reads
-# 524302 KiB of FETCH_SIZE, factor 2.0, and 1048576 KiB of WRITE_SIZE, factor
-# 1.0).  Only valid for the sources the counters were read on.
-TRAFFIC_SOURCES = ("logprob_fwd.hip", "logits_epilogue.h", "gemm_core.h", "gemm_dma.h")
-TRAFFIC = {
-    "sources_sha256": "74be3da0398d2c050fc75bbdc4a6edc2e8c77e272754abee17e5e653457de83f",
-    "fetch_bytes": {"logits_lse_partial_kernel": 28308226048,   # 13822376 KiB x 2.0
-                    "lse_merge_kernel": 391094955},             # 190964 KiB x 2.0
-    "write_bytes": {"logits_lse_partial_kernel": 155713536,     # 152064 KiB
-                    "lse_merge_kernel": 328363},                # 320.7 KiB
+# HBM traffic per step of each product of the single pass at the 16384-token
+# micro-batch (d=3584, V=152064): FETCH_SIZE and WRITE_SIZE per dispatch from
+# two rocprofv3 --pmc passes over this script, scaled by what the same
+# counters read for a plain copy of known size (--copy-probe-mib), summed over
+# a product's launches in one step.  Only valid for the sources the counters
+# were read on (None until they are).
+TRAFFIC_SOURCES = ("fused.hip", "logprob_bwd.hip", "logits_epilogue.h", "gemm_core.h",
+                   "gemm_dma.h", "advantage_loss.hip")
+TRAFFIC = None
+
+# the three products of the single pass, by the phase that times them
+PRODUCTS = {
+    "logits": "logits_store_kernel (forward product; stores exp(z - M) as bf16)",
+    "dW": "dweight_kernel (dW product: two launches, the side stream's rescale beside "
+          "the first)",
+    "dhidden": "dhidden_kernel + add_f32_kernel (dhidden product, split-K 2)",
 }
 
 
@@ -57,8 +67,12 @@ def parse():
     ap.add_argument("--no-aux", action="store_true",
                     help="skip the HBM-rate measurement of sample+gather and loss on the "
                          "10^6-record stress buffer")
-    ap.add_argument("--no-fused", action="store_true",
-                    help="skip the separately reported single-pass policy_fused_fwd_bwd leg")
+    ap.add_argument("--no-four-call", action="store_true",
+                    help="skip the separately reported four-call leg")
+    ap.add_argument("--no-bounded", action="store_true",
+                    help="skip the bounded-workspace legs (both paths in chunks)")
+    ap.add_argument("--bounded-tokens", type=int, default=4096,
+                    help="token chunk the bounded-workspace legs size their workspace for")
     ap.add_argument("--blas-probe", action="store_true",
                     help="only time the vendor library's plain bf16 GEMM on the forward's "
                          "shape (W [V, d] x hidden^T [d, T], torch.mm) as a practical "
@@ -133,12 +147,12 @@ def sources_sha256():
     return h.hexdigest()
 
 
-def traffic_bytes():
-    """HBM bytes per forward call, or None once the kernel sources differ
-    from the ones the counters were read on."""
+def traffic_bytes(product):
+    """HBM bytes per step of one product of the single pass, or None when
+    not measured on the current kernel sources."""
     if TRAFFIC is None or TRAFFIC["sources_sha256"] != sources_sha256():
         return None
-    return sum(TRAFFIC["fetch_bytes"].values()) + sum(TRAFFIC["write_bytes"].values())
+    return TRAFFIC["bytes"].get(product)
 
 
 def setup(wl, seed=0):
@@ -210,24 +224,29 @@ def align_old_logp(rbp, wl, S, steps, noise_sd, seed=0):
     torch.cuda.synchronize()
 
 
-def run_step(rbp, wl, S, step, out, ev=None):
+def run_step(rbp, wl, S, step, out, ev=None, ws_bwd=None):
+    """The four-call step.  ev: 5 timing events (step start, after the
+    sampler, after the forward, after the loss, after the backward)."""
+    if ev is not None:
+        ev[0].record()
     rbp.rb_group_advantage(S["rewards"], S["group_off"], S["adv_rec"])
     rbp.rb_sample_gather(S["rec"], cfg_for(rbp, wl, step), out, S["ws_sample"])
     if ev is not None:
-        ev[0].record()
+        ev[1].record()
     rbp.policy_logprob_fwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"], S["logp"],
                            S["lse"], S["ws_fwd"])
     if ev is not None:
-        ev[1].record()
+        ev[2].record()
     rbp.policy_loss_fwd_bwd(S["logp"], out["old_logp"], out["seq_of_token"], out["adv"],
                             out["len"], wl.n_draw, S["loss"], S["dlogp"], S["stats"],
                             S["ws_loss"])
     if ev is not None:
-        ev[2].record()
-    rbp.policy_logprob_bwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"], S["lse"],
-                           S["dlogp"], S["dh"], S["dW"], S["ws_bwd"], accumulate_dW=True)
-    if ev is not None:
         ev[3].record()
+    rbp.policy_logprob_bwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"], S["lse"],
+                           S["dlogp"], S["dh"], S["dW"], S["ws_bwd"] if ws_bwd is None else ws_bwd,
+                           accumulate_dW=True)
+    if ev is not None:
+        ev[4].record()
 
 
 def aux_stress(iters=20):
@@ -511,55 +530,106 @@ def cpu_sampler_stress(seed=3):
             "sample": f"{wl.n_draw} draws from {n} records, padded [{wl.n_draw}, {wl.l_max}]"}
 
 
-def run_step_fused(rbp, wl, S, step, out, ev=None):
+def run_step_fused(rbp, wl, S, step, out, ex, ev0=None):
     """The same step through policy_fused_fwd_bwd (forward, loss, backward and
-    entropy in one call; keeps T x V exp(z - max) in its workspace)."""
+    entropy in one call).  ev0: an event recorded at the step start; the
+    phase events of the call, if any, are in ex."""
+    if ev0 is not None:
+        ev0.record()
     rbp.rb_group_advantage(S["rewards"], S["group_off"], S["adv_rec"])
     rbp.rb_sample_gather(S["rec"], cfg_for(rbp, wl, step), out, S["ws_sample"])
-    if ev is not None:
-        ev[0].record()
     rbp.policy_fused_fwd_bwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"],
                              out["old_logp"], out["adv"], out["len"], wl.n_draw, S["logp"],
                              S["lse"], S["entropy"], S["loss"], S["dlogp"], S["stats"], S["dh"],
-                             S["dW"], S["ws_fused"], accumulate_dW=True)
-    if ev is not None:
-        ev[1].record()
+                             S["dW"], S["ws_fused"], accumulate_dW=True, exec=ex)
 
 
-def fused_leg(rbp, wl, S, out, first_step, steps, warmup):
-    """Time the single-pass path on the same sampled batches as the main loop."""
+def tokens_of_steps(rbp, wl, S, out, steps):
+    """Valid tokens each step's draw packs (untimed: a draw depends only on
+    the seed and the step number)."""
+    n = []
+    for k in steps:
+        rbp.rb_sample_gather(S["rec"], cfg_for(rbp, wl, k), out, S["ws_sample"])
+        n.append(int(out["n_tokens"].item()))
+    return n
+
+
+def spread(xs):
+    return {"min": round(float(np.min(xs)), 3), "median": round(float(np.median(xs)), 3),
+            "max": round(float(np.max(xs)), 3)}
+
+
+PHASES = ("logits", "merge", "loss", "scale", "dW", "dhidden")
+
+
+def fused_leg(rbp, wl, S, out, first_step, steps, warmup, ws_tokens=None):
+    """Time the single pass over `steps` sampled batches (after `warmup`),
+    with the rescale overlapped on a side stream and the call's phase events
+    recorded on the caller's stream.  ws_tokens: size the workspace for that
+    many tokens (the call then runs in chunks)."""
     import torch
 
-    S["entropy"] = torch.empty(S["T"], device="cuda")
-    S["ws_fused"] = rbp.workspace(rbp.RBP_OP_FUSED, S["T"], wl.d, wl.V)
+    T = S["T"]
+    S["entropy"] = torch.empty(T, device="cuda")
+    S["ws_fused"] = rbp.workspace(rbp.RBP_OP_FUSED, ws_tokens or T, wl.d, wl.V)
+    ovl = rbp.Overlap()
     for k in range(warmup):
-        run_step_fused(rbp, wl, S, first_step + k, out)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        run_step_fused(rbp, wl, S, first_step + k, out, ovl.exec())
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(1 + rbp.RBP_NUM_PHASES)]
+          for _ in range(steps)]
+    exs = [ovl.exec(e[1:]) for e in ev]  # creates the events before timing
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for i in range(steps):
-        run_step_fused(rbp, wl, S, first_step + warmup + i, out, evs[i])
+        run_step_fused(rbp, wl, S, first_step + warmup + i, out, exs[i], ev[i][0])
     stop.record()
     torch.cuda.synchronize()
-    ms_step = start.elapsed_time(stop) / steps
-    n_valid = int(out["n_tokens"].item())
-    med = float(np.median([e[0].elapsed_time(e[1]) for e in evs]))
-    dV = wl.d * wl.V
+    ms_total = start.elapsed_time(stop)
+    timed = range(first_step + warmup, first_step + warmup + steps)
+    n_tok = tokens_of_steps(rbp, wl, S, out, timed)
+    step_ms = [e[0].elapsed_time(ev[i + 1][0]) for i, e in enumerate(ev[:-1])]
+    step_ms.append(ev[-1][0].elapsed_time(stop))
+    # phase k ends at phase event k + 1 (event list index k + 2)
+    ph = {name: float(np.mean([e[k + 1].elapsed_time(e[k + 2]) for e in ev]))
+          for k, name in enumerate(PHASES)}
+    call_ms = [e[1].elapsed_time(e[-1]) for e in ev]
     del S["ws_fused"]
     torch.cuda.empty_cache()
-    return {
-        "entry": "policy_fused_fwd_bwd (stores T x V exp(z - max) in bf16; "
-                 "not the headline, whose forward never materialises T x V)",
-        "tokens_per_s": round(n_valid / (ms_step / 1e3), 1),
-        "ms_per_step": round(ms_step, 3),
-        "median_ms_fwd_loss_bwd": round(med, 3),
-        "tokens_per_s_median_fwd_loss_bwd": round(n_valid / (med / 1e3), 1),
-        "mfma_peak_frac_6dV": round(n_valid / (ms_step / 1e3) * 6 * dV / PEAK_BF16, 4),
-        "steps": steps,
-        "warmup": warmup,
-    }
+    return {"ms_total": ms_total, "n_tok": n_tok, "step_ms": step_ms, "phase_ms": ph,
+            "call_ms": call_ms, "Tc": ws_tokens or T}
+
+
+def four_leg(rbp, wl, S, out, first_step, steps, warmup, ws_tokens=None):
+    """Time the four-call step (forward, loss, recomputing backward)."""
+    import torch
+
+    T = S["T"]
+    ws_bwd = rbp.workspace(rbp.RBP_OP_LOGPROB_BWD, ws_tokens or T, wl.d, wl.V)
+    for k in range(warmup):
+        run_step(rbp, wl, S, first_step + k, out, ws_bwd=ws_bwd)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(steps):
+        run_step(rbp, wl, S, first_step + warmup + i, out, ev[i], ws_bwd=ws_bwd)
+    stop.record()
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    n_tok = tokens_of_steps(rbp, wl, S, out, range(first_step + warmup,
+                                                   first_step + warmup + steps))
+    step_ms = [e[0].elapsed_time(ev[i + 1][0]) for i, e in enumerate(ev[:-1])]
+    step_ms.append(ev[-1][0].elapsed_time(stop))
+    ph = {"fwd": float(np.mean([e[1].elapsed_time(e[2]) for e in ev])),
+          "loss": float(np.mean([e[2].elapsed_time(e[3]) for e in ev])),
+          "bwd": float(np.mean([e[3].elapsed_time(e[4]) for e in ev]))}
+    del ws_bwd
+    torch.cuda.empty_cache()
+    return {"ms_total": ms_total, "n_tok": n_tok, "step_ms": step_ms, "phase_ms": ph,
+            "Tc": ws_tokens or T}
 
 
 def main():
@@ -584,73 +654,99 @@ def main():
         raise SystemExit("bench workload must use the packed layout")
     S = setup(wl)
     T = S["T"]
-    steps = list(range((args.warmup + args.steps) * (1 if args.no_fused else 2)))
-    align_old_logp(rbp, wl, S, steps, wl.noise_sd)
-    cfg0 = cfg_for(rbp, wl, 0)
-    out = rbp.alloc_batch(cfg0)
-    for k in range(args.warmup):
-        run_step(rbp, wl, S, k, out)
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    start.record()
-    for i in range(args.steps):
-        run_step(rbp, wl, S, args.warmup + i, out, evs[i])
-    stop.record()
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_total = start.elapsed_time(stop)
-    ms_step = ms_total / args.steps
-    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    loss_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    n_valid = int(out["n_tokens"].item())
-    # forward + loss + backward only (the sampler excluded), median over steps
-    k24_ms = float(np.median([e[0].elapsed_time(e[3]) for e in evs]))
-    tok_s = n_valid * args.steps / (ms_total / 1e3)
+    K, Wm = args.steps, args.warmup
+    n_legs = 2 + (0 if args.no_four_call else 1) + (0 if args.no_bounded else 2)
+    align_old_logp(rbp, wl, S, range(n_legs * (K + Wm)), wl.noise_sd)
+    out = rbp.alloc_batch(cfg_for(rbp, wl, 0))
     dV = wl.d * wl.V
+    prod_flop = 2.0 * T * dV  # one product over the micro-batch (the tail tokens pad to 0)
+
+    # headline: the single pass
+    t_wall = time.perf_counter()
+    f = fused_leg(rbp, wl, S, out, 0, K, Wm)
+    t_wall = time.perf_counter() - t_wall
+    tok = float(np.sum(f["n_tok"]))
+    tok_s = tok / (f["ms_total"] / 1e3)
     frac = tok_s * 6 * dV / PEAK_BF16
-    fwd_flops = 2.0 * T * dV
+    ph = f["phase_ms"]
+    # the three products; the dW phase holds its two launches and, beside the
+    # first, the side stream's part of the rescale
+    products = {k: ph[k] for k in PRODUCTS}
+    dom = max(products, key=products.get)
+    dom_ms = products[dom]
+    tb = traffic_bytes(dom)
     rec = {
         "metric": "replayed tokens/sec (fwd+bwd logprob+loss) at 7B shape; % bf16 MFMA peak",
         "value": round(tok_s, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 3),
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": round(f["ms_total"] / K, 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded; Qwen2.5-7B-shaped LM head, log-normal rollout lengths)",
         "config": {"workload": f"{wl.name}: packed micro-batch of {T} replayed tokens, "
-                               f"d={wl.d}, V={wl.V}, buffer {wl.n_records} records",
-                   "tokens_per_step": n_valid, "d": wl.d, "V": wl.V},
+                               f"d={wl.d}, V={wl.V}, buffer {wl.n_records} records; "
+                               "single-pass entry policy_fused_fwd_bwd (one chunk)",
+                   "tokens_per_step_mean": round(tok / K, 1), "d": wl.d, "V": wl.V},
         "mfma_peak_frac_6dV": round(frac, 4),
-        "mfma_peak_frac_8dV_executed": round(tok_s * 8 * dV / PEAK_BF16, 4),
-        "median_ms_fwd_loss_bwd": round(k24_ms, 3),
-        "tokens_per_s_median_fwd_loss_bwd": round(n_valid / (k24_ms / 1e3), 1),
-        "phase_ms": {"fwd": round(fwd_ms, 3), "loss": round(loss_ms, 3),
-                     "bwd": round(bwd_ms, 3),
-                     "sample+adv+rest": round(ms_step - fwd_ms - loss_ms - bwd_ms, 3)},
+        "step_ms": spread(f["step_ms"]),
+        "call_ms": spread(f["call_ms"]),
+        "phase_ms": {k: round(v, 3) for k, v in ph.items()},
+        "product_frac": {k: round(prod_flop / (v / 1e3) / PEAK_BF16, 4)
+                         for k, v in products.items()},
         "roofline": {
-            "kernel": "policy_logprob_fwd (logits_lse_partial_kernel + lse_merge_kernel)",
+            "kernel": PRODUCTS[dom],
             "bound": "mfma",
-            "achieved": round(fwd_flops / (fwd_ms / 1e3) / 1e12, 2),
+            "achieved": round(prod_flop / (dom_ms / 1e3) / 1e12, 2),
             "peak": PEAK_BF16 / 1e12,
             "unit": "TFLOP/s",
-            "frac": round(fwd_flops / (fwd_ms / 1e3) / PEAK_BF16, 4),
-            "traffic": traffic_bytes(),
+            "frac": round(prod_flop / (dom_ms / 1e3) / PEAK_BF16, 4),
+            "traffic": tb,
         },
         "wall_s_timed": round(t_wall, 3),
     }
-    if not args.no_fused:
-        rec["fused_single_pass"] = fused_leg(rbp, wl, S, out, args.warmup + args.steps,
-                                             args.steps, args.warmup)
+    step0 = K + Wm
+    if not args.no_four_call:
+        g = four_leg(rbp, wl, S, out, step0, K, Wm)
+        step0 += K + Wm
+        g_tok_s = float(np.sum(g["n_tok"])) / (g["ms_total"] / 1e3)
+        g_bwd = g["phase_ms"]["bwd"]
+        rec["four_call"] = {
+            "entries": "policy_logprob_fwd + policy_loss_fwd_bwd + policy_logprob_bwd "
+                       "(the forward keeps logits in registers; the backward recomputes them)",
+            "tokens_per_s": round(g_tok_s, 1),
+            "ms_per_step": round(g["ms_total"] / K, 3),
+            "mfma_peak_frac_6dV": round(g_tok_s * 6 * dV / PEAK_BF16, 4),
+            "mfma_peak_frac_8dV_executed": round(g_tok_s * 8 * dV / PEAK_BF16, 4),
+            "step_ms": spread(g["step_ms"]),
+            "phase_ms": {k: round(v, 3) for k, v in g["phase_ms"].items()},
+            "fwd_frac": round(prod_flop / (g["phase_ms"]["fwd"] / 1e3) / PEAK_BF16, 4),
+            "bwd_frac_4dV": round(2 * prod_flop / (g_bwd / 1e3) / PEAK_BF16, 4),
+        }
+    if not args.no_bounded:
+        Tc = args.bounded_tokens
+        bf = fused_leg(rbp, wl, S, out, step0, K, Wm, ws_tokens=Tc)
+        step0 += K + Wm
+        bg = four_leg(rbp, wl, S, out, step0, K, Wm, ws_tokens=Tc)
+        step0 += K + Wm
+        b_tok = float(np.sum(bf["n_tok"])) / (bf["ms_total"] / 1e3)
+        g_tok = float(np.sum(bg["n_tok"])) / (bg["ms_total"] / 1e3)
+        rec["bounded_workspace"] = {
+            "chunk_tokens": Tc,
+            "single_pass": {
+                "workspace_bytes": rbp.rbp_workspace_bytes(rbp.RBP_OP_FUSED, Tc, wl.d, wl.V),
+                "tokens_per_s": round(b_tok, 1), "ms_per_step": round(bf["ms_total"] / K, 3),
+                "mfma_peak_frac_6dV": round(b_tok * 6 * dV / PEAK_BF16, 4)},
+            "four_call": {
+                "workspace_bytes": rbp.rbp_workspace_bytes(rbp.RBP_OP_LOGPROB_BWD, Tc, wl.d,
+                                                           wl.V),
+                "tokens_per_s": round(g_tok, 1), "ms_per_step": round(bg["ms_total"] / K, 3),
+                "mfma_peak_frac_6dV": round(g_tok * 6 * dV / PEAK_BF16, 4)},
+        }
     if not args.no_aux:
         rec["memory_bound_steps"] = aux_stress()
     if not args.no_cpu_baseline:

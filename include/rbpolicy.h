@@ -34,13 +34,13 @@
  *   - Tensors are dense, row-major and contiguous.  bf16 tensors are passed as
  *     uint16_t bit patterns (IEEE binary32 truncated to its upper 16 bits).
  *   - The caller owns and allocates every buffer, workspace included; the
- *     library never allocates memory, frees or synchronises (one exception,
- *     policy_fused_fwd_bwd, owns a stream and two events per device; see
- *     there).  Size the workspace with
- *     rbp_workspace_bytes().  Workspace contents are scratch between calls.
+ *     library never allocates memory, frees or synchronises.  Size the
+ *     workspace with rbp_workspace_bytes().  Workspace contents are scratch
+ *     between calls.
  *   - All device work is enqueued on `stream` (a hipStream_t; NULL = the null
- *     stream; policy_fused_fwd_bwd also uses its side stream, ordered against
- *     `stream` by events) and is asynchronous to the host.
+ *     stream) and is asynchronous to the host.  policy_fused_fwd_bwd can also
+ *     use a second stream the caller passes in (rbp_exec), ordered against
+ *     `stream` by the caller's events.
  *   - Return value: RBP_OK (0) or a negative RBP_E* code.  Arguments are checked
  *     on the host before anything is enqueued; on an error nothing is enqueued,
  *     except RBP_EHIP, which reports a failed launch (outputs then undefined).
@@ -48,9 +48,7 @@
  *   - Results are bitwise reproducible for identical inputs (no floating-point
  *     atomics; every reduction runs in a fixed order).
  *   - No exception crosses this interface.  The library holds no mutable global
- *     state except the thread-local error text and, per device, the side
- *     stream and events of policy_fused_fwd_bwd (created on first use, guarded
- *     by a lock, kept until the process ends).
+ *     state except the thread-local error text.
  */
 #ifndef RBPOLICY_H
 #define RBPOLICY_H
@@ -336,6 +334,47 @@ int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
                        void* stream);
 
 /*
+ * Execution controls of policy_fused_fwd_bwd, all owned by the caller (the
+ * library keeps nothing between calls).
+ *   side_stream  a hipStream_t of default priority, other than `stream`, or
+ *                NULL.  When set, the HBM-bound second part of the in-place
+ *                rescale runs there beside the first part of the dW product
+ *                (fork_event is recorded on `stream` and waited for on
+ *                side_stream; join_event is recorded on side_stream and
+ *                waited for on `stream` before the rest of the products), so
+ *                that all the call's work is complete in `stream` order when
+ *                later work on `stream` runs.  The fork / join works under
+ *                HIP graph capture of `stream` as well.  NULL: everything
+ *                runs on `stream`, in order.
+ *   fork_event, join_event  hipEvent_t (created by the caller, e.g. with
+ *                hipEventDisableTiming); required when side_stream is set.
+ *   phase_event[k]  hipEvent_t or NULL: recorded on `stream` when phase k of
+ *                a chunk is done (RBP_PHASE_*), for timing the phases
+ *                without a profiler; with several chunks a later record
+ *                replaces an earlier one.  Leave them NULL under graph
+ *                capture.
+ * Two calls that may run at the same time need their own rbp_exec events
+ * (a shared side stream only serialises their side work).
+ */
+enum {
+  RBP_PHASE_START = 0,    /* before the chunk's first kernel                    */
+  RBP_PHASE_LOGITS = 1,   /* logit tile pass done (q stored, partial sums)      */
+  RBP_PHASE_MERGE = 2,    /* lse, logp and entropy done                         */
+  RBP_PHASE_LOSS = 3,     /* loss pass done (dlogp)                             */
+  RBP_PHASE_SCALE = 4,    /* the rescale's part on `stream` done                */
+  RBP_PHASE_DW = 5,       /* dW done (side stream joined)                       */
+  RBP_PHASE_DHIDDEN = 6,  /* dhidden done                                       */
+  RBP_NUM_PHASES = 7
+};
+
+typedef struct rbp_exec {
+  void* side_stream;                  /* hipStream_t or NULL                    */
+  void* fork_event;                   /* hipEvent_t, needed with side_stream    */
+  void* join_event;                   /* hipEvent_t, needed with side_stream    */
+  void* phase_event[RBP_NUM_PHASES];  /* hipEvent_t or NULL each                */
+} rbp_exec;
+
+/*
  * policy_logprob_fwd + policy_loss_fwd_bwd + policy_logprob_bwd in one pass,
  * plus the per-token entropy of the policy, H_t = -sum_v p_{t,v} log p_{t,v}
  * (the training entropy of App. E).  The separate calls execute 8 d V flop
@@ -343,13 +382,12 @@ int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
  * 6 d V of the definition by keeping, per token, the forward tile pass's
  * exp(z - max) for every vocabulary entry as bf16 in the workspace (2 V bytes
  * per token; it does materialise a T x V array, which policy_logprob_fwd
- * never does).  dz is rounded to bf16 twice instead of once.
- * Overlap: on its first call on a device the entry creates one stream of
- * default priority and two events there, kept until the process ends; it
- * runs the second half of its HBM-bound rescale on that stream beside the
- * first half of the dW product, ordered against `stream` by the events, so
- * all its work is complete in `stream` order when later work on `stream`
- * runs.
+ * never does).  The array is the one the backward's dz needs in any case:
+ * exp(z - M) is turned into dz in place once the loss is known, so the
+ * logits themselves never reach memory.  dz is rounded to bf16 twice instead
+ * of once.
+ * exec: NULL (all work on `stream`, in order) or the caller's rbp_exec
+ * (side stream for the rescale overlap, phase events); see rbp_exec.
  * Arguments: hidden, W, tokens, seq_of_token as in policy_logprob_fwd
  * (seq_of_token required); old_logp, adv, seq_len, B, n_seq_total, eps_low,
  * eps_high, loss_accum, stats as in policy_loss_fwd_bwd (loss_accum and stats
@@ -363,8 +401,12 @@ int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
  * sums, fp32 [Tc, d] and the loss pass's sums -- 5.5 GB for Tc = 16384 at
  * d = 3584, V = 152064.
  * Errors: RBP_EINVAL (null pointers, T < 0, d < 1, V < 1, B < 1,
- *         n_seq_total < 1, eps < 0); RBP_EUNSUPPORTED (d % 8 != 0);
- *         RBP_EWORKSPACE (not even a 256-token chunk fits).
+ *         n_seq_total < 1, eps < 0, a side stream without both events or
+ *         equal to `stream`); RBP_EUNSUPPORTED (d % 8 != 0);
+ *         RBP_EWORKSPACE (not even a 256-token chunk fits); RBP_EHIP (a
+ *         launch, event record or stream wait failed: earlier work may
+ *         still be pending on `stream` and on the side stream, which the
+ *         caller then synchronises before reusing any buffer).
  */
 int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
                          const int32_t* tokens, const int32_t* seq_of_token,
@@ -374,7 +416,7 @@ int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
                          float eps_high, float* logp, float* lse, float* entropy,
                          float* loss_accum, float* dlogp, float* stats,
                          float* dhidden, float* dW, int accumulate_dW, void* ws,
-                         size_t ws_bytes, void* stream);
+                         size_t ws_bytes, const rbp_exec* exec, void* stream);
 
 /*
  * The record table as rb_push writes it: the rb_records arrays, writable, with

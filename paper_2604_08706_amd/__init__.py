@@ -31,10 +31,21 @@ from ._binding import (  # noqa: F401
     RBP_OP_NOTE_USE,
     RBP_OP_LOSS_SEQ,
     RBP_OP_SAMPLE_GATHER,
+    RBP_NUM_PHASES,
+    RBP_PHASE_DHIDDEN,
+    RBP_PHASE_DW,
+    RBP_PHASE_LOGITS,
+    RBP_PHASE_LOSS,
+    RBP_PHASE_MERGE,
+    RBP_PHASE_SCALE,
+    RBP_PHASE_START,
+    Overlap,
     RbpError,
+    RbpExec,
     alloc_batch,
     lib,
     load_library,
+    make_exec,
     make_records,
     make_ring,
     make_sample_cfg,

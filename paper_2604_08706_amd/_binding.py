@@ -36,6 +36,15 @@ RBP_OP_LOSS_SEQ = 5
 RBP_OP_FUSED = 6
 RBP_OP_NOTE_USE = 7
 
+RBP_PHASE_START = 0
+RBP_PHASE_LOGITS = 1
+RBP_PHASE_MERGE = 2
+RBP_PHASE_LOSS = 3
+RBP_PHASE_SCALE = 4
+RBP_PHASE_DW = 5
+RBP_PHASE_DHIDDEN = 6
+RBP_NUM_PHASES = 7
+
 EXPORTED = (
     "rb_sample_gather", "rb_group_advantage", "policy_logprob_fwd",
     "policy_loss_fwd_bwd", "policy_logprob_bwd", "rbp_workspace_bytes",
@@ -96,6 +105,13 @@ class RbBatch(ctypes.Structure):
     ]
 
 
+class RbpExec(ctypes.Structure):
+    _fields_ = [
+        ("side_stream", ctypes.c_void_p), ("fork_event", ctypes.c_void_p),
+        ("join_event", ctypes.c_void_p), ("phase_event", ctypes.c_void_p * RBP_NUM_PHASES),
+    ]
+
+
 def load_library(path=LIB_PATH):
     """Load librbpolicy.so and declare its signatures.  Raises if missing."""
     if not os.path.exists(path):
@@ -119,7 +135,7 @@ def load_library(path=LIB_PATH):
     lib.policy_asymre_fwd_bwd.argtypes = [vp, vp, vp, i64, i32, i64, vp, vp, vp, vp, sz, vp]
     lib.policy_fused_fwd_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i32, i32, i32, i64,
                                          f32, f32, vp, vp, vp, vp, vp, vp, vp, vp,
-                                         ctypes.c_int, vp, sz, vp]
+                                         ctypes.c_int, vp, sz, ctypes.POINTER(RbpExec), vp]
     lib.rb_push.argtypes = [ctypes.POINTER(RbRing), i32, i32, vp, vp, vp, vp, i32, vp, vp, i32,
                             f32, vp]
     lib.rb_note_use.argtypes = [vp, i64, i64, i64, i64, vp, vp, vp, vp, sz, vp]
@@ -367,9 +383,56 @@ def policy_logprob_bwd(hidden, W, tokens, seq_of_token, lse, dlogp, dhidden, dW,
     _check("policy_logprob_bwd", st)
 
 
+def _event_handle(ev, stream):
+    # torch creates the underlying event on its first record
+    if ev.cuda_event == 0:
+        ev.record(stream)
+    return ev.cuda_event
+
+
+def make_exec(side_stream=None, fork_event=None, join_event=None, phase_events=None,
+              stream=None):
+    """rbp_exec from torch objects: a side torch.cuda.Stream with its two
+    torch.cuda.Events, and/or a list of RBP_NUM_PHASES timing events (None
+    entries allowed).  The struct holds references to them, so the raw
+    handles it carries stay valid while the struct is alive."""
+    ex = RbpExec()
+    # torch destroys an event's HIP handle when the Python object goes away
+    ex._keep = (side_stream, fork_event, join_event, list(phase_events or ()))
+    s = torch.cuda.current_stream() if stream is None else stream
+    if side_stream is not None:
+        if fork_event is None or join_event is None:
+            raise ValueError("a side stream needs fork_event and join_event")
+        ex.side_stream = side_stream.cuda_stream
+        ex.fork_event = _event_handle(fork_event, s)
+        ex.join_event = _event_handle(join_event, s)
+    for k, ev in enumerate(phase_events or ()):
+        if ev is not None:
+            ex.phase_event[k] = _event_handle(ev, s)
+    return ex
+
+
+class Overlap:
+    """A side stream and its fork / join events for policy_fused_fwd_bwd
+    (torch allocates them; the library only uses them)."""
+
+    def __init__(self, device=None):
+        self.stream = torch.cuda.Stream(device=device)
+        self.fork = torch.cuda.Event()
+        self.join = torch.cuda.Event()
+
+    def exec(self, phase_events=None, stream=None):
+        ex = make_exec(self.stream, self.fork, self.join, phase_events, stream)
+        ex._owner = self  # keeps the stream and events alive with the struct
+        return ex
+
+
 def policy_fused_fwd_bwd(hidden, W, tokens, seq_of_token, old_logp, adv, seq_len, n_seq_total,
                          logp, lse, entropy, loss_accum, dlogp, stats, dhidden, dW, ws,
-                         accumulate_dW=False, eps_low=0.2, eps_high=0.2, stream=None):
+                         accumulate_dW=False, eps_low=0.2, eps_high=0.2, exec=None,
+                         stream=None):
+    """exec: None (all work on the stream, in order) or an RbpExec
+    (make_exec / Overlap.exec)."""
     T, d = hidden.shape
     V = W.shape[0]
     B = adv.numel()
@@ -390,7 +453,9 @@ def policy_fused_fwd_bwd(hidden, W, tokens, seq_of_token, old_logp, adv, seq_len
                                     _dev(stats, torch.float32, "stats", 4),
                                     _dev(dhidden, torch.float32, "dhidden", T * d),
                                     _dev(dW, torch.float32, "dW", V * d),
-                                    1 if accumulate_dW else 0, wsp, wsb, _stream(stream))
+                                    1 if accumulate_dW else 0, wsp, wsb,
+                                    None if exec is None else ctypes.byref(exec),
+                                    _stream(stream))
     _check("policy_fused_fwd_bwd", st)
 
 

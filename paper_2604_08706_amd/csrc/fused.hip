@@ -25,8 +25,6 @@
 // the workspace).  dz is rounded to bf16 twice (q, then the scaled value)
 // instead of once.
 
-#include <mutex>
-
 #include "logits_epilogue.h"
 #include "rbp_internal.h"
 
@@ -337,36 +335,6 @@ FusedWs carve_fused(void* base, int64_t Tc, int32_t d, int32_t V) {
   return w;
 }
 
-// A second stream per device, owned by the library (created on the first call
-// on that device, default priority, kept for the life of the process), and
-// two events that order it against the caller's stream.  It lets the second
-// half of the in-place rescale (HBM-bound) run beside the first half of the
-// dW product (MFMA-bound); both fit on a CU at once (dW: one 512-thread
-// workgroup, 128 KiB of LDS, 216 VGPRs per lane, two waves per SIMD; rescale:
-// 40 VGPRs, no LDS -- 2 x 216 + 40 <= 512).
-struct SideStream {
-  hipStream_t stream = nullptr;
-  hipEvent_t head_done = nullptr, tail_done = nullptr;
-  std::mutex lock;  // serialises event record / wait pairs of concurrent calls
-  bool ready = false;
-};
-SideStream g_side[64];
-
-SideStream* side_stream() {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-  SideStream& ss = g_side[dev];
-  std::lock_guard<std::mutex> g(ss.lock);
-  if (!ss.ready) {
-    if (hipStreamCreateWithFlags(&ss.stream, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    if (hipEventCreateWithFlags(&ss.head_done, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&ss.tail_done, hipEventDisableTiming) != hipSuccess)
-      return nullptr;
-    ss.ready = true;
-  }
-  return &ss;
-}
-
 // Vocabulary tiles of the first dW part: the smallest multiple of the tiles
 // that make whole rounds of the persistent grid (tiles_d * tv0 % n_cu == 0)
 // that is at least a fifth of the vocabulary -- the rescale of the rest, run
@@ -391,6 +359,16 @@ size_t rbp::fused_ws(int64_t Tc, int32_t d, int32_t V) {
   return carve_fused(nullptr, round256(Tc < 1 ? 1 : Tc), d < 1 ? 1 : d, V < 1 ? 1 : V).bytes;
 }
 
+namespace {
+
+// Records phase event k of `ex` (if given) on s.
+inline hipError_t mark(const rbp_exec* ex, int k, hipStream_t s) {
+  if (ex == nullptr || ex->phase_event[k] == nullptr) return hipSuccess;
+  return hipEventRecord(reinterpret_cast<hipEvent_t>(ex->phase_event[k]), s);
+}
+
+}  // namespace
+
 extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
                                     const int32_t* tokens, const int32_t* seq_of_token,
                                     const float* old_logp, const float* adv,
@@ -399,7 +377,7 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
                                     float eps_high, float* logp, float* lse, float* entropy,
                                     float* loss_accum, float* dlogp, float* stats,
                                     float* dhidden, float* dW, int accumulate_dW, void* ws,
-                                    size_t ws_bytes, void* stream) {
+                                    size_t ws_bytes, const rbp_exec* exec, void* stream) {
   rbp::clear_error();
   RBP_REQUIRE(T >= 0 && d >= 1 && V >= 1, RBP_EINVAL,
               "policy_fused_fwd_bwd: need T >= 0, d >= 1, V >= 1");
@@ -413,6 +391,11 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
   RBP_REQUIRE(T == 0 || (hidden && tokens && seq_of_token && old_logp && logp && lse && dlogp &&
                          dhidden),
               RBP_EINVAL, "policy_fused_fwd_bwd: null per-token pointer");
+  const bool overlap = exec != nullptr && exec->side_stream != nullptr;
+  RBP_REQUIRE(!overlap || (exec->fork_event && exec->join_event), RBP_EINVAL,
+              "policy_fused_fwd_bwd: a side stream needs both fork_event and join_event");
+  RBP_REQUIRE(!overlap || exec->side_stream != stream, RBP_EINVAL,
+              "policy_fused_fwd_bwd: the side stream must differ from `stream`");
   hipStream_t s = rbp::as_stream(stream);
   if (T == 0) {
     rbp::launch_grad_products(nullptr, W, nullptr, 0, 0, d, V, nullptr, nullptr, dW,
@@ -437,71 +420,80 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
               "policy_fused_fwd_bwd: workspace of %zu bytes holds no 256-token chunk (needs %zu)",
               ws_bytes, rbp::fused_ws(256, d, V));
   const FusedWs w = carve_fused(ws, Tc, d, V);
-  SideStream* side = side_stream();
+  hipStream_t side = overlap ? rbp::as_stream(exec->side_stream) : nullptr;
+  hipEvent_t fork = overlap ? reinterpret_cast<hipEvent_t>(exec->fork_event) : nullptr;
+  hipEvent_t join = overlap ? reinterpret_cast<hipEvent_t>(exec->join_event) : nullptr;
   const int64_t Vp = round256(V), tiles_v = Vp / 256;
   const int n_cu = device_cus();
+  hipError_t e = hipSuccess;
+#define RBP_FUSED_HIP(call)                                                               \
+  do {                                                                                    \
+    e = (call);                                                                           \
+    if (e != hipSuccess) {                                                                \
+      rbp::set_error("policy_fused_fwd_bwd: %s: %s", #call, hipGetErrorString(e));        \
+      return RBP_EHIP;                                                                    \
+    }                                                                                     \
+  } while (0)
   for (int64_t t0 = 0; t0 < T; t0 += Tc) {
     const int64_t Tn = (T - t0) < Tc ? (T - t0) : Tc;
     const int64_t T256 = round256(Tn), tiles_t = T256 / 256;
     const uint16_t* Hc = hidden + t0 * d;
     const int32_t* sq = seq_of_token + t0;
+    RBP_FUSED_HIP(mark(exec, RBP_PHASE_START, s));
     hipLaunchKernelGGL(logits_store_kernel, dim3(rbp::gemm::stream_grid(tiles_v * tiles_t, n_cu)),
                        dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, w.pM, w.pS, w.pE, Tc, w.Qt, Tc,
                        tiles_v, tiles_t);
+    RBP_FUSED_HIP(mark(exec, RBP_PHASE_LOGITS, s));
     hipLaunchKernelGGL(fused_merge_kernel, dim3(rbp::ceil_div(Tn, kMergeTokens)),
                        dim3(64 * kMergeWaves), 0, s,
                        w.pM, w.pS, w.pE, Tc, (int32_t)(Vp / 128), Hc, W, tokens + t0, sq, Tn, d, V,
                        logp + t0, lse + t0, entropy ? entropy + t0 : nullptr);
     RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+    RBP_FUSED_HIP(mark(exec, RBP_PHASE_MERGE, s));
     const int st = policy_loss_fwd_bwd(logp + t0, old_logp + t0, sq, adv, seq_len, Tn, B,
                                        n_seq_total, eps_low, eps_high, loss_accum, dlogp + t0,
                                        stats, w.loss, w.loss_bytes, stream);
     if (st != RBP_OK) return st;
+    RBP_FUSED_HIP(mark(exec, RBP_PHASE_LOSS, s));
     const int acc = (accumulate_dW || t0 > 0) ? 1 : 0;
     const unsigned gx = (unsigned)rbp::ceil_div(T256, kScaleTokens);
-    const int64_t tv0 = side ? head_tiles(rbp::ceil_div(d, 256), tiles_v, n_cu) : 0;
+    const int64_t tv0 = overlap ? head_tiles(rbp::ceil_div(d, 256), tiles_v, n_cu) : 0;
     if (tv0 > 0) {
       // rescale rows [0, 256 tv0); then, on the side stream, the rest while
       // dW runs over the first tv0 vocabulary tiles; dW of the rest and
-      // dhidden once both halves are done
+      // dhidden once both parts are done
       const int32_t g0 = (int32_t)(tv0 * 2);  // 128-row groups in the head
       hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)g0), dim3(256), 0, s, w.Qt, Tc,
                          T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0, tokens + t0, sq, Tn, V,
                          0);
-      hipError_t e;
-      {
-        std::lock_guard<std::mutex> g(side->lock);
-        e = hipEventRecord(side->head_done, s);
-        if (e == hipSuccess) e = hipStreamWaitEvent(side->stream, side->head_done, 0);
-        if (e == hipSuccess) {
-          hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)(Vp / 128 - g0)), dim3(256),
-                             0, side->stream, w.Qt, Tc, T256, w.pM, Tc, lse + t0, logp + t0,
-                             dlogp + t0, tokens + t0, sq, Tn, V, g0);
-          e = hipGetLastError();
-        }
-        if (e == hipSuccess) e = hipEventRecord(side->tail_done, side->stream);
-      }
+      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+      RBP_FUSED_HIP(mark(exec, RBP_PHASE_SCALE, s));
+      RBP_FUSED_HIP(hipEventRecord(fork, s));
+      RBP_FUSED_HIP(hipStreamWaitEvent(side, fork, 0));
+      hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)(Vp / 128 - g0)), dim3(256), 0,
+                         side, w.Qt, Tc, T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0,
+                         tokens + t0, sq, Tn, V, g0);
+      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+      RBP_FUSED_HIP(hipEventRecord(join, side));
       rbp::launch_dweight(Hc, w.Qt, Tc, Tn, d, V, dW, acc, 0, tv0, s);
-      // waits for the latest rescale tail on the side stream: this call's, or
-      // a later one of a concurrent call (which then comes after it)
-      if (e == hipSuccess) e = hipStreamWaitEvent(s, side->tail_done, 0);
-      if (e != hipSuccess) {
-        // no side-stream work may outlive a failed call
-        (void)hipStreamSynchronize(side->stream);
-        rbp::set_error("policy_fused_fwd_bwd: ordering the side stream failed: %s",
-                       hipGetErrorString(e));
-        return RBP_EHIP;
-      }
+      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+      RBP_FUSED_HIP(hipStreamWaitEvent(s, join, 0));
       rbp::launch_dweight(Hc, w.Qt, Tc, Tn, d, V, dW, acc, tv0, tiles_v, s);
-      rbp::launch_dhidden(W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, s);
+      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
     } else {
       hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)(Vp / 128)), dim3(256), 0, s,
                          w.Qt, Tc, T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0, tokens + t0,
                          sq, Tn, V, 0);
-      rbp::launch_grad_products(Hc, W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, dW,
-                                acc, s);
+      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+      RBP_FUSED_HIP(mark(exec, RBP_PHASE_SCALE, s));
+      rbp::launch_dweight(Hc, w.Qt, Tc, Tn, d, V, dW, acc, 0, tiles_v, s);
+      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
     }
+    RBP_FUSED_HIP(mark(exec, RBP_PHASE_DW, s));
+    rbp::launch_dhidden(W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, s);
+    RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+    RBP_FUSED_HIP(mark(exec, RBP_PHASE_DHIDDEN, s));
   }
-  RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+#undef RBP_FUSED_HIP
   return RBP_OK;
 }

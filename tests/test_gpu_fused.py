@@ -33,8 +33,22 @@ def _sequences(T, seed, masked=0.1, mean_len=40):
     return seq, np.array(lens, dtype=np.int32)
 
 
+_OVERLAP = {}
+
+
+def _overlap(rbp):
+    """One side stream with its events per thread (calls that may run at the
+    same time need their own)."""
+    import threading
+
+    key = threading.get_ident()
+    if key not in _OVERLAP:
+        _OVERLAP[key] = rbp.Overlap()
+    return _OVERLAP[key]
+
+
 def _run(rbp, hidden, W, tokens, seq, old, adv, slen, n_seq, ws_tokens=None, dW0=None,
-         want_entropy=True):
+         want_entropy=True, overlap=True, phase_events=None):
     T, d = hidden.shape
     V = W.shape[0]
     out = {k: torch.empty(T, device="cuda") for k in ("logp", "lse", "dlogp")}
@@ -44,10 +58,16 @@ def _run(rbp, hidden, W, tokens, seq, old, adv, slen, n_seq, ws_tokens=None, dW0
     out["dh"] = torch.empty((T, d), device="cuda")
     out["dW"] = torch.empty((V, d), device="cuda") if dW0 is None else dW0.clone()
     ws = rbp.workspace(rbp.RBP_OP_FUSED, T if ws_tokens is None else ws_tokens, d, V)
+    if isinstance(overlap, rbp.RbpExec):
+        ex = overlap
+    elif overlap:
+        ex = _overlap(rbp).exec(phase_events)
+    else:
+        ex = rbp.make_exec(phase_events=phase_events) if phase_events else None
     rbp.policy_fused_fwd_bwd(hidden, W, tokens, seq, old, adv, slen, n_seq, out["logp"],
                              out["lse"], out["entropy"], out["loss"], out["dlogp"],
                              out["stats"], out["dh"], out["dW"], ws,
-                             accumulate_dW=dW0 is not None)
+                             accumulate_dW=dW0 is not None, exec=ex)
     torch.cuda.synchronize()
     return out
 
@@ -208,9 +228,9 @@ def test_fused_reproducible_empty_and_bad_args():
 
 
 def test_fused_concurrent_calls_on_two_streams():
-    """Two host threads run the single pass on their own streams at once (the
-    library's side stream and events are shared between them); every result
-    must equal the same call made alone."""
+    """Two host threads run the single pass on their own streams at once, each
+    with its own side stream and events; every result must equal the same call
+    made alone."""
     import threading
 
     rbp = require_gpu()
@@ -309,3 +329,67 @@ def test_fused_three_chunks_with_sequences_across_chunk_boundaries():
     assert np.sqrt(num / den) < RTOL
     del hidden, W, out, dW0
     torch.cuda.empty_cache()
+
+
+def test_fused_overlap_serial_and_phase_events_agree():
+    """The side-stream overlap only reorders independent work: results are
+    bit-identical to the serial call (exec = NULL).  Phase events recorded on
+    the caller's stream bracket every phase, in order."""
+    rbp = require_gpu()
+    T, d, V = 2048, 512, 70000  # large enough that the overlapped path runs
+    (hidden, W, tokens, seq, lens, *_r) = _case(T, d, V, 0.02, 41, device="cuda")
+    old, adv = _r[-2], _r[-1]
+    args = (rbp, hidden, W, tokens, torch.from_numpy(seq).cuda(), torch.from_numpy(old).cuda(),
+            torch.from_numpy(adv).cuda(), torch.from_numpy(lens).cuda(), len(lens))
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(rbp.RBP_NUM_PHASES)]
+    a = _run(*args, overlap=True, phase_events=evs)
+    ms = [evs[k].elapsed_time(evs[k + 1]) for k in range(rbp.RBP_NUM_PHASES - 1)]
+    assert all(m >= 0.0 for m in ms) and sum(ms) > 0.0, ms
+    b = _run(*args, overlap=False)
+    c = _run(*args, overlap=False, phase_events=evs[:3] + [None] * 4)
+    for key in ("logp", "lse", "entropy", "loss", "dlogp", "stats", "dh", "dW"):
+        assert torch.equal(a[key], b[key]), key
+        assert torch.equal(a[key], c[key]), key
+
+
+def test_fused_rejects_bad_exec():
+    rbp = require_gpu()
+    T, d, V = 256, 64, 1000
+    (hidden, W, tokens, seq, lens, *_r) = _case(T, d, V, 0.02, 43, device="cuda")
+    old, adv = _r[-2], _r[-1]
+    f = lambda t: torch.empty(t, device="cuda")  # noqa: E731
+    ws = rbp.workspace(rbp.RBP_OP_FUSED, T, d, V)
+    bad = rbp.RbpExec()
+    bad.side_stream = torch.cuda.Stream().cuda_stream  # no events
+    st = torch.cuda.Stream()  # the default stream's handle is NULL, i.e. "no side stream"
+    same = rbp.make_exec(st, torch.cuda.Event(), torch.cuda.Event(), stream=st)
+    for ex in (bad, same):
+        with pytest.raises(rbp.RbpError) as e:
+            rbp.policy_fused_fwd_bwd(hidden, W, tokens, torch.from_numpy(seq).cuda(),
+                                     torch.from_numpy(old).cuda(), torch.from_numpy(adv).cuda(),
+                                     torch.from_numpy(lens).cuda(), len(lens), f(T), f(T), None,
+                                     torch.zeros(1, device="cuda"), f(T),
+                                     torch.zeros(4, device="cuda"), f(T * d), f(V * d), ws,
+                                     exec=ex, stream=st)
+        assert e.value.status == rbp.RBP_EINVAL
+
+
+def test_fused_exec_outlives_its_temporaries():
+    """An rbp_exec built from a temporary Overlap keeps the torch stream and
+    events it points to alive (torch frees an event's handle with the Python
+    object), so a later call may use it."""
+    import gc
+
+    rbp = require_gpu()
+    T, d, V = 2048, 512, 70000  # large enough that the overlapped path runs
+    (hidden, W, tokens, seq, lens, *_r) = _case(T, d, V, 0.02, 47, device="cuda")
+    old, adv = _r[-2], _r[-1]
+    args = (rbp, hidden, W, tokens, torch.from_numpy(seq).cuda(), torch.from_numpy(old).cuda(),
+            torch.from_numpy(adv).cuda(), torch.from_numpy(lens).cuda(), len(lens))
+    ex = rbp.Overlap().exec([torch.cuda.Event(enable_timing=True)
+                             for _ in range(rbp.RBP_NUM_PHASES)])
+    gc.collect()
+    a = _run(*args, overlap=ex)
+    b = _run(*args, overlap=False)
+    for key in ("logp", "dlogp", "dh", "dW"):
+        assert torch.equal(a[key], b[key]), key

@@ -98,3 +98,58 @@ def test_replay_step_as_a_graph():
         got = _snapshot(b)
         for k, v in want.items():
             assert torch.equal(got[k], v), (r, k)
+
+
+def _fused_step(rbp, ring, cfg, b, hidden, W, ex):
+    out = b["out"]
+    rbp.rb_sample_gather(ring.rec, cfg, out, b["ws_s"])
+    b["loss"].zero_()
+    b["stats"].zero_()
+    rbp.policy_fused_fwd_bwd(hidden, W, out["tokens"], out["seq_of_token"], out["old_logp"],
+                             out["adv"], out["len"], cfg.n_draw, b["logp"], b["lse"], b["ent"],
+                             b["loss"], b["dlogp"], b["stats"], b["dh"], b["dW"], b["ws_u"],
+                             exec=ex)
+
+
+@pytest.mark.parametrize("overlap", [True, False])
+def test_fused_step_as_a_graph(overlap):
+    """The single pass captured with its side-stream fork / join (the caller's
+    stream and events of rbp_exec; the library keeps none) replays bit for bit
+    like the eager call."""
+    rbp = require_gpu()
+    ring, cfg, b, hidden, W = _setup(rbp)
+    T, d = hidden.shape
+    V = W.shape[0]
+    b["ent"] = torch.empty(T, device="cuda")
+    b["ws_u"] = rbp.workspace(rbp.RBP_OP_FUSED, T, d, V)
+    ovl = rbp.Overlap() if overlap else None
+    ex = ovl.exec() if overlap else None
+    print(f"[graph] fused eager step (overlap={overlap})", flush=True)
+    _fused_step(rbp, ring, cfg, b, hidden, W, ex)
+    torch.cuda.synchronize()
+    want = _snapshot(b)
+    want["ent"] = b["ent"].clone()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        _fused_step(rbp, ring, cfg, b, hidden, W, ex)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    print("[graph] fused capture", flush=True)
+    with torch.cuda.graph(g):
+        _fused_step(rbp, ring, cfg, b, hidden, W, ex)
+    torch.cuda.synchronize()
+    for r in range(3):
+        for k in ("logp", "lse", "dlogp", "dh", "dW", "ent"):
+            b[k].fill_(float("nan"))
+        b["out"]["tokens"].fill_(-7)
+        b["loss"].fill_(123.0)
+        torch.cuda.synchronize()
+        print(f"[graph] fused replay {r}", flush=True)
+        g.replay()
+        torch.cuda.synchronize()
+        got = _snapshot(b)
+        got["ent"] = b["ent"].clone()
+        for k, v in want.items():
+            assert torch.equal(got[k], v), (r, k)
