@@ -199,6 +199,24 @@ int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
                      void* stream);
 
 /*
+ * rb_sample_gather without a workspace argument, for callers that cannot
+ * allocate (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments (minus ws, ws_bytes), same results bit
+ * for bit, same errors.  Its workspace is a static device array of 32 MiB
+ * that each GPU the library runs on holds from module load until the
+ * process ends; the call allocates and frees nothing.  Record tables whose
+ * rbp_workspace_bytes(RBP_OP_SAMPLE_GATHER, capacity, 0, 0) exceeds 32 MiB
+ * (capacity above about 1.6 million records) are rejected with
+ * RBP_EWORKSPACE before anything is enqueued.  Every call on a GPU uses that
+ * GPU's one array: calls that may overlap on the same GPU (two streams, two
+ * threads) race and must be ordered by the caller.  The first call on a
+ * device resolves the array's device address (hipGetSymbolAddress) and
+ * should run outside graph capture.
+ */
+int rb_sample_gather_noalloc(const rb_records* rec, const rb_sample_cfg* cfg,
+                             const rb_batch* out, void* stream);
+
+/*
  * Group-normalised advantage at insert time (App. D.2):
  * A_i = (r_i - mean_g) / (std_g + eps) over group g = [group_off[g],
  * group_off[g+1]); std uses `ddof` (1 = sample estimate); a group whose rewards

@@ -61,6 +61,7 @@ from ._binding import (  # noqa: F401
     rb_note_use,
     rb_push,
     rb_sample_gather,
+    rb_sample_gather_noalloc,
     rbp_workspace_bytes,
     ring_records,
     workspace,

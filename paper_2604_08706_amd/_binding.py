@@ -50,7 +50,7 @@ EXPORTED = (
     "policy_loss_fwd_bwd", "policy_logprob_bwd", "rbp_workspace_bytes",
     "rbp_status_string", "rbp_last_error", "policy_loss_seq_fwd_bwd", "rb_asymre_coef",
     "policy_asymre_fwd_bwd", "policy_fused_fwd_bwd", "rb_push", "rb_note_use",
-    "rb_hist_accumulate",
+    "rb_hist_accumulate", "rb_sample_gather_noalloc",
 )
 
 
@@ -123,6 +123,9 @@ def load_library(path=LIB_PATH):
                              ctypes.c_size_t, ctypes.c_float)
     lib.rb_sample_gather.argtypes = [ctypes.POINTER(RbRecords), ctypes.POINTER(RbSampleCfg),
                                      ctypes.POINTER(RbBatch), vp, sz, vp]
+    lib.rb_sample_gather_noalloc.argtypes = [ctypes.POINTER(RbRecords),
+                                             ctypes.POINTER(RbSampleCfg),
+                                             ctypes.POINTER(RbBatch), vp]
     lib.rb_group_advantage.argtypes = [vp, vp, i32, i32, f32, vp, vp]
     lib.policy_logprob_fwd.argtypes = [vp, vp, vp, vp, i64, i32, i32, vp, vp, vp, sz, vp]
     lib.policy_loss_fwd_bwd.argtypes = [vp, vp, vp, vp, vp, i64, i32, i64, f32, f32,
@@ -269,7 +272,7 @@ def alloc_batch(cfg, device="cuda"):
     }
 
 
-def rb_sample_gather(rec, cfg, out, ws, stream=None):
+def _batch(cfg, out):
     n = cfg.n_draw
     width = cfg.max_tokens if cfg.layout == RB_LAYOUT_PACKED else n * cfg.l_max
     b = RbBatch()
@@ -282,10 +285,24 @@ def rb_sample_gather(rec, cfg, out, ws, stream=None):
     b.old_logp = _dev(out["old_logp"], torch.float32, "old_logp", width).value
     b.seq_of_token = _dev(out["seq_of_token"], torch.int32, "seq_of_token", width).value
     b.n_tokens = _dev(out["n_tokens"], torch.int64, "n_tokens", 1).value
+    return b
+
+
+def rb_sample_gather(rec, cfg, out, ws, stream=None):
+    b = _batch(cfg, out)
     wsp, wsb = _ws(ws)
     st = lib().rb_sample_gather(ctypes.byref(rec), ctypes.byref(cfg), ctypes.byref(b), wsp,
                                 wsb, _stream(stream))
     _check("rb_sample_gather", st)
+
+
+def rb_sample_gather_noalloc(rec, cfg, out, stream=None):
+    """rb_sample_gather with the library's static per-GPU scratch as its
+    workspace (no workspace tensor; calls on one GPU must not overlap)."""
+    b = _batch(cfg, out)
+    st = lib().rb_sample_gather_noalloc(ctypes.byref(rec), ctypes.byref(cfg), ctypes.byref(b),
+                                        _stream(stream))
+    _check("rb_sample_gather_noalloc", st)
 
 
 def _bf16_bits(t, name, numel):

@@ -24,6 +24,9 @@
 //              from the token arena.
 // Everything is integer work or a bit-exact copy of stored floats.
 
+#include <atomic>
+#include <mutex>
+
 #include "rbp_internal.h"
 
 namespace {
@@ -691,10 +694,12 @@ size_t rbp::sample_gather_ws(int64_t capacity) {
   return align_up(c.used, 256);
 }
 
-extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
-                                const rb_batch* out, void* ws, size_t ws_bytes,
-                                void* stream) {
-  rbp::clear_error();
+namespace {
+
+// Everything rb_sample_gather does after clearing the error text: argument
+// checks, then the device pipeline with `ws` as its workspace.
+int sample_gather(const rb_records* rec, const rb_sample_cfg* cfg, const rb_batch* out, void* ws,
+                  size_t ws_bytes, void* stream) {
   RBP_REQUIRE(rec && cfg && out, RBP_EINVAL, "rb_sample_gather: null struct pointer");
   RBP_REQUIRE(rec->capacity >= 1 && rec->n_live >= 1 && rec->n_live <= rec->capacity,
               RBP_EINVAL, "rb_sample_gather: need 1 <= n_live <= capacity (got %lld, %lld)",
@@ -837,4 +842,68 @@ extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
   }
   RBP_CHECK_LAUNCH("rb_sample_gather");
   return RBP_OK;
+}
+
+// Workspace of rb_sample_gather_noalloc: one array per device, held from
+// module load until the process ends.  In host code `scratch` names a
+// host-side stand-in; the device address comes from hipGetSymbolAddress.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_lock;
+
+// The current device's address of `scratch`, resolved on the first call on
+// that device (with the device current) and kept.
+int scratch_addr(void** addr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  RBP_REQUIRE(e == hipSuccess, RBP_EHIP, "rb_sample_gather_noalloc: hipGetDevice: %s",
+              hipGetErrorString(e));
+  RBP_REQUIRE(dev >= 0 && dev < kMaxDevices, RBP_EUNSUPPORTED,
+              "rb_sample_gather_noalloc: device %d beyond the %d the library tracks", dev,
+              kMaxDevices);
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    std::lock_guard<std::mutex> g(g_scratch_lock);
+    p = g_scratch_addr[dev].load(std::memory_order_relaxed);
+    if (p == nullptr) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      RBP_REQUIRE(e == hipSuccess && p != nullptr, RBP_EHIP,
+                  "rb_sample_gather_noalloc: hipGetSymbolAddress(scratch) on device %d: %s",
+                  dev, hipGetErrorString(e));
+      g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *addr = p;
+  return RBP_OK;
+}
+
+}  // namespace
+
+extern "C" int rb_sample_gather(const rb_records* rec, const rb_sample_cfg* cfg,
+                                const rb_batch* out, void* ws, size_t ws_bytes,
+                                void* stream) {
+  rbp::clear_error();
+  return sample_gather(rec, cfg, out, ws, ws_bytes, stream);
+}
+
+extern "C" int rb_sample_gather_noalloc(const rb_records* rec, const rb_sample_cfg* cfg,
+                                        const rb_batch* out, void* stream) {
+  rbp::clear_error();
+  RBP_REQUIRE(rec, RBP_EINVAL, "rb_sample_gather_noalloc: null record table");
+  RBP_REQUIRE(rec->capacity >= 1 && rec->capacity <= INT32_MAX, RBP_EINVAL,
+              "rb_sample_gather_noalloc: capacity %lld outside [1, 2^31-1]",
+              (long long)rec->capacity);
+  const size_t need = rbp::sample_gather_ws(rec->capacity);
+  RBP_REQUIRE(need <= kScratchBytes, RBP_EWORKSPACE,
+              "rb_sample_gather_noalloc: a record table of capacity %lld needs %zu bytes of "
+              "workspace, more than the %zu-byte static scratch (use rb_sample_gather with a "
+              "caller workspace)",
+              (long long)rec->capacity, need, kScratchBytes);
+  void* ws = nullptr;
+  const int st = scratch_addr(&ws);
+  if (st != RBP_OK) return st;
+  return sample_gather(rec, cfg, out, ws, kScratchBytes, stream);
 }
