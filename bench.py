@@ -49,8 +49,7 @@ TRAFFIC = None
 # the three products of the single pass, by the phase that times them
 PRODUCTS = {
     "logits": "logits_store_kernel (forward product; stores exp(z - M) as bf16)",
-    "dW": "dweight_kernel (dW product: two launches, the side stream's rescale beside "
-          "the first)",
+    "dW": "dweight_kernel (dW product)",
     "dhidden": "dhidden_kernel + add_f32_kernel (dhidden product, split-K 2)",
 }
 
@@ -559,25 +558,23 @@ def spread(xs):
             "max": round(float(np.max(xs)), 3)}
 
 
-PHASES = ("logits", "merge", "loss", "scale", "dW", "dhidden")
+PHASES = ("logits", "merge", "loss", "scale", "dW", "dhidden")  # the RBP_PHASE_* order
 
 
 def fused_leg(rbp, wl, S, out, first_step, steps, warmup, ws_tokens=None):
     """Time the single pass over `steps` sampled batches (after `warmup`),
-    with the rescale overlapped on a side stream and the call's phase events
-    recorded on the caller's stream.  ws_tokens: size the workspace for that
-    many tokens (the call then runs in chunks)."""
+    with the call's phase events recorded on the caller's stream.  ws_tokens:
+    size the workspace for that many tokens (the call then runs in chunks)."""
     import torch
 
     T = S["T"]
     S["entropy"] = torch.empty(T, device="cuda")
     S["ws_fused"] = rbp.workspace(rbp.RBP_OP_FUSED, ws_tokens or T, wl.d, wl.V)
-    ovl = rbp.Overlap()
     for k in range(warmup):
-        run_step_fused(rbp, wl, S, first_step + k, out, ovl.exec())
+        run_step_fused(rbp, wl, S, first_step + k, out, None)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(1 + rbp.RBP_NUM_PHASES)]
           for _ in range(steps)]
-    exs = [ovl.exec(e[1:]) for e in ev]  # creates the events before timing
+    exs = [rbp.make_exec(e[1:]) for e in ev]  # creates the events before timing
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()

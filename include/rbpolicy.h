@@ -38,9 +38,7 @@
  *     workspace with rbp_workspace_bytes().  Workspace contents are scratch
  *     between calls.
  *   - All device work is enqueued on `stream` (a hipStream_t; NULL = the null
- *     stream) and is asynchronous to the host.  policy_fused_fwd_bwd can also
- *     use a second stream the caller passes in (rbp_exec), ordered against
- *     `stream` by the caller's events.
+ *     stream) and is asynchronous to the host.
  *   - Return value: RBP_OK (0) or a negative RBP_E* code.  Arguments are checked
  *     on the host before anything is enqueued; on an error nothing is enqueued,
  *     except RBP_EHIP, which reports a failed launch (outputs then undefined).
@@ -352,43 +350,25 @@ int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,
                        void* stream);
 
 /*
- * Execution controls of policy_fused_fwd_bwd, all owned by the caller (the
- * library keeps nothing between calls).
- *   side_stream  a hipStream_t of default priority, other than `stream`, or
- *                NULL.  When set, the HBM-bound second part of the in-place
- *                rescale runs there beside the first part of the dW product
- *                (fork_event is recorded on `stream` and waited for on
- *                side_stream; join_event is recorded on side_stream and
- *                waited for on `stream` before the rest of the products), so
- *                that all the call's work is complete in `stream` order when
- *                later work on `stream` runs.  The fork / join works under
- *                HIP graph capture of `stream` as well.  NULL: everything
- *                runs on `stream`, in order.
- *   fork_event, join_event  hipEvent_t (created by the caller, e.g. with
- *                hipEventDisableTiming); required when side_stream is set.
- *   phase_event[k]  hipEvent_t or NULL: recorded on `stream` when phase k of
- *                a chunk is done (RBP_PHASE_*), for timing the phases
- *                without a profiler; with several chunks a later record
- *                replaces an earlier one.  Leave them NULL under graph
- *                capture.
- * Two calls that may run at the same time need their own rbp_exec events
- * (a shared side stream only serialises their side work).
+ * Optional phase events of policy_fused_fwd_bwd, owned by the caller (the
+ * library keeps nothing between calls): phase_event[k], a hipEvent_t or
+ * NULL, is recorded on `stream` when phase k of a chunk is done
+ * (RBP_PHASE_*), for timing the phases without a profiler; with several
+ * chunks a later record replaces an earlier one.  Leave them NULL under
+ * graph capture.
  */
 enum {
   RBP_PHASE_START = 0,    /* before the chunk's first kernel                    */
-  RBP_PHASE_LOGITS = 1,   /* logit tile pass done (q stored, partial sums)      */
+  RBP_PHASE_LOGITS = 1,   /* target logits and the logit tile pass done         */
   RBP_PHASE_MERGE = 2,    /* lse, logp and entropy done                         */
   RBP_PHASE_LOSS = 3,     /* loss pass done (dlogp)                             */
-  RBP_PHASE_SCALE = 4,    /* the rescale's part on `stream` done                */
-  RBP_PHASE_DW = 5,       /* dW done (side stream joined)                       */
+  RBP_PHASE_SCALE = 4,    /* per-token scales, scaled hidden states done        */
+  RBP_PHASE_DW = 5,       /* dW done                                            */
   RBP_PHASE_DHIDDEN = 6,  /* dhidden done                                       */
   RBP_NUM_PHASES = 7
 };
 
 typedef struct rbp_exec {
-  void* side_stream;                  /* hipStream_t or NULL                    */
-  void* fork_event;                   /* hipEvent_t, needed with side_stream    */
-  void* join_event;                   /* hipEvent_t, needed with side_stream    */
   void* phase_event[RBP_NUM_PHASES];  /* hipEvent_t or NULL each                */
 } rbp_exec;
 
@@ -397,15 +377,19 @@ typedef struct rbp_exec {
  * plus the per-token entropy of the policy, H_t = -sum_v p_{t,v} log p_{t,v}
  * (the training entropy of App. E).  The separate calls execute 8 d V flop
  * per token because the backward recomputes the logits; this one executes the
- * 6 d V of the definition by keeping, per token, the forward tile pass's
- * exp(z - max) for every vocabulary entry as bf16 in the workspace (2 V bytes
- * per token; it does materialise a T x V array, which policy_logprob_fwd
- * never does).  The array is the one the backward's dz needs in any case:
- * exp(z - M) is turned into dz in place once the loss is known, so the
- * logits themselves never reach memory.  dz is rounded to bf16 twice instead
- * of once.
- * exec: NULL (all work on `stream`, in order) or the caller's rbp_exec
- * (side stream for the rescale overlap, phase events); see rbp_exec.
+ * 6 d V of the definition by keeping, per token and vocabulary entry, the
+ * forward tile pass's exponential exp(z - R_t) as bf16 in the workspace (2 V
+ * bytes per token: a T x V array, which policy_logprob_fwd never holds).  The
+ * per-token reference R_t = z_{t,y_t} - old_logp_t is the log-sum-exp the
+ * behaviour log-prob implies (lse_t - log rho_t), so the stored values are
+ * p_{t,v} / rho_t and the backward's dz is one scalar per token times them:
+ * the logits never reach memory and no pass over the array rescales it.
+ * A token whose R_t lies outside [M_t - 20, M_t + 40] (M_t its largest
+ * logit: a ratio below about e^-20 or above e^40, or an invalid old_logp)
+ * is re-referenced to M_t by a pass over its column alone.  dz is rounded to
+ * bf16 once (as exp(z - R_t)); the dW product reads h_t scaled by the token's
+ * factor, rounded to bf16.
+ * exec: NULL, or the caller's rbp_exec of phase events.
  * Arguments: hidden, W, tokens, seq_of_token as in policy_logprob_fwd
  * (seq_of_token required); old_logp, adv, seq_len, B, n_seq_total, eps_low,
  * eps_high, loss_accum, stats as in policy_loss_fwd_bwd (loss_accum and stats
@@ -416,15 +400,14 @@ typedef struct rbp_exec {
  * multiple of 256 (at most T rounded up to 256, at most 2^21) whose
  * rbp_workspace_bytes(RBP_OP_FUSED, Tc, d, V) fits in ws_bytes: with
  * Vp = V rounded up to 256, bf16 [Vp, Tc], fp32 [3 Vp / 128, Tc] partial
- * sums, fp32 [Tc, d] and the loss pass's sums -- 5.5 GB for Tc = 16384 at
+ * sums, five fp32 / int32 [Tc] arrays, bf16 [Tc, d] (scaled hidden states),
+ * fp32 [Tc, d] and the loss pass's sums -- 5.6 GB for Tc = 16384 at
  * d = 3584, V = 152064.
  * Errors: RBP_EINVAL (null pointers, T < 0, d < 1, V < 1, B < 1,
- *         n_seq_total < 1, eps < 0, a side stream without both events or
- *         equal to `stream`); RBP_EUNSUPPORTED (d % 8 != 0);
+ *         n_seq_total < 1, eps < 0); RBP_EUNSUPPORTED (d % 8 != 0);
  *         RBP_EWORKSPACE (not even a 256-token chunk fits); RBP_EHIP (a
- *         launch, event record or stream wait failed: earlier work may
- *         still be pending on `stream` and on the side stream, which the
- *         caller then synchronises before reusing any buffer).
+ *         launch or a phase-event record failed: earlier work may still be
+ *         pending on `stream`).
  */
 int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
                          const int32_t* tokens, const int32_t* seq_of_token,

@@ -39,7 +39,6 @@ from ._binding import (  # noqa: F401
     RBP_PHASE_MERGE,
     RBP_PHASE_SCALE,
     RBP_PHASE_START,
-    Overlap,
     RbpError,
     RbpExec,
     alloc_batch,

@@ -106,10 +106,7 @@ class RbBatch(ctypes.Structure):
 
 
 class RbpExec(ctypes.Structure):
-    _fields_ = [
-        ("side_stream", ctypes.c_void_p), ("fork_event", ctypes.c_void_p),
-        ("join_event", ctypes.c_void_p), ("phase_event", ctypes.c_void_p * RBP_NUM_PHASES),
-    ]
+    _fields_ = [("phase_event", ctypes.c_void_p * RBP_NUM_PHASES)]
 
 
 def load_library(path=LIB_PATH):
@@ -407,49 +404,25 @@ def _event_handle(ev, stream):
     return ev.cuda_event
 
 
-def make_exec(side_stream=None, fork_event=None, join_event=None, phase_events=None,
-              stream=None):
-    """rbp_exec from torch objects: a side torch.cuda.Stream with its two
-    torch.cuda.Events, and/or a list of RBP_NUM_PHASES timing events (None
-    entries allowed).  The struct holds references to them, so the raw
-    handles it carries stay valid while the struct is alive."""
+def make_exec(phase_events, stream=None):
+    """rbp_exec from a list of RBP_NUM_PHASES torch.cuda.Events (None entries
+    allowed).  The struct holds references to them, so the raw handles it
+    carries stay valid while the struct is alive."""
     ex = RbpExec()
     # torch destroys an event's HIP handle when the Python object goes away
-    ex._keep = (side_stream, fork_event, join_event, list(phase_events or ()))
+    ex._keep = list(phase_events)
     s = torch.cuda.current_stream() if stream is None else stream
-    if side_stream is not None:
-        if fork_event is None or join_event is None:
-            raise ValueError("a side stream needs fork_event and join_event")
-        ex.side_stream = side_stream.cuda_stream
-        ex.fork_event = _event_handle(fork_event, s)
-        ex.join_event = _event_handle(join_event, s)
-    for k, ev in enumerate(phase_events or ()):
+    for k, ev in enumerate(phase_events):
         if ev is not None:
             ex.phase_event[k] = _event_handle(ev, s)
     return ex
-
-
-class Overlap:
-    """A side stream and its fork / join events for policy_fused_fwd_bwd
-    (torch allocates them; the library only uses them)."""
-
-    def __init__(self, device=None):
-        self.stream = torch.cuda.Stream(device=device)
-        self.fork = torch.cuda.Event()
-        self.join = torch.cuda.Event()
-
-    def exec(self, phase_events=None, stream=None):
-        ex = make_exec(self.stream, self.fork, self.join, phase_events, stream)
-        ex._owner = self  # keeps the stream and events alive with the struct
-        return ex
 
 
 def policy_fused_fwd_bwd(hidden, W, tokens, seq_of_token, old_logp, adv, seq_len, n_seq_total,
                          logp, lse, entropy, loss_accum, dlogp, stats, dhidden, dW, ws,
                          accumulate_dW=False, eps_low=0.2, eps_high=0.2, exec=None,
                          stream=None):
-    """exec: None (all work on the stream, in order) or an RbpExec
-    (make_exec / Overlap.exec)."""
+    """exec: None or an RbpExec of phase events (make_exec)."""
     T, d = hidden.shape
     V = W.shape[0]
     B = adv.numel()

@@ -9,21 +9,36 @@
 //
 // The 4-call path recomputes the logit product in its backward, 8 d V flop per
 // token; this path executes the 6 d V of the definition by keeping the forward
-// tile pass's exponentials.  Per chunk of Tc tokens:
+// tile pass's exponentials, taken against a per-token reference R_t chosen
+// before the pass, so that dz becomes one scalar per token times the stored
+// values.  Per chunk of Tc tokens:
+//   0. R_t = z_{t,y_t} - old_logp_t, with the target logit as one dot
+//      product: the log-sum-exp the behaviour policy's probability implies,
+//      equal to lse_t - log rho_t (rho_t the importance ratio, close to 1 for
+//      a replayed token);
 //   1. Z^T = W H^T tile by tile.  For each token column and 128-row half tile
 //      i (one wave's rows), the epilogue writes the partial M_i = max z,
 //      S_i = sum exp(z - M_i), E_i = sum exp(z - M_i) z, and stores
-//      q = exp(z - M_i) as bf16 into Q^T [Vp][Tc] -- the layout the backward
-//      products read (dz^T);
-//   2. merge: lse and entropy from the partials, logp from one target dot
-//      product;
+//      q = exp(z - R_t) as bf16 into Q^T [Vp][Tc] (the layout the backward
+//      products read) -- or, where that would exceed exp(20) (M_i > R_t + 20),
+//      q = exp(z - M_i);
+//   2. merge: lse and entropy from the partials, logp from the target logit;
+//      a token is "referenced" when R_t lies in [M_t - 20, M_t + 40] (M_t its
+//      largest logit); the others -- a ratio below about e^-20 or above e^40,
+//      or an invalid behaviour log-prob -- are listed and take M_t as their
+//      reference instead;
 //   3. the loss pass writes dlogp (policy_loss_fwd_bwd);
-//   4. in place, q -> dz = -dlogp_t exp(M_i - lse_t) q, and each token's target
-//      entry -> dlogp_t (1 - exp(logp_t)) from the fp32 logp;
-//   5. dhidden and dW, the products of the 4-call backward.
+//   4. the listed tokens' columns of Q^T are re-referenced to M_t in place;
+//      then per token c_t = -dlogp_t exp(ref_t - lse_t), so that
+//      dz_{t,v} = c_t q_{t,v} off the target, and the target entry becomes
+//      q_{t,y} = dz_{t,y} / c_t = exp(lse_t - ref_t) (p_{t,y} - 1); and
+//      H' = c (.) H, row t of the hidden states scaled by c_t, in bf16;
+//   5. dW (+)= Q H' (sum over tokens of q_t (c_t h_t)^T) and
+//      dh_t = c_t (Q^T W)_t, the products of the 4-call backward with the
+//      per-token scale folded into an operand and into an epilogue.
 // Unlike policy_logprob_fwd this keeps a T x V array (2 V bytes per token, in
-// the workspace).  dz is rounded to bf16 twice (q, then the scaled value)
-// instead of once.
+// the workspace): exp(z - R_t), the backward's dz up to one factor per token.
+// dz is rounded to bf16 once, as q, and c_t h_t once more.
 
 #include "logits_epilogue.h"
 #include "rbp_internal.h"
@@ -54,12 +69,13 @@ __device__ __forceinline__ void column_max(const f32x16 (&acc)[GL::MI][GL::NI], 
   }
 }
 
-// q = exp(z - M) for four consecutive rows of one token, packed to bf16 pairs;
-// the fp32 q and q z are added to the column's sums (rows past the vocabulary
-// hold q = 0).
+// e = exp(z - M) for four consecutive rows of one token: the fp32 e and e z
+// are added to the column's sums, e f (f = exp(M - ref)) is packed to bf16
+// pairs (rows past the vocabulary hold 0).
 template <bool kFull>
-__device__ __forceinline__ void q_pack(const f32x16& acc, float ls, int mi, int rg, int32_t lim,
-                                       uint32_t& P0, uint32_t& P1, float& S, float& E) {
+__device__ __forceinline__ void q_pack(const f32x16& acc, float ls, float f, int mi, int rg,
+                                       int32_t lim, uint32_t& P0, uint32_t& P1, float& S,
+                                       float& E) {
   float q[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -71,22 +87,22 @@ __device__ __forceinline__ void q_pack(const f32x16& acc, float ls, int mi, int 
     S += q[i];
     E = fmaf(q[i], z, E);
   }
-  P0 = pack_bf16x2(q[0], q[1]);
-  P1 = pack_bf16x2(q[2], q[3]);
+  P0 = pack_bf16x2(q[0] * f, q[1] * f);
+  P1 = pack_bf16x2(q[2] * f, q[3] * f);
 }
 
 // dz_rows of the backward with q in place of dz, plus the sums.
 template <bool kFull>
 __device__ __forceinline__ void q_rows(const f32x16 (&acc)[GL::MI][GL::NI], const float (&ls)[2],
-                                       int mi, int32_t lim, const QuadSel& qs,
-                                       __amdgpu_buffer_rsrc_t rQ, uint32_t off, int64_t ldQ,
-                                       float (&S)[2], float (&E)[2]) {
+                                       const float (&f)[2], int mi, int32_t lim,
+                                       const QuadSel& qs, __amdgpu_buffer_rsrc_t rQ, uint32_t off,
+                                       int64_t ldQ, float (&S)[2], float (&E)[2]) {
   static_assert(GL::NI == 2, "two column blocks per wave");
 #pragma unroll
   for (int rg = 0; rg < 4; ++rg) {
     uint32_t X0, X1, Y0, Y1;
-    q_pack<kFull>(acc[mi][0], ls[0], mi, rg, lim, X0, X1, S[0], E[0]);
-    q_pack<kFull>(acc[mi][1], ls[1], mi, rg, lim, Y0, Y1, S[1], E[1]);
+    q_pack<kFull>(acc[mi][0], ls[0], f[0], mi, rg, lim, X0, X1, S[0], E[0]);
+    q_pack<kFull>(acc[mi][1], ls[1], f[1], mi, rg, lim, Y0, Y1, S[1], E[1]);
     const auto s0 = __builtin_amdgcn_permlane32_swap(X0, Y0, false, false);
     const auto s1 = __builtin_amdgcn_permlane32_swap(X1, Y1, false, false);
     uint32_t w0, w1;
@@ -99,14 +115,55 @@ __device__ __forceinline__ void q_rows(const f32x16 (&acc)[GL::MI][GL::NI], cons
   }
 }
 
+// A half tile stores against the token's reference R_t unless its largest
+// logit exceeds R_t by more than kRefAbove (q would pass exp(20)); a token
+// keeps R_t as its reference when R_t is within [M_t - kRefAbove,
+// M_t + kRefBelow] of its largest logit M_t (the top entries' q then stay in
+// [exp(-40), exp(20)] and c_t = -dlogp_t rho_t stays finite).  The same fp32
+// comparison is made wherever the decision is needed.
+constexpr float kRefAbove = 20.0f;
+constexpr float kRefBelow = 40.0f;
+
+__device__ __forceinline__ bool stores_against_ref(float m_half, float ref) {
+  return m_half - ref <= kRefAbove;  // false for a NaN reference
+}
+
+// Step 0: the target logit z_{t,y_t} (one wave per token, fp32 dot product)
+// and the reference R_t = z_{t,y_t} - old_logp_t for the tokens [0, T256);
+// masked and padding tokens get R = 0 and z = 0, an invalid target id z = NaN.
+// Also clears the count of tokens listed by the merge.
+__global__ void __launch_bounds__(256) target_ref_kernel(
+    const uint16_t* __restrict__ Hc, const uint16_t* __restrict__ W,
+    const int32_t* __restrict__ tokens, const int32_t* __restrict__ seq,
+    const float* __restrict__ old_logp, int64_t Tn, int64_t T256, int32_t d, int32_t V,
+    float* __restrict__ zy, float* __restrict__ R, int32_t* __restrict__ n_listed) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) *n_listed = 0;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= T256) return;
+  const bool valid = t < Tn && (seq == nullptr || seq[t] >= 0);
+  float z = 0.0f, r = 0.0f;
+  if (valid) {
+    const int32_t y = tokens[t];
+    z = (y >= 0 && y < V) ? dot_bf16_wave(Hc + t * d, W + (int64_t)y * d, d, lane) : NAN;
+    r = z - old_logp[t];
+  }
+  if (lane == 0) {
+    zy[t] = z;
+    R[t] = r;
+  }
+}
+
 // Step 1: logit tiles -> partials (M, S, E) per (half tile, token) and
-// q = exp(z - M) into Q^T.  One exponential per logit: a max pass, then the
-// store pass, which also sums q and q z.
+// q = exp(z - M) f into Q^T, f = exp(M - R_t) for a half tile stored against
+// the reference, else 1.  One exponential per logit: a max pass, then the
+// store pass, which also sums exp(z - M) and exp(z - M) z.
 RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
                                            const uint16_t* __restrict__ Hc, int64_t Tn,
-                                           int32_t d, int32_t V, float* __restrict__ pM,
-                                           float* __restrict__ pS, float* __restrict__ pE,
-                                           int64_t ldp, uint16_t* __restrict__ Qt, int64_t ldQ,
+                                           int32_t d, int32_t V, const float* __restrict__ Rc,
+                                           float* __restrict__ pM, float* __restrict__ pS,
+                                           float* __restrict__ pE, int64_t ldp,
+                                           uint16_t* __restrict__ Qt, int64_t ldQ,
                                            int64_t tiles_m, int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const Operand A{W, d, V, d};
@@ -119,6 +176,16 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
     map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupLogits, tm, tn);
     return Tile{tm * 256, tn * 256, 0, d};
   };
+  // the references of this lane's token columns, loaded one tile ahead
+  // (issued after an epilogue, used at the next one)
+  float Rr[GL::NI];
+  auto load_ref = [&](int32_t vid) {
+    const Tile tile = tile_of(vid);
+#pragma unroll
+    for (int ni = 0; ni < GL::NI; ++ni) Rr[ni] = Rc[tile.n0 + GL::col(ni)];
+  };
+  load_ref((int32_t)blockIdx.x);
+  const int32_t n_vid = (int32_t)(tiles_m * tiles_n);
   auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
     const Tile tile = tile_of(vid);
     const int32_t vlim = V - tile.m0;
@@ -129,10 +196,13 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
     else
       column_max<false>(acc, lim, mx);
     // a half tile past the vocabulary has M = -inf: offset 0 keeps its
-    // (discarded) exponentials finite
-    float ls[GL::NI], S[GL::NI] = {0.0f, 0.0f}, E[GL::NI] = {0.0f, 0.0f};
+    // (discarded) exponentials finite, and f = exp(-inf) = 0
+    float ls[GL::NI], f[GL::NI], S[GL::NI] = {0.0f, 0.0f}, E[GL::NI] = {0.0f, 0.0f};
 #pragma unroll
-    for (int ni = 0; ni < GL::NI; ++ni) ls[ni] = mx[ni] == -INFINITY ? 0.0f : mx[ni] * kLog2e;
+    for (int ni = 0; ni < GL::NI; ++ni) {
+      ls[ni] = mx[ni] == -INFINITY ? 0.0f : mx[ni] * kLog2e;
+      f[ni] = stores_against_ref(mx[ni], Rr[ni]) ? exp2_hw((mx[ni] - Rr[ni]) * kLog2e) : 1.0f;
+    }
     const auto rQ = __builtin_amdgcn_make_buffer_rsrc(
         uniform_ptr(Qt + (int64_t)tile.m0 * ldQ + tile.n0), 0, (int)(256 * ldQ * 2), 0x00020000);
     const uint32_t off =
@@ -141,9 +211,9 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
 #pragma unroll
     for (int mi = 0; mi < GL::MI; ++mi) {
       if (vlim >= 256)
-        q_rows<true>(acc, ls, mi, lim, qs, rQ, off, ldQ, S, E);
+        q_rows<true>(acc, ls, f, mi, lim, qs, rQ, off, ldQ, S, E);
       else
-        q_rows<false>(acc, ls, mi, lim, qs, rQ, off, ldQ, S, E);
+        q_rows<false>(acc, ls, f, mi, lim, qs, rQ, off, ldQ, S, E);
     }
     // both lane halves hold rows of the same columns; the lower half writes
     // the sums, 128 contiguous bytes per array and column block
@@ -159,8 +229,9 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
         pE[o] = e;
       }
     }
+    if (vid + (int32_t)gridDim.x < n_vid) load_ref(vid + (int32_t)gridDim.x);
   };
-  tile_stream<GL, false, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
+  tile_stream<GL, false, false>(A, B, n_vid, smem, tile_of, epi);
 }
 
 // (m, s, e) <- merge with the partial (Mi, Si, Ei), rescaling to the larger max.
@@ -181,23 +252,23 @@ __device__ __forceinline__ void merge_partial(float& m, float& s, float& e, floa
 
 // Step 2: 64 tokens per block of 16 waves.  Wave q merges the partials
 // i = q, q + 16, ... of the block's tokens (coalesced: consecutive lanes read
-// consecutive tokens), the 16 results are combined in a fixed order, then
-// each wave forms the target logits of 4 tokens with one dot product each.
+// consecutive tokens), the 16 results are combined in a fixed order by the
+// first wave, which writes lse, logp (from the step-0 target logit), the
+// entropy and the token's reference, and lists the tokens that cannot keep
+// R_t (order-free: the fix-up treats each listed token on its own).
 constexpr int kMergeTokens = 64;
 constexpr int kMergeWaves = 16;
 
 __global__ void __launch_bounds__(64 * kMergeWaves) fused_merge_kernel(
     const float* __restrict__ pM, const float* __restrict__ pS, const float* __restrict__ pE,
-    int64_t ldp, int32_t n_half, const uint16_t* __restrict__ Hc,
-    const uint16_t* __restrict__ W, const int32_t* __restrict__ tokens,
-    const int32_t* __restrict__ seq, int64_t Tn, int32_t d, int32_t V, float* __restrict__ logp,
-    float* __restrict__ lse, float* __restrict__ ent) {
+    int64_t ldp, int32_t n_half, const float* __restrict__ zy, const float* __restrict__ R,
+    const int32_t* __restrict__ seq, int64_t Tn, float* __restrict__ logp,
+    float* __restrict__ lse, float* __restrict__ ent, float* __restrict__ ref,
+    int32_t* __restrict__ listed, int32_t* __restrict__ n_listed) {
   __shared__ float sm[kMergeWaves][kMergeTokens], ss[kMergeWaves][kMergeTokens],
       se[kMergeWaves][kMergeTokens];
-  __shared__ float sl[kMergeTokens];
   const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
-  const int64_t t0 = (int64_t)blockIdx.x * kMergeTokens;
-  const int64_t t = t0 + c;
+  const int64_t t = (int64_t)blockIdx.x * kMergeTokens + c;
   float m = -INFINITY, s = 0.0f, e = 0.0f;
   if (t < Tn) {
     int32_t i = q;
@@ -218,102 +289,100 @@ __global__ void __launch_bounds__(64 * kMergeWaves) fused_merge_kernel(
   ss[q][c] = s;
   se[q][c] = e;
   __syncthreads();
-  if (threadIdx.x < kMergeTokens) {
-    float M = -INFINITY, S = 0.0f, E = 0.0f;
+  if (threadIdx.x >= kMergeTokens || t >= Tn) return;
+  float M = -INFINITY, S = 0.0f, E = 0.0f;
 #pragma unroll
-    for (int k = 0; k < kMergeWaves; ++k) merge_partial(M, S, E, sm[k][c], ss[k][c], se[k][c]);
-    const bool valid = t < Tn && (seq == nullptr || seq[t] >= 0);
-    const float l = M + logf(S);
-    sl[c] = valid ? l : 0.0f;
+  for (int k = 0; k < kMergeWaves; ++k) merge_partial(M, S, E, sm[k][c], ss[k][c], se[k][c]);
+  const bool valid = seq == nullptr || seq[t] >= 0;
+  const float l = M + logf(S);
+  lse[t] = valid ? l : 0.0f;
+  logp[t] = valid ? zy[t] - l : 0.0f;
+  if (ent != nullptr) ent[t] = valid ? l - E / S : 0.0f;
+  const float r = R[t];
+  const bool keeps = (M - r <= kRefAbove) && (r - M <= kRefBelow);  // false for NaN
+  ref[t] = keeps ? r : M;
+  if (valid && !keeps) listed[atomicAdd(n_listed, 1)] = (int32_t)t;
+}
+
+// Step 4a: the listed tokens' columns re-referenced to M_t in place.  Block b
+// owns the 128 vocabulary rows of half tile b (one row per thread) and walks
+// the list; each q is multiplied by exp(R_t - M_t) where its half tile was
+// stored against R_t, else by exp(M_b - M_t).  Rows whose stored value
+// underflowed stay 0 (their p is below exp(-87) of the reference's).
+__global__ void __launch_bounds__(128) fixup_kernel(uint16_t* __restrict__ Qt, int64_t ldQ,
+                                                    const float* __restrict__ pM, int64_t ldp,
+                                                    const float* __restrict__ R,
+                                                    const float* __restrict__ ref,
+                                                    const int32_t* __restrict__ listed,
+                                                    const int32_t* __restrict__ n_listed,
+                                                    int64_t Tn, int32_t V) {
+  const int32_t half = (int32_t)blockIdx.x;
+  const int32_t v = half * 128 + (int32_t)threadIdx.x;
+  int64_t n = *n_listed;
+  if (n > Tn) n = Tn;
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t t = listed[i];
+    const float Mb = pM[(int64_t)half * ldp + t], r = R[t], M = ref[t];
+    const float x = stores_against_ref(Mb, r) ? fminf((r - M) * kLog2e, 126.0f)
+                                              : (Mb - M) * kLog2e;
+    const float fct = exp2_hw(x);
+    if (v < V) {
+      uint16_t* p = Qt + (int64_t)v * ldQ + t;
+      *p = __builtin_bit_cast(uint16_t, (__bf16)(bf16_to_f32(*p) * fct));
+    }
+  }
+}
+
+// Step 4b: one block per token t < T256.  c_t = -dlogp_t exp(ref_t - lse_t)
+// (0 for masked and padding tokens); H'_t = c_t h_t in bf16; the target
+// entry q_{t,y} = exp(lse_t - ref_t) expm1(logp_t), so that c_t q_{t,y} =
+// dlogp_t (1 - p_{t,y}).
+__global__ void __launch_bounds__(256) token_scale_kernel(
+    const uint16_t* __restrict__ Hc, const int32_t* __restrict__ tokens,
+    const int32_t* __restrict__ seq, const float* __restrict__ lse,
+    const float* __restrict__ logp, const float* __restrict__ dlogp,
+    const float* __restrict__ ref, int64_t Tn, int32_t d, int32_t V, uint16_t* __restrict__ Hp,
+    float* __restrict__ cs, uint16_t* __restrict__ Qt, int64_t ldQ) {
+  const int64_t t = blockIdx.x;
+  const bool valid = t < Tn && (seq == nullptr || seq[t] >= 0);
+  const float c = valid ? -dlogp[t] * exp2_hw((ref[t] - lse[t]) * kLog2e) : 0.0f;
+  uint4* dst = reinterpret_cast<uint4*>(Hp + t * d);
+  const uint4* src = reinterpret_cast<const uint4*>(Hc + t * d);
+  for (int32_t k = threadIdx.x; k < d / 8; k += 256) {
+    uint4 o = make_uint4(0u, 0u, 0u, 0u);
     if (t < Tn) {
-      lse[t] = valid ? l : 0.0f;
-      if (ent != nullptr) ent[t] = valid ? l - E / S : 0.0f;
+      const uint4 h = src[k];
+      const uint32_t w[4] = {h.x, h.y, h.z, h.w};
+      uint32_t r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        r[j] = pack_bf16x2(c * bf16_to_f32((uint16_t)(w[j] & 0xffff)),
+                           c * bf16_to_f32((uint16_t)(w[j] >> 16)));
+      o = make_uint4(r[0], r[1], r[2], r[3]);
     }
+    dst[k] = o;
   }
-  __syncthreads();
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int k = 0; k < kMergeTokens / kMergeWaves; ++k) {
-    const int cc = q * (kMergeTokens / kMergeWaves) + k;
-    const int64_t tt = t0 + cc;
-    if (tt >= Tn) break;
-    if (seq != nullptr && seq[tt] < 0) {
-      if (lane == 0) logp[tt] = 0.0f;
-      continue;
-    }
-    const int32_t y = tokens[tt];
-    const bool y_ok = y >= 0 && y < V;
-    const float z = dot_bf16_wave(Hc + tt * d, W + (int64_t)(y_ok ? y : 0) * d, d, lane);
-    if (lane == 0) logp[tt] = y_ok ? z - sl[cc] : NAN;
-  }
-}
-
-// Step 4: one block per (128 vocabulary rows, 2048 tokens), eight tokens per
-// thread.  q -> -dlogp_t exp(M_i - lse_t) q in place; invalid tokens and the
-// padding columns Tn..T256 become zero; then the target entries.
-constexpr int kScaleTokens = 2048;
-
-template <int kRows>
-__device__ __forceinline__ void scale_rows(uint16_t* __restrict__ q, int64_t ldQ, int rows,
-                                           const float (&c)[8]) {
-#pragma unroll 8
-  for (int r = 0; r < (kRows > 0 ? kRows : rows); ++r) {
-    uint4* p = reinterpret_cast<uint4*>(q + r * ldQ);
-    const uint4 x = *p;
-    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-    uint32_t o[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      o[k] = pack_bf16x2(c[2 * k] * bf16_to_f32((uint16_t)(w[k] & 0xffff)),
-                         c[2 * k + 1] * bf16_to_f32((uint16_t)(w[k] >> 16)));
-    *p = make_uint4(o[0], o[1], o[2], o[3]);
-  }
-}
-
-__global__ void __launch_bounds__(256) grad_scale_kernel(
-    uint16_t* __restrict__ Qt, int64_t ldQ, int64_t T256, const float* __restrict__ pM,
-    int64_t ldp, const float* __restrict__ lse, const float* __restrict__ logp,
-    const float* __restrict__ dlogp, const int32_t* __restrict__ tokens,
-    const int32_t* __restrict__ seq, int64_t Tn, int32_t V, int32_t group0) {
-  const int64_t tb = (int64_t)blockIdx.x * kScaleTokens + threadIdx.x * 8;
-  const int32_t group = group0 + (int32_t)blockIdx.y;  // 128-row vocabulary group
-  const int32_t v0 = group * 128;
-  const int32_t rows = V - v0 < 128 ? V - v0 : 128;
-  if (tb >= T256 || rows <= 0) return;
-  const float* m = pM + (int64_t)group * ldp + tb;
-  float c[8], gy[8];
-  int32_t y[8];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int64_t t = tb + k;
-    const bool valid = t < Tn && (seq == nullptr || seq[t] >= 0);
-    c[k] = 0.0f;
-    gy[k] = 0.0f;
-    y[k] = -1;
+  if (threadIdx.x == 0) {
+    cs[t] = c;
     if (valid) {
-      const float dl = dlogp[t];
-      c[k] = -dl * exp2_hw((m[k] - lse[t]) * kLog2e);
-      gy[k] = -dl * expm1f(logp[t]);
-      y[k] = tokens[t];
+      const int32_t y = tokens[t];
+      if (y >= 0 && y < V)
+        Qt[(int64_t)y * ldQ + t] = __builtin_bit_cast(
+            uint16_t, (__bf16)(exp2_hw((lse[t] - ref[t]) * kLog2e) * expm1f(logp[t])));
     }
   }
-  uint16_t* q = Qt + (int64_t)v0 * ldQ + tb;
-  if (rows == 128)
-    scale_rows<128>(q, ldQ, rows, c);
-  else
-    scale_rows<0>(q, ldQ, rows, c);
-  // the target rows, written after this thread's own scaled stores to them
-#pragma unroll
-  for (int k = 0; k < 8; ++k)
-    if (y[k] >= v0 && y[k] < v0 + rows)
-      q[(int64_t)(y[k] - v0) * ldQ + k] = __builtin_bit_cast(uint16_t, (__bf16)gy[k]);
 }
 
 // Workspace: Q^T [Vp][Tc] bf16, partials M, S, E [Vp / 128][Tc] fp32, the
+// per-token target logit, reference R, chosen reference and scale [Tc] fp32,
+// the list of re-referenced tokens [Tc] and its count, H' [Tc][d] bf16, the
 // second dhidden K half [Tc][d] fp32, the loss pass's partial sums.
 struct FusedWs {
   uint16_t* Qt;
   float *pM, *pS, *pE;
+  float *zy, *R, *ref, *cs;
+  int32_t *listed, *n_listed;
+  uint16_t* Hp;
   float* dh_half;
   void* loss;
   size_t loss_bytes;
@@ -328,29 +397,18 @@ FusedWs carve_fused(void* base, int64_t Tc, int32_t d, int32_t V) {
   w.pM = c.take<float>((size_t)(Vp / 128) * (size_t)Tc);
   w.pS = c.take<float>((size_t)(Vp / 128) * (size_t)Tc);
   w.pE = c.take<float>((size_t)(Vp / 128) * (size_t)Tc);
+  w.zy = c.take<float>((size_t)Tc);
+  w.R = c.take<float>((size_t)Tc);
+  w.ref = c.take<float>((size_t)Tc);
+  w.cs = c.take<float>((size_t)Tc);
+  w.listed = c.take<int32_t>((size_t)Tc);
+  w.n_listed = c.take<int32_t>(1);
+  w.Hp = c.take<uint16_t>((size_t)Tc * (size_t)d);
   w.dh_half = c.take<float>((size_t)Tc * (size_t)d);
   w.loss_bytes = rbp::loss_ws(Tc);
   w.loss = c.take<uint8_t>(w.loss_bytes);
   w.bytes = rbp::align_up(c.used, 256);
   return w;
-}
-
-// Vocabulary tiles of the first dW part: the smallest multiple of the tiles
-// that make whole rounds of the persistent grid (tiles_d * tv0 % n_cu == 0)
-// that is at least a fifth of the vocabulary -- the rescale of the rest, run
-// beside it, then still finishes within it -- and leaves some tiles over; 0
-// when no such split exists.
-int64_t head_tiles(int64_t tiles_d, int64_t tiles_v, int n_cu) {
-  int64_t a = tiles_d, b = n_cu;
-  while (b != 0) {
-    const int64_t r = a % b;
-    a = b;
-    b = r;
-  }
-  const int64_t step = n_cu / a;
-  for (int64_t t = step; t < tiles_v; t += step)
-    if (5 * t >= tiles_v) return t;
-  return 0;
 }
 
 }  // namespace
@@ -391,11 +449,6 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
   RBP_REQUIRE(T == 0 || (hidden && tokens && seq_of_token && old_logp && logp && lse && dlogp &&
                          dhidden),
               RBP_EINVAL, "policy_fused_fwd_bwd: null per-token pointer");
-  const bool overlap = exec != nullptr && exec->side_stream != nullptr;
-  RBP_REQUIRE(!overlap || (exec->fork_event && exec->join_event), RBP_EINVAL,
-              "policy_fused_fwd_bwd: a side stream needs both fork_event and join_event");
-  RBP_REQUIRE(!overlap || exec->side_stream != stream, RBP_EINVAL,
-              "policy_fused_fwd_bwd: the side stream must differ from `stream`");
   hipStream_t s = rbp::as_stream(stream);
   if (T == 0) {
     rbp::launch_grad_products(nullptr, W, nullptr, 0, 0, d, V, nullptr, nullptr, dW,
@@ -420,17 +473,15 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
               "policy_fused_fwd_bwd: workspace of %zu bytes holds no 256-token chunk (needs %zu)",
               ws_bytes, rbp::fused_ws(256, d, V));
   const FusedWs w = carve_fused(ws, Tc, d, V);
-  hipStream_t side = overlap ? rbp::as_stream(exec->side_stream) : nullptr;
-  hipEvent_t fork = overlap ? reinterpret_cast<hipEvent_t>(exec->fork_event) : nullptr;
-  hipEvent_t join = overlap ? reinterpret_cast<hipEvent_t>(exec->join_event) : nullptr;
   const int64_t Vp = round256(V), tiles_v = Vp / 256;
   const int n_cu = device_cus();
   hipError_t e = hipSuccess;
-#define RBP_FUSED_HIP(call)                                                               \
+#define RBP_FUSED_MARK(k)                                                                 \
   do {                                                                                    \
-    e = (call);                                                                           \
+    e = mark(exec, (k), s);                                                               \
     if (e != hipSuccess) {                                                                \
-      rbp::set_error("policy_fused_fwd_bwd: %s: %s", #call, hipGetErrorString(e));        \
+      rbp::set_error("policy_fused_fwd_bwd: recording phase event %d: %s", (k),           \
+                     hipGetErrorString(e));                                               \
       return RBP_EHIP;                                                                    \
     }                                                                                     \
   } while (0)
@@ -439,61 +490,40 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
     const int64_t T256 = round256(Tn), tiles_t = T256 / 256;
     const uint16_t* Hc = hidden + t0 * d;
     const int32_t* sq = seq_of_token + t0;
-    RBP_FUSED_HIP(mark(exec, RBP_PHASE_START, s));
+    RBP_FUSED_MARK(RBP_PHASE_START);
+    hipLaunchKernelGGL(target_ref_kernel, dim3(rbp::ceil_div(T256, 4)), dim3(256), 0, s, Hc, W,
+                       tokens + t0, sq, old_logp + t0, Tn, T256, d, V, w.zy, w.R, w.n_listed);
     hipLaunchKernelGGL(logits_store_kernel, dim3(rbp::gemm::stream_grid(tiles_v * tiles_t, n_cu)),
-                       dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, w.pM, w.pS, w.pE, Tc, w.Qt, Tc,
-                       tiles_v, tiles_t);
-    RBP_FUSED_HIP(mark(exec, RBP_PHASE_LOGITS, s));
-    hipLaunchKernelGGL(fused_merge_kernel, dim3(rbp::ceil_div(Tn, kMergeTokens)),
-                       dim3(64 * kMergeWaves), 0, s,
-                       w.pM, w.pS, w.pE, Tc, (int32_t)(Vp / 128), Hc, W, tokens + t0, sq, Tn, d, V,
-                       logp + t0, lse + t0, entropy ? entropy + t0 : nullptr);
+                       dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, w.R, w.pM, w.pS, w.pE, Tc,
+                       w.Qt, Tc, tiles_v, tiles_t);
     RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
-    RBP_FUSED_HIP(mark(exec, RBP_PHASE_MERGE, s));
+    RBP_FUSED_MARK(RBP_PHASE_LOGITS);
+    hipLaunchKernelGGL(fused_merge_kernel, dim3(rbp::ceil_div(Tn, kMergeTokens)),
+                       dim3(64 * kMergeWaves), 0, s, w.pM, w.pS, w.pE, Tc, (int32_t)(Vp / 128),
+                       w.zy, w.R, sq, Tn, logp + t0, lse + t0, entropy ? entropy + t0 : nullptr,
+                       w.ref, w.listed, w.n_listed);
+    RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+    RBP_FUSED_MARK(RBP_PHASE_MERGE);
     const int st = policy_loss_fwd_bwd(logp + t0, old_logp + t0, sq, adv, seq_len, Tn, B,
                                        n_seq_total, eps_low, eps_high, loss_accum, dlogp + t0,
                                        stats, w.loss, w.loss_bytes, stream);
     if (st != RBP_OK) return st;
-    RBP_FUSED_HIP(mark(exec, RBP_PHASE_LOSS, s));
-    const int acc = (accumulate_dW || t0 > 0) ? 1 : 0;
-    const unsigned gx = (unsigned)rbp::ceil_div(T256, kScaleTokens);
-    const int64_t tv0 = overlap ? head_tiles(rbp::ceil_div(d, 256), tiles_v, n_cu) : 0;
-    if (tv0 > 0) {
-      // rescale rows [0, 256 tv0); then, on the side stream, the rest while
-      // dW runs over the first tv0 vocabulary tiles; dW of the rest and
-      // dhidden once both parts are done
-      const int32_t g0 = (int32_t)(tv0 * 2);  // 128-row groups in the head
-      hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)g0), dim3(256), 0, s, w.Qt, Tc,
-                         T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0, tokens + t0, sq, Tn, V,
-                         0);
-      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
-      RBP_FUSED_HIP(mark(exec, RBP_PHASE_SCALE, s));
-      RBP_FUSED_HIP(hipEventRecord(fork, s));
-      RBP_FUSED_HIP(hipStreamWaitEvent(side, fork, 0));
-      hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)(Vp / 128 - g0)), dim3(256), 0,
-                         side, w.Qt, Tc, T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0,
-                         tokens + t0, sq, Tn, V, g0);
-      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
-      RBP_FUSED_HIP(hipEventRecord(join, side));
-      rbp::launch_dweight(Hc, w.Qt, Tc, Tn, d, V, dW, acc, 0, tv0, s);
-      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
-      RBP_FUSED_HIP(hipStreamWaitEvent(s, join, 0));
-      rbp::launch_dweight(Hc, w.Qt, Tc, Tn, d, V, dW, acc, tv0, tiles_v, s);
-      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
-    } else {
-      hipLaunchKernelGGL(grad_scale_kernel, dim3(gx, (unsigned)(Vp / 128)), dim3(256), 0, s,
-                         w.Qt, Tc, T256, w.pM, Tc, lse + t0, logp + t0, dlogp + t0, tokens + t0,
-                         sq, Tn, V, 0);
-      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
-      RBP_FUSED_HIP(mark(exec, RBP_PHASE_SCALE, s));
-      rbp::launch_dweight(Hc, w.Qt, Tc, Tn, d, V, dW, acc, 0, tiles_v, s);
-      RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
-    }
-    RBP_FUSED_HIP(mark(exec, RBP_PHASE_DW, s));
-    rbp::launch_dhidden(W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, s);
+    RBP_FUSED_MARK(RBP_PHASE_LOSS);
+    hipLaunchKernelGGL(fixup_kernel, dim3((unsigned)(Vp / 128)), dim3(128), 0, s, w.Qt, Tc, w.pM,
+                       Tc, w.R, w.ref, w.listed, w.n_listed, Tn, V);
+    hipLaunchKernelGGL(token_scale_kernel, dim3((unsigned)T256), dim3(256), 0, s, Hc,
+                       tokens + t0, sq, lse + t0, logp + t0, dlogp + t0, w.ref, Tn, d, V, w.Hp,
+                       w.cs, w.Qt, Tc);
     RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
-    RBP_FUSED_HIP(mark(exec, RBP_PHASE_DHIDDEN, s));
+    RBP_FUSED_MARK(RBP_PHASE_SCALE);
+    const int acc = (accumulate_dW || t0 > 0) ? 1 : 0;
+    rbp::launch_dweight(w.Hp, w.Qt, Tc, Tn, d, V, dW, acc, 0, tiles_v, s);
+    RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+    RBP_FUSED_MARK(RBP_PHASE_DW);
+    rbp::launch_dhidden(W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, s, w.cs);
+    RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
+    RBP_FUSED_MARK(RBP_PHASE_DHIDDEN);
   }
-#undef RBP_FUSED_HIP
+#undef RBP_FUSED_MARK
   return RBP_OK;
 }

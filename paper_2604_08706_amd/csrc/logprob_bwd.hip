@@ -118,8 +118,9 @@ __global__ void __launch_bounds__(256) target_dz_kernel(
 RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
                                       const uint16_t* __restrict__ Gt, int64_t ldGt, int64_t Tn,
                                       int32_t d, int32_t V, int64_t k_split, int splits,
-                                      float* __restrict__ out0, float* __restrict__ out1,
-                                      int64_t tiles_m, int64_t tiles_n) {
+                                      const float* __restrict__ cs, float* __restrict__ out0,
+                                      float* __restrict__ out1, int64_t tiles_m,
+                                      int64_t tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int64_t T256 = (Tn + 255) / 256 * 256;
   const Operand A{W, d, d, V};          // (m = hidden unit, k = vocab): W[v][m]
@@ -141,6 +142,7 @@ RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
     for (int ni = 0; ni < GL::NI; ++ni) {
       const int64_t t = tile.n0 + GL::col(ni);
       if (t >= Tn) continue;
+      const float c = cs != nullptr ? cs[t] : 1.0f;  // per-token scale of the single pass
 #pragma unroll
       for (int mi = 0; mi < GL::MI; ++mi)
 #pragma unroll
@@ -148,8 +150,8 @@ RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
           const int64_t m = tile.m0 + GL::row(mi, rg * 4);
           if (m < d)
             *reinterpret_cast<float4*>(dH + t * d + m) =
-                make_float4(acc[mi][ni][rg * 4 + 0], acc[mi][ni][rg * 4 + 1],
-                            acc[mi][ni][rg * 4 + 2], acc[mi][ni][rg * 4 + 3]);
+                make_float4(c * acc[mi][ni][rg * 4 + 0], c * acc[mi][ni][rg * 4 + 1],
+                            c * acc[mi][ni][rg * 4 + 2], c * acc[mi][ni][rg * 4 + 3]);
         }
     }
   };
@@ -287,7 +289,8 @@ void rbp::launch_dweight(const uint16_t* Hc, const uint16_t* Gt, int64_t ldGt, i
 }
 
 void rbp::launch_dhidden(const uint16_t* W, const uint16_t* Gt, int64_t ldGt, int64_t Tn,
-                         int32_t d, int32_t V, float* dhidden_c, float* dh_half, hipStream_t s) {
+                         int32_t d, int32_t V, float* dhidden_c, float* dh_half, hipStream_t s,
+                         const float* cs) {
   const int n_cu = device_cus();
   const int64_t tiles_d = rbp::ceil_div(d, 256), tiles_t = rbp::ceil_div(Tn, 256);
   // dhidden in two K halves when one pass would give each CU only a few
@@ -296,8 +299,8 @@ void rbp::launch_dhidden(const uint16_t* W, const uint16_t* Gt, int64_t ldGt, in
   const int splits = tiles_dh < 4 * (int64_t)n_cu && V >= 512 ? 2 : 1;
   const int64_t k_split = splits == 2 ? (rbp::ceil_div(V, 2) + 63) / 64 * 64 : V;
   hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(tiles_dh * splits, n_cu)),
-                     dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, k_split, splits, dhidden_c,
-                     dh_half, tiles_d, tiles_t);
+                     dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, k_split, splits, cs,
+                     dhidden_c, dh_half, tiles_d, tiles_t);
   if (splits == 2) {
     const int64_t n4 = Tn * d / 4;
     int64_t blocks = rbp::ceil_div(n4, 256);

@@ -50,12 +50,14 @@ void launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint16_t*
                           int64_t ldGt, int64_t Tn, int32_t d, int32_t V, float* dhidden_c,
                           float* dh_half, float* dW, int accumulate, hipStream_t s);
 // Its two parts: dW rows of the vocabulary tiles [tn_begin, tn_end) (256 rows
-// each), and dhidden (with its split-K sum).
+// each), and dhidden (with its split-K sum; row t scaled by cs[t] when cs is
+// given).
 void launch_dweight(const uint16_t* Hc, const uint16_t* Gt, int64_t ldGt, int64_t Tn, int32_t d,
                     int32_t V, float* dW, int accumulate, int64_t tn_begin, int64_t tn_end,
                     hipStream_t s);
 void launch_dhidden(const uint16_t* W, const uint16_t* Gt, int64_t ldGt, int64_t Tn, int32_t d,
-                    int32_t V, float* dhidden_c, float* dh_half, hipStream_t s);
+                    int32_t V, float* dhidden_c, float* dh_half, hipStream_t s,
+                    const float* cs = nullptr);
 
 }  // namespace rbp
 

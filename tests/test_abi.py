@@ -74,11 +74,14 @@ def test_status_strings_and_workspace_sizes():
     # tile and token (tokens rounded up to 256)
     assert lib.rbp_workspace_bytes(b.RBP_OP_LOGPROB_FWD, 100, 64, 513) == 256 * 6 * 8
     assert lib.rbp_workspace_bytes(b.RBP_OP_LOSS, 10, 0, 0) > 0
-    # fused workspace: exp(z - max) bf16 [Vp, Tc], (max, sum, sum z) fp32
-    # [Vp / 128, Tc] each, the dhidden K half and the loss pass's sums
+    # fused workspace: exp(z - R) bf16 [Vp, Tc], (max, sum, sum z) fp32
+    # [Vp / 128, Tc] each, five per-token arrays [Tc] (target logit, R,
+    # reference, scale, list) and the list's count, the scaled hidden states
+    # bf16 [Tc, d], the dhidden K half and the loss pass's sums
     loss = lib.rbp_workspace_bytes(b.RBP_OP_LOSS, 16384, 0, 0)
     assert lib.rbp_workspace_bytes(b.RBP_OP_FUSED, 16384, 3584, 152064) == \
-        152064 * 16384 * 2 + 3 * 1188 * 16384 * 4 + 16384 * 3584 * 4 + (loss + 255) // 256 * 256
+        152064 * 16384 * 2 + 3 * 1188 * 16384 * 4 + 5 * 16384 * 4 + 256 + \
+        16384 * 3584 * 2 + 16384 * 3584 * 4 + (loss + 255) // 256 * 256
     assert lib.rbp_workspace_bytes(b.RBP_OP_SAMPLE_GATHER, 1_000_000, 0, 0) >= 4_000_000
 
 

@@ -148,8 +148,7 @@ def test_dense_single_pass(case):
     rbp.policy_fused_fwd_bwd(dev["hidden"], dev["W"], dev["tokens"], dev["seq"], dev["old"],
                              dev["adv"], dev["lens"], dev["lens"].numel(), out["logp"],
                              out["lse"], out["ent"], out["loss"], out["dlogp"], out["stats"],
-                             out["dh"], out["dW"], rbp.workspace(rbp.RBP_OP_FUSED, T, d, V),
-                             exec=rbp.Overlap().exec())
+                             out["dh"], out["dW"], rbp.workspace(rbp.RBP_OP_FUSED, T, d, V))
     torch.cuda.synchronize()
     _check(out, want, T, V, with_entropy=True)
     del out

@@ -33,37 +33,17 @@ def _sequences(T, seed, masked=0.1, mean_len=40):
     return seq, np.array(lens, dtype=np.int32)
 
 
-_OVERLAP = {}
-
-
-def _overlap(rbp):
-    """One side stream with its events per thread (calls that may run at the
-    same time need their own)."""
-    import threading
-
-    key = threading.get_ident()
-    if key not in _OVERLAP:
-        _OVERLAP[key] = rbp.Overlap()
-    return _OVERLAP[key]
-
-
 def _run(rbp, hidden, W, tokens, seq, old, adv, slen, n_seq, ws_tokens=None, dW0=None,
-         want_entropy=True, overlap=True, phase_events=None):
+         want_entropy=True, ex=None, loss0=0.25):
     T, d = hidden.shape
     V = W.shape[0]
     out = {k: torch.empty(T, device="cuda") for k in ("logp", "lse", "dlogp")}
     out["entropy"] = torch.empty(T, device="cuda") if want_entropy else None
-    out["loss"] = torch.full((1,), 0.25, device="cuda")
+    out["loss"] = torch.full((1,), loss0, device="cuda")
     out["stats"] = torch.zeros(4, device="cuda")
     out["dh"] = torch.empty((T, d), device="cuda")
     out["dW"] = torch.empty((V, d), device="cuda") if dW0 is None else dW0.clone()
     ws = rbp.workspace(rbp.RBP_OP_FUSED, T if ws_tokens is None else ws_tokens, d, V)
-    if isinstance(overlap, rbp.RbpExec):
-        ex = overlap
-    elif overlap:
-        ex = _overlap(rbp).exec(phase_events)
-    else:
-        ex = rbp.make_exec(phase_events=phase_events) if phase_events else None
     rbp.policy_fused_fwd_bwd(hidden, W, tokens, seq, old, adv, slen, n_seq, out["logp"],
                              out["lse"], out["entropy"], out["loss"], out["dlogp"],
                              out["stats"], out["dh"], out["dW"], ws,
@@ -228,13 +208,13 @@ def test_fused_reproducible_empty_and_bad_args():
 
 
 def test_fused_concurrent_calls_on_two_streams():
-    """Two host threads run the single pass on their own streams at once, each
-    with its own side stream and events; every result must equal the same call
-    made alone."""
+    """Two host threads run the single pass on their own streams at once (the
+    library holds no state between calls); every result must equal the same
+    call made alone."""
     import threading
 
     rbp = require_gpu()
-    T, d, V = 2048, 512, 70000  # large enough that the overlapped path runs
+    T, d, V = 2048, 512, 70000
     cases = []
     for seed in (31, 32):
         (hidden, W, tokens, seq, lens, *_r) = _case(T, d, V, 0.02, seed, device="cuda")
@@ -331,65 +311,68 @@ def test_fused_three_chunks_with_sequences_across_chunk_boundaries():
     torch.cuda.empty_cache()
 
 
-def test_fused_overlap_serial_and_phase_events_agree():
-    """The side-stream overlap only reorders independent work: results are
-    bit-identical to the serial call (exec = NULL).  Phase events recorded on
-    the caller's stream bracket every phase, in order."""
+def test_fused_phase_events():
+    """Phase events recorded on the caller's stream bracket every phase in
+    order and change no result; an rbp_exec keeps its torch events alive."""
+    import gc
+
     rbp = require_gpu()
-    T, d, V = 2048, 512, 70000  # large enough that the overlapped path runs
+    T, d, V = 2048, 512, 70000
     (hidden, W, tokens, seq, lens, *_r) = _case(T, d, V, 0.02, 41, device="cuda")
     old, adv = _r[-2], _r[-1]
     args = (rbp, hidden, W, tokens, torch.from_numpy(seq).cuda(), torch.from_numpy(old).cuda(),
             torch.from_numpy(adv).cuda(), torch.from_numpy(lens).cuda(), len(lens))
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(rbp.RBP_NUM_PHASES)]
-    a = _run(*args, overlap=True, phase_events=evs)
+    ex = rbp.make_exec([torch.cuda.Event(enable_timing=True) for _ in range(rbp.RBP_NUM_PHASES)])
+    evs = ex._keep
+    gc.collect()
+    a = _run(*args, ex=ex)
     ms = [evs[k].elapsed_time(evs[k + 1]) for k in range(rbp.RBP_NUM_PHASES - 1)]
     assert all(m >= 0.0 for m in ms) and sum(ms) > 0.0, ms
-    b = _run(*args, overlap=False)
-    c = _run(*args, overlap=False, phase_events=evs[:3] + [None] * 4)
+    b = _run(*args)
+    c = _run(*args, ex=rbp.make_exec(evs[:3] + [None] * 4))
     for key in ("logp", "lse", "entropy", "loss", "dlogp", "stats", "dh", "dW"):
         assert torch.equal(a[key], b[key]), key
         assert torch.equal(a[key], c[key]), key
 
 
-def test_fused_rejects_bad_exec():
+@pytest.mark.parametrize("shift,adv_sign", [(35.0, 1.0), (-45.0, -1.0), ("mixed", 0.0)])
+def test_fused_tokens_off_their_reference(shift, adv_sign):
+    """Tokens whose behaviour log-prob puts the reference R_t far from their
+    largest logit take the re-referencing path: old = logp + 35 (ratio e^-35,
+    positive advantages, so a tiny but unclipped gradient) or old = logp - 45
+    (ratio e^45, negative advantages: an unclipped gradient e^45 times the
+    usual).  'mixed': half the sequences shifted by +35, the rest ordinary, so
+    the pass must leave the ordinary tokens' columns alone.  Everything
+    against the oracle at the usual bars; in the mixed case dhidden is also
+    checked on each group's rows alone."""
     rbp = require_gpu()
-    T, d, V = 256, 64, 1000
-    (hidden, W, tokens, seq, lens, *_r) = _case(T, d, V, 0.02, 43, device="cuda")
-    old, adv = _r[-2], _r[-1]
-    f = lambda t: torch.empty(t, device="cuda")  # noqa: E731
-    ws = rbp.workspace(rbp.RBP_OP_FUSED, T, d, V)
-    bad = rbp.RbpExec()
-    bad.side_stream = torch.cuda.Stream().cuda_stream  # no events
-    st = torch.cuda.Stream()  # the default stream's handle is NULL, i.e. "no side stream"
-    same = rbp.make_exec(st, torch.cuda.Event(), torch.cuda.Event(), stream=st)
-    for ex in (bad, same):
-        with pytest.raises(rbp.RbpError) as e:
-            rbp.policy_fused_fwd_bwd(hidden, W, tokens, torch.from_numpy(seq).cuda(),
-                                     torch.from_numpy(old).cuda(), torch.from_numpy(adv).cuda(),
-                                     torch.from_numpy(lens).cuda(), len(lens), f(T), f(T), None,
-                                     torch.zeros(1, device="cuda"), f(T),
-                                     torch.zeros(4, device="cuda"), f(T * d), f(V * d), ws,
-                                     exec=ex, stream=st)
-        assert e.value.status == rbp.RBP_EINVAL
-
-
-def test_fused_exec_outlives_its_temporaries():
-    """An rbp_exec built from a temporary Overlap keeps the torch stream and
-    events it points to alive (torch frees an event's handle with the Python
-    object), so a later call may use it."""
-    import gc
-
-    rbp = require_gpu()
-    T, d, V = 2048, 512, 70000  # large enough that the overlapped path runs
-    (hidden, W, tokens, seq, lens, *_r) = _case(T, d, V, 0.02, 47, device="cuda")
-    old, adv = _r[-2], _r[-1]
-    args = (rbp, hidden, W, tokens, torch.from_numpy(seq).cuda(), torch.from_numpy(old).cuda(),
-            torch.from_numpy(adv).cuda(), torch.from_numpy(lens).cuda(), len(lens))
-    ex = rbp.Overlap().exec([torch.cuda.Event(enable_timing=True)
-                             for _ in range(rbp.RBP_NUM_PHASES)])
-    gc.collect()
-    a = _run(*args, overlap=ex)
-    b = _run(*args, overlap=False)
-    for key in ("logp", "dlogp", "dh", "dW"):
-        assert torch.equal(a[key], b[key]), key
+    T, d, V = 700, 136, 4097
+    (hidden, W, tokens, seq, lens, h64, W64, y, want_logp, want_lse, old,
+     adv) = _case(T, d, V, 0.02, 53)
+    rng = np.random.default_rng(54)
+    B = len(lens)
+    if shift == "mixed":
+        shifted = rng.random(B) < 0.5
+        adv = np.where(shifted, np.abs(adv), adv)
+        tok_shift = np.where((seq >= 0) & shifted[np.maximum(seq, 0)], 35.0, 0.0)
+    else:
+        adv = adv_sign * np.abs(adv) + adv_sign * 0.1
+        tok_shift = np.full(T, shift)
+    old = (want_logp + tok_shift + rng.normal(0, 0.05, T)).astype(np.float32)
+    print(f"[fused] off-reference tokens shift={shift}", flush=True)
+    out = _run(rbp, hidden.cuda(), W.cuda(), tokens.cuda(), torch.from_numpy(seq).cuda(),
+               torch.from_numpy(old).cuda(), torch.from_numpy(adv.astype(np.float32)).cuda(),
+               torch.from_numpy(lens).cuda(), B, loss0=0.0)
+    assert np.abs(to_np(out["logp"]) - want_logp).max() < ATOL
+    assert np.abs(to_np(out["lse"]) - want_lse).max() < ATOL
+    loss, dlogp, _ = grpo_loss(want_logp, old, seq, adv, lens, B)
+    assert abs(to_np(out["loss"])[0] - loss) <= RTOL * abs(loss)
+    assert rel_l2(to_np(out["dlogp"]), dlogp) < RTOL
+    want_dh, want_dW = logprob_backward(h64, W64, y, want_lse, dlogp, seq)
+    dh, dW = to_np(out["dh"]), to_np(out["dW"])
+    assert np.all(np.isfinite(dh)) and np.all(np.isfinite(dW))
+    assert rel_l2(dh, want_dh) < RTOL
+    assert rel_l2(dW, want_dW) < RTOL
+    if shift == "mixed":
+        for grp in (tok_shift > 0, (tok_shift == 0) & (seq >= 0)):
+            assert rel_l2(dh[grp], want_dh[grp]) < RTOL
