@@ -561,14 +561,15 @@ def spread(xs):
 PHASES = ("logits", "merge", "loss", "scale", "dW", "dhidden")  # the RBP_PHASE_* order
 
 
-def fused_leg(rbp, wl, S, out, first_step, steps, warmup, ws_tokens=None):
+def fused_leg(rbp, wl, S, out, first_step, steps, warmup, ws_tokens=None, entropy=True):
     """Time the single pass over `steps` sampled batches (after `warmup`),
     with the call's phase events recorded on the caller's stream.  ws_tokens:
-    size the workspace for that many tokens (the call then runs in chunks)."""
+    size the workspace for that many tokens (the call then runs in chunks).
+    entropy: also compute the per-token entropy."""
     import torch
 
     T = S["T"]
-    S["entropy"] = torch.empty(T, device="cuda")
+    S["entropy"] = torch.empty(T, device="cuda") if entropy else None
     S["ws_fused"] = rbp.workspace(rbp.RBP_OP_FUSED, ws_tokens or T, wl.d, wl.V)
     for k in range(warmup):
         run_step_fused(rbp, wl, S, first_step + k, out, None)

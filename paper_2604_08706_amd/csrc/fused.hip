@@ -72,7 +72,7 @@ __device__ __forceinline__ void column_max(const f32x16 (&acc)[GL::MI][GL::NI], 
 // e = exp(z - M) for four consecutive rows of one token: the fp32 e and e z
 // are added to the column's sums, e f (f = exp(M - ref)) is packed to bf16
 // pairs (rows past the vocabulary hold 0).
-template <bool kFull>
+template <bool kFull, bool kEnt>
 __device__ __forceinline__ void q_pack(const f32x16& acc, float ls, float f, int mi, int rg,
                                        int32_t lim, uint32_t& P0, uint32_t& P1, float& S,
                                        float& E) {
@@ -85,14 +85,14 @@ __device__ __forceinline__ void q_pack(const f32x16& acc, float ls, float f, int
       q[i] = __uint_as_float(select_below(GL::row_off(mi, rg * 4 + i), lim,
                                           __float_as_uint(q[i]), 0u));
     S += q[i];
-    E = fmaf(q[i], z, E);
+    if constexpr (kEnt) E = fmaf(q[i], z, E);
   }
   P0 = pack_bf16x2(q[0] * f, q[1] * f);
   P1 = pack_bf16x2(q[2] * f, q[3] * f);
 }
 
 // dz_rows of the backward with q in place of dz, plus the sums.
-template <bool kFull>
+template <bool kFull, bool kEnt>
 __device__ __forceinline__ void q_rows(const f32x16 (&acc)[GL::MI][GL::NI], const float (&ls)[2],
                                        const float (&f)[2], int mi, int32_t lim,
                                        const QuadSel& qs, __amdgpu_buffer_rsrc_t rQ, uint32_t off,
@@ -101,8 +101,8 @@ __device__ __forceinline__ void q_rows(const f32x16 (&acc)[GL::MI][GL::NI], cons
 #pragma unroll
   for (int rg = 0; rg < 4; ++rg) {
     uint32_t X0, X1, Y0, Y1;
-    q_pack<kFull>(acc[mi][0], ls[0], f[0], mi, rg, lim, X0, X1, S[0], E[0]);
-    q_pack<kFull>(acc[mi][1], ls[1], f[1], mi, rg, lim, Y0, Y1, S[1], E[1]);
+    q_pack<kFull, kEnt>(acc[mi][0], ls[0], f[0], mi, rg, lim, X0, X1, S[0], E[0]);
+    q_pack<kFull, kEnt>(acc[mi][1], ls[1], f[1], mi, rg, lim, Y0, Y1, S[1], E[1]);
     const auto s0 = __builtin_amdgcn_permlane32_swap(X0, Y0, false, false);
     const auto s1 = __builtin_amdgcn_permlane32_swap(X1, Y1, false, false);
     uint32_t w0, w1;
@@ -157,7 +157,9 @@ __global__ void __launch_bounds__(256) target_ref_kernel(
 // Step 1: logit tiles -> partials (M, S, E) per (half tile, token) and
 // q = exp(z - M) f into Q^T, f = exp(M - R_t) for a half tile stored against
 // the reference, else 1.  One exponential per logit: a max pass, then the
-// store pass, which also sums exp(z - M) and exp(z - M) z.
+// store pass, which also sums exp(z - M) and, when the entropy is wanted
+// (kEnt), exp(z - M) z.
+template <bool kEnt>
 RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
                                            const uint16_t* __restrict__ Hc, int64_t Tn,
                                            int32_t d, int32_t V, const float* __restrict__ Rc,
@@ -211,9 +213,9 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
 #pragma unroll
     for (int mi = 0; mi < GL::MI; ++mi) {
       if (vlim >= 256)
-        q_rows<true>(acc, ls, f, mi, lim, qs, rQ, off, ldQ, S, E);
+        q_rows<true, kEnt>(acc, ls, f, mi, lim, qs, rQ, off, ldQ, S, E);
       else
-        q_rows<false>(acc, ls, f, mi, lim, qs, rQ, off, ldQ, S, E);
+        q_rows<false, kEnt>(acc, ls, f, mi, lim, qs, rQ, off, ldQ, S, E);
     }
     // both lane halves hold rows of the same columns; the lower half writes
     // the sums, 128 contiguous bytes per array and column block
@@ -221,12 +223,12 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
 #pragma unroll
     for (int ni = 0; ni < GL::NI; ++ni) {
       const float s = S[ni] + __shfl_xor(S[ni], 32, 64);
-      const float e = E[ni] + __shfl_xor(E[ni], 32, 64);
+      const float e = kEnt ? E[ni] + __shfl_xor(E[ni], 32, 64) : 0.0f;
       if (lane < 32) {
         const int64_t o = half * ldp + tile.n0 + GL::col(ni);
         pM[o] = mx[ni];
         pS[o] = s;
-        pE[o] = e;
+        if (kEnt) pE[o] = e;
       }
     }
     if (vid + (int32_t)gridDim.x < n_vid) load_ref(vid + (int32_t)gridDim.x);
@@ -273,16 +275,17 @@ __global__ void __launch_bounds__(64 * kMergeWaves) fused_merge_kernel(
   if (t < Tn) {
     int32_t i = q;
     // two partials per iteration: their loads are issued together
+    // pE is read only when the entropy is wanted (the tile pass wrote it)
     for (; i + kMergeWaves < n_half; i += 2 * kMergeWaves) {
       const int64_t o0 = (int64_t)i * ldp + t, o1 = o0 + (int64_t)kMergeWaves * ldp;
-      const float M0 = pM[o0], S0 = pS[o0], E0 = pE[o0];
-      const float M1 = pM[o1], S1 = pS[o1], E1 = pE[o1];
+      const float M0 = pM[o0], S0 = pS[o0], E0 = ent ? pE[o0] : 0.0f;
+      const float M1 = pM[o1], S1 = pS[o1], E1 = ent ? pE[o1] : 0.0f;
       merge_partial(m, s, e, M0, S0, E0);
       merge_partial(m, s, e, M1, S1, E1);
     }
     if (i < n_half) {
       const int64_t o = (int64_t)i * ldp + t;
-      merge_partial(m, s, e, pM[o], pS[o], pE[o]);
+      merge_partial(m, s, e, pM[o], pS[o], ent ? pE[o] : 0.0f);
     }
   }
   sm[q][c] = m;
@@ -493,7 +496,8 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
     RBP_FUSED_MARK(RBP_PHASE_START);
     hipLaunchKernelGGL(target_ref_kernel, dim3(rbp::ceil_div(T256, 4)), dim3(256), 0, s, Hc, W,
                        tokens + t0, sq, old_logp + t0, Tn, T256, d, V, w.zy, w.R, w.n_listed);
-    hipLaunchKernelGGL(logits_store_kernel, dim3(rbp::gemm::stream_grid(tiles_v * tiles_t, n_cu)),
+    hipLaunchKernelGGL(entropy ? logits_store_kernel<true> : logits_store_kernel<false>,
+                       dim3(rbp::gemm::stream_grid(tiles_v * tiles_t, n_cu)),
                        dim3(GL::kThreads), 0, s, W, Hc, Tn, d, V, w.R, w.pM, w.pS, w.pE, Tc,
                        w.Qt, Tc, tiles_v, tiles_t);
     RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
@@ -517,7 +521,9 @@ extern "C" int policy_fused_fwd_bwd(const uint16_t* hidden, const uint16_t* W,
     RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
     RBP_FUSED_MARK(RBP_PHASE_SCALE);
     const int acc = (accumulate_dW || t0 > 0) ? 1 : 0;
-    rbp::launch_dweight(w.Hp, w.Qt, Tc, Tn, d, V, dW, acc, 0, tiles_v, s);
+    // the dhidden K half is free until dhidden runs
+    rbp::launch_dweight(w.Hp, w.Qt, Tc, Tn, d, V, dW, acc, 0, tiles_v, s, w.dh_half,
+                        Tc * (int64_t)d);
     RBP_CHECK_LAUNCH("policy_fused_fwd_bwd");
     RBP_FUSED_MARK(RBP_PHASE_DW);
     rbp::launch_dhidden(W, w.Qt, Tc, Tn, d, V, dhidden + t0 * d, w.dh_half, s, w.cs);

@@ -172,7 +172,10 @@ struct QuadSel {
 // Cache policy of the dz^T stores: non-temporal.  32 tiles per XCD write 4 MB
 // per round -- the whole L2 -- and, cached normally, would evict the operand
 // rows the next tiles share (measured: 1.1 ms of 15.5 at T=16384, V=152064).
-constexpr int kStreamStore = 2;
+#ifndef RBP_QSTORE_CPOL
+#define RBP_QSTORE_CPOL 2
+#endif
+constexpr int kStreamStore = RBP_QSTORE_CPOL;
 
 // -dl p -> bf16 for four consecutive rows of one token, packed in pairs.
 template <bool kFull>

@@ -111,33 +111,38 @@ __global__ void __launch_bounds__(256) target_dz_kernel(
   }
 }
 
-// Backward step 2: one K half of dH[t][m] = sum_v W[v][m] dz[t][v], with
-// A = W and B = dz^T both read MN-major (m / t contiguous, k = vocabulary).
-// Virtual blocks of split s write out0 (s = 0) or out1 (s = 1); the halves
-// are added afterwards.
+// Backward step 2: dH[t][m] = c_t sum_v W[v][m] dz[t][v], with A = W and
+// B = dz^T both read MN-major (m / t contiguous, k = vocabulary); c_t = 1,
+// or cs[t] for the single pass.  The launch covers n_vid tiles from virtual
+// tile vid_base on, over the whole vocabulary, or (split_steps > 0) each in
+// two K halves of split_steps steps: virtual block 2 i + h is half h of tile
+// vid_base + i; half 0 writes dH, half 1 its part[i] block ([t][m], 256 x
+// 256 fp32), added by part_add_dh_kernel -- or, with part_full, its rows of
+// part laid out like dH ([Tn][d]), added by add_f32_kernel.
 RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
                                       const uint16_t* __restrict__ Gt, int64_t ldGt, int64_t Tn,
-                                      int32_t d, int32_t V, int64_t k_split, int splits,
-                                      const float* __restrict__ cs, float* __restrict__ out0,
-                                      float* __restrict__ out1, int64_t tiles_m,
-                                      int64_t tiles_n) {
+                                      int32_t d, int32_t V, const float* __restrict__ cs,
+                                      float* __restrict__ dH, int64_t tiles_m, int64_t tiles_n,
+                                      int32_t vid_base, int32_t n_vid, int32_t split_steps,
+                                      float* __restrict__ part, int part_full) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const int64_t T256 = (Tn + 255) / 256 * 256;
   const Operand A{W, d, d, V};          // (m = hidden unit, k = vocab): W[v][m]
   const Operand B{Gt, ldGt, T256, V};   // (n = token, k = vocab): Gt[v][t]
-  const int32_t per_split = (int32_t)(tiles_m * tiles_n);
   auto tile_of = [&](int32_t vid) {
-    const int32_t split = vid >= per_split ? 1 : 0;  // at most two K splits
     int32_t tm, tn;
-    map_tile(vid - split * per_split, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
-    // both splits span k_split columns (uniform step count); columns past V
-    // read as zero
-    const int32_t kb = split * (int32_t)k_split;
-    return Tile{tm * 256, tn * 256, kb, kb + (int32_t)k_split};
+    const int32_t half = split_steps > 0 ? (vid & 1) : 0;
+    const int32_t tv = vid_base + (split_steps > 0 ? vid >> 1 : vid);
+    map_tile(tv, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+    // both halves span split_steps steps (uniform step count); columns past
+    // V read as zero
+    const int32_t kb = half * split_steps * 64;
+    return Tile{tm * 256, tn * 256, kb, split_steps > 0 ? kb + split_steps * 64 : V};
   };
   auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
     const Tile tile = tile_of(vid);
-    float* __restrict__ dH = tile.k_begin == 0 ? out0 : out1;
+    const bool to_part = split_steps > 0 && (vid & 1);
+    float* blk = part + (int64_t)(vid >> 1) * 65536;
 #pragma unroll
     for (int ni = 0; ni < GL::NI; ++ni) {
       const int64_t t = tile.n0 + GL::col(ni);
@@ -148,51 +153,109 @@ RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
           const int64_t m = tile.m0 + GL::row(mi, rg * 4);
-          if (m < d)
-            *reinterpret_cast<float4*>(dH + t * d + m) =
-                make_float4(c * acc[mi][ni][rg * 4 + 0], c * acc[mi][ni][rg * 4 + 1],
-                            c * acc[mi][ni][rg * 4 + 2], c * acc[mi][ni][rg * 4 + 3]);
+          const float4 val = make_float4(c * acc[mi][ni][rg * 4 + 0], c * acc[mi][ni][rg * 4 + 1],
+                                         c * acc[mi][ni][rg * 4 + 2], c * acc[mi][ni][rg * 4 + 3]);
+          if (to_part && !part_full)
+            *reinterpret_cast<float4*>(blk + GL::col(ni) * 256 + GL::row(mi, rg * 4)) = val;
+          else if (m < d)
+            *reinterpret_cast<float4*>((to_part ? part : dH) + t * d + m) = val;
         }
     }
   };
-  tile_stream<GL, true, true>(A, B, per_split * splits, smem, tile_of, epi);
+  tile_stream<GL, true, true>(A, B, n_vid, smem, tile_of, epi);
+}
+
+// dH += part[i] over the tiles vid_base + i of a split dhidden launch; one
+// block per (tile, 16 tokens).
+__global__ void __launch_bounds__(256) part_add_dh_kernel(float* __restrict__ dH,
+                                                          const float* __restrict__ part,
+                                                          int32_t vid_base, int64_t tiles_m,
+                                                          int64_t tiles_n, int32_t d,
+                                                          int64_t Tn) {
+  const int32_t i = (int32_t)blockIdx.x;
+  int32_t tm, tn;
+  map_tile(vid_base + i, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+  const int32_t tl = (int32_t)blockIdx.y * 16 + (threadIdx.x >> 4);
+  const int64_t t = (int64_t)tn * 256 + tl;
+  if (t >= Tn) return;
+  const float* src = part + (int64_t)i * 65536 + (int64_t)tl * 256;
+  for (int32_t ml = (threadIdx.x & 15) * 4; ml < 256; ml += 64) {
+    const int32_t m = tm * 256 + ml;
+    if (m >= d) break;  // d % 8 == 0: a float4 never straddles the edge
+    float4* dst = reinterpret_cast<float4*>(dH + t * d + m);
+    const float4 p = *reinterpret_cast<const float4*>(src + ml);
+    float4 o = *dst;
+    o.x += p.x;
+    o.y += p.y;
+    o.z += p.z;
+    o.w += p.w;
+    *dst = o;
+  }
 }
 
 // Backward step 3: dW[v][m] (+)= sum_t H[t][m] dz[t][v], with A = H read
 // MN-major (m contiguous, k = token) and B = dz^T K-major (rows v, k = token).
-// The launch covers the vocabulary tiles [tn_off, tn_off + tiles_n).
+// The launch covers n_vid of the tiles of the vocabulary range [tn_off,
+// tn_off + tiles_n), from virtual tile vid_base on.  With split_steps > 0
+// each of them is done in two K halves of split_steps steps (virtual block
+// 2 i + h = half h of tile vid_base + i): half 0 updates dW, half 1 writes
+// its raw sums to part[i] (a 256 x 256 fp32 block, [v][m]), which
+// part_add_kernel adds afterwards -- the last, partly filled round of a
+// persistent launch done as one round of half-length tiles.  Columns of dz^T
+// past Tn are finite (the single pass) or zero, and meet zero rows of H.
 RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
                                       const uint16_t* __restrict__ Gt, int64_t ldGt, int64_t Tn,
                                       int32_t d, int32_t V, float* __restrict__ dW, int accumulate,
-                                      int64_t tiles_m, int64_t tiles_n, int64_t tn_off) {
+                                      int64_t tiles_m, int64_t tiles_n, int64_t tn_off,
+                                      int32_t vid_base, int32_t n_vid, int32_t split_steps,
+                                      float* __restrict__ part) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
-  const int64_t T8 = (Tn + 7) / 8 * 8;  // dz^T columns Tn..T8 hold zeros
+  const int64_t T8 = (Tn + 7) / 8 * 8;
   const Operand A{Hc, d, d, Tn};        // (m = hidden unit, k = token): H[t][m]
   const Operand B{Gt, ldGt, V, T8};     // (n = vocab, k = token): Gt[v][t]
   auto tile_of = [&](int32_t vid) {
     int32_t tm, tn;
-    map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
-    return Tile{tm * 256, (tn + (int32_t)tn_off) * 256, 0, (int32_t)Tn};
+    const int32_t half = split_steps > 0 ? (vid & 1) : 0;
+    const int32_t tv = vid_base + (split_steps > 0 ? vid >> 1 : vid);
+    map_tile(tv, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+    const int32_t kb = half * split_steps * 64;
+    return Tile{tm * 256, (tn + (int32_t)tn_off) * 256, kb,
+                split_steps > 0 ? kb + split_steps * 64 : (int32_t)Tn};
   };
   auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) {
     const Tile tile = tile_of(vid);
+    if (split_steps > 0 && (vid & 1)) {
+      float* blk = part + (int64_t)(vid >> 1) * 65536;
+#pragma unroll
+      for (int ni = 0; ni < GL::NI; ++ni)
+#pragma unroll
+        for (int mi = 0; mi < GL::MI; ++mi)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg)
+            *reinterpret_cast<float4*>(blk + GL::col(ni) * 256 + GL::row(mi, rg * 4)) =
+                make_float4(acc[mi][ni][rg * 4 + 0], acc[mi][ni][rg * 4 + 1],
+                            acc[mi][ni][rg * 4 + 2], acc[mi][ni][rg * 4 + 3]);
+      return;
+    }
     if (accumulate && tile.n0 + 256 <= V && tile.m0 + 256 <= d) {
-      // interior tile: the previous values are loaded eight float4 at a time
-      // before any of them is stored back, so the tile waits for memory four
-      // times rather than once per float4.  Eight, not sixteen: the kernel
-      // must stay within 232 VGPRs, so that a 40-VGPR wave of the rescale
-      // that the single pass runs beside it still fits on each SIMD.
+      // interior tile: the previous values are loaded kDwBatch float4 at a
+      // time before any of them is stored back, so the tile waits for memory
+      // a few times rather than once per float4
+#ifndef RBP_DW_BATCH
+#define RBP_DW_BATCH 8
+#endif
+      constexpr int kDwBatch = RBP_DW_BATCH;  // 4, 8 or 16 (float4 per batch)
 #pragma unroll
       for (int ni = 0; ni < GL::NI; ++ni) {
         float* row = dW + (int64_t)(tile.n0 + GL::col(ni)) * d + tile.m0;
 #pragma unroll
-        for (int mh = 0; mh < GL::MI; mh += 2) {
-          float4 o[8];
+        for (int mh = 0; mh < GL::MI; mh += kDwBatch / 4) {
+          float4 o[kDwBatch];
 #pragma unroll
-          for (int k = 0; k < 8; ++k)
+          for (int k = 0; k < kDwBatch; ++k)
             o[k] = *reinterpret_cast<const float4*>(row + GL::row(mh + k / 4, (k % 4) * 4));
 #pragma unroll
-          for (int k = 0; k < 8; ++k) {
+          for (int k = 0; k < kDwBatch; ++k) {
             const int mi = mh + k / 4, rg = k % 4;
             *reinterpret_cast<float4*>(row + GL::row(mi, rg * 4)) =
                 make_float4(acc[mi][ni][rg * 4 + 0] + o[k].x, acc[mi][ni][rg * 4 + 1] + o[k].y,
@@ -230,7 +293,36 @@ RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
         }
     }
   };
-  tile_stream<GL, true, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
+  tile_stream<GL, true, false>(A, B, n_vid, smem, tile_of, epi);
+}
+
+// dW += part[i] over the tiles vid_base + i (i < n_tiles) of a split
+// dweight launch; one block per (tile, 16 vocabulary rows).
+__global__ void __launch_bounds__(256) part_add_kernel(float* __restrict__ dW,
+                                                       const float* __restrict__ part,
+                                                       int32_t vid_base, int64_t tiles_m,
+                                                       int64_t tiles_n, int64_t tn_off,
+                                                       int32_t d, int32_t V) {
+  const int32_t i = (int32_t)blockIdx.x;
+  int32_t tm, tn;
+  map_tile(vid_base + i, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+  const int32_t m0 = tm * 256, v0 = (tn + (int32_t)tn_off) * 256;
+  const int32_t vl = (int32_t)blockIdx.y * 16 + (threadIdx.x >> 4);
+  const int32_t v = v0 + vl;
+  if (v >= V) return;
+  const float* src = part + (int64_t)i * 65536 + (int64_t)vl * 256;
+  for (int32_t ml = (threadIdx.x & 15) * 4; ml < 256; ml += 64) {
+    const int32_t m = m0 + ml;
+    if (m >= d) break;  // d % 8 == 0: a float4 never straddles the edge
+    float4* dst = reinterpret_cast<float4*>(dW + (int64_t)v * d + m);
+    const float4 p = *reinterpret_cast<const float4*>(src + ml);
+    float4 o = *dst;
+    o.x += p.x;
+    o.y += p.y;
+    o.z += p.z;
+    o.w += p.w;
+    *dst = o;
+  }
 }
 
 // a[i] += b[i] (n % 4 == 0), fixed order per element.
@@ -279,13 +371,28 @@ size_t rbp::logprob_bwd_ws(int64_t Tc, int32_t d, int32_t V) {
 
 void rbp::launch_dweight(const uint16_t* Hc, const uint16_t* Gt, int64_t ldGt, int64_t Tn,
                          int32_t d, int32_t V, float* dW, int accumulate, int64_t tn_begin,
-                         int64_t tn_end, hipStream_t s) {
-  const int64_t tiles_d = rbp::ceil_div(d, 256);
-  if (tn_end <= tn_begin) return;
-  hipLaunchKernelGGL(dweight_kernel,
-                     dim3(rbp::gemm::stream_grid(tiles_d * (tn_end - tn_begin), device_cus())),
+                         int64_t tn_end, hipStream_t s, float* scratch, int64_t scratch_floats) {
+  const int64_t tiles_d = rbp::ceil_div(d, 256), tiles_n = tn_end - tn_begin;
+  if (tiles_n <= 0) return;
+  const int64_t tiles = tiles_d * tiles_n;
+  const int64_t grid = rbp::gemm::stream_grid(tiles, device_cus());
+  // A last round filled to at most half: its tiles go to a second launch as
+  // two K halves each (one round of half the length), when the K range has
+  // at least 8 steps and the scratch holds one 256 x 256 block per tile.
+  const int64_t rem = tiles % grid, nk = rbp::ceil_div(Tn, 64);
+  const bool split = tiles > grid && rem > 0 && 2 * rem <= grid && nk >= 8 &&
+                     scratch != nullptr && rem * 65536 <= scratch_floats;
+  const int64_t n_main = split ? tiles - rem : tiles;
+  hipLaunchKernelGGL(dweight_kernel, dim3(grid), dim3(GL::kThreads), 0, s, Hc, Gt, ldGt, Tn, d,
+                     V, dW, accumulate, tiles_d, tiles_n, tn_begin, 0, (int32_t)n_main, 0,
+                     (float*)nullptr);
+  if (!split) return;
+  const int32_t half_steps = (int32_t)((nk + 1) / 2);
+  hipLaunchKernelGGL(dweight_kernel, dim3(rbp::gemm::stream_grid(2 * rem, device_cus())),
                      dim3(GL::kThreads), 0, s, Hc, Gt, ldGt, Tn, d, V, dW, accumulate, tiles_d,
-                     tn_end - tn_begin, tn_begin);
+                     tiles_n, tn_begin, (int32_t)n_main, (int32_t)(2 * rem), half_steps, scratch);
+  hipLaunchKernelGGL(part_add_kernel, dim3((unsigned)rem, 16), dim3(256), 0, s, dW, scratch,
+                     (int32_t)n_main, tiles_d, tiles_n, tn_begin, d, V);
 }
 
 void rbp::launch_dhidden(const uint16_t* W, const uint16_t* Gt, int64_t ldGt, int64_t Tn,
@@ -293,20 +400,38 @@ void rbp::launch_dhidden(const uint16_t* W, const uint16_t* Gt, int64_t ldGt, in
                          const float* cs) {
   const int n_cu = device_cus();
   const int64_t tiles_d = rbp::ceil_div(d, 256), tiles_t = rbp::ceil_div(Tn, 256);
-  // dhidden in two K halves when one pass would give each CU only a few
-  // tiles (the last, partly empty round would then cost a large share)
-  const int64_t tiles_dh = tiles_d * tiles_t;
-  const int splits = tiles_dh < 4 * (int64_t)n_cu && V >= 512 ? 2 : 1;
-  const int64_t k_split = splits == 2 ? (rbp::ceil_div(V, 2) + 63) / 64 * 64 : V;
-  hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(tiles_dh * splits, n_cu)),
-                     dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, k_split, splits, cs,
-                     dhidden_c, dh_half, tiles_d, tiles_t);
-  if (splits == 2) {
+  const int64_t tiles = tiles_d * tiles_t;
+  const int64_t G = rbp::gemm::stream_grid(int64_t(1) << 30, n_cu);  // one round
+  const int64_t nk = rbp::ceil_div(V, 64);
+  const int32_t half_steps = (int32_t)((nk + 1) / 2);
+  // The whole vocabulary per tile; when the tiles fill at most half a round,
+  // all of them in two K halves (the second halves into dh_half, laid out
+  // like dhidden, then summed); otherwise a last round filled to at most
+  // half goes to a second launch as two K halves per tile (dh_half holds one
+  // 256 x 256 block per tile).
+  if (nk >= 8 && 2 * tiles <= G) {
+    hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(2 * tiles, n_cu)),
+                       dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, cs, dhidden_c, tiles_d,
+                       tiles_t, 0, (int32_t)(2 * tiles), half_steps, dh_half, 1);
     const int64_t n4 = Tn * d / 4;
     int64_t blocks = rbp::ceil_div(n4, 256);
     if (blocks > 8192) blocks = 8192;
     hipLaunchKernelGGL(add_f32_kernel, dim3(blocks), dim3(256), 0, s, dhidden_c, dh_half, n4);
+    return;
   }
+  const int64_t r = tiles % G;
+  const int64_t rem = (nk >= 8 && tiles > G && r > 0 && 2 * r <= G &&
+                       r * 65536 <= ldGt * (int64_t)d) ? r : 0;
+  const int64_t n_main = tiles - rem;
+  hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(n_main, n_cu)),
+                     dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, cs, dhidden_c, tiles_d,
+                     tiles_t, 0, (int32_t)n_main, 0, (float*)nullptr, 0);
+  if (rem == 0) return;
+  hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(2 * rem, n_cu)),
+                     dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, cs, dhidden_c, tiles_d,
+                     tiles_t, (int32_t)n_main, (int32_t)(2 * rem), half_steps, dh_half, 0);
+  hipLaunchKernelGGL(part_add_dh_kernel, dim3((unsigned)rem, 16), dim3(256), 0, s, dhidden_c,
+                     dh_half, (int32_t)n_main, tiles_d, tiles_t, d, Tn);
 }
 
 void rbp::launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint16_t* Gt,
@@ -322,7 +447,9 @@ void rbp::launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint
     return;
   }
   launch_dhidden(W, Gt, ldGt, Tn, d, V, dhidden_c, dh_half, s);
-  launch_dweight(Hc, Gt, ldGt, Tn, d, V, dW, accumulate, 0, round256(V) / 256, s);
+  // dh_half is free again once dhidden's sum has read it
+  launch_dweight(Hc, Gt, ldGt, Tn, d, V, dW, accumulate, 0, round256(V) / 256, s, dh_half,
+                 ldGt * (int64_t)d);
 }
 
 extern "C" int policy_logprob_bwd(const uint16_t* hidden, const uint16_t* W,

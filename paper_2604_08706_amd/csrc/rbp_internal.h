@@ -52,9 +52,10 @@ void launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint16_t*
 // Its two parts: dW rows of the vocabulary tiles [tn_begin, tn_end) (256 rows
 // each), and dhidden (with its split-K sum; row t scaled by cs[t] when cs is
 // given).
+// scratch (fp32, scratch_floats) may hold partial sums of dW's last round.
 void launch_dweight(const uint16_t* Hc, const uint16_t* Gt, int64_t ldGt, int64_t Tn, int32_t d,
                     int32_t V, float* dW, int accumulate, int64_t tn_begin, int64_t tn_end,
-                    hipStream_t s);
+                    hipStream_t s, float* scratch = nullptr, int64_t scratch_floats = 0);
 void launch_dhidden(const uint16_t* W, const uint16_t* Gt, int64_t ldGt, int64_t Tn, int32_t d,
                     int32_t V, float* dhidden_c, float* dh_half, hipStream_t s,
                     const float* cs = nullptr);

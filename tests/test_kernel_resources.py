@@ -48,10 +48,11 @@ def _resources(src):
     return out
 
 
-def _kernel(src, fragment):
+def _kernels(src, fragment):
+    """Every instance (template instantiations included) of a kernel."""
     hits = [v for k, v in _resources(src).items() if fragment in k]
-    assert len(hits) == 1, (src, fragment, list(_resources(src)))
-    return hits[0]
+    assert hits, (src, fragment, list(_resources(src)))
+    return hits
 
 
 @pytest.mark.parametrize("src,kernel", [
@@ -67,6 +68,6 @@ def _kernel(src, fragment):
     ("sample_gather.hip", "draw_kernel"),
 ])
 def test_hot_kernels_do_not_spill(src, kernel):
-    vgprs, scratch = _kernel(src, kernel)
-    assert scratch == 0, f"{kernel} spills {scratch} bytes per lane"
-    assert vgprs <= 256
+    for vgprs, scratch in _kernels(src, kernel):
+        assert scratch == 0, f"{kernel} spills {scratch} bytes per lane"
+        assert vgprs <= 256
