@@ -44,7 +44,15 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 # were read on (None until they are).
 TRAFFIC_SOURCES = ("fused.hip", "logprob_bwd.hip", "logits_epilogue.h", "gemm_core.h",
                    "gemm_dma.h", "advantage_loss.hip")
-TRAFFIC = None
+# FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0 (a 1 GiB copy reads 524300 KiB of
+# FETCH_SIZE and 1048576 KiB of WRITE_SIZE), per step:
+#   logits  = target_ref_kernel + logits_store_kernel
+#   dW      = dweight_kernel (main launch + last-round launch) + part_add_kernel
+#   dhidden = dhidden_kernel (main launch + last-round launch) + part_add_dh_kernel
+TRAFFIC = {
+    "sources_sha256": "ade79da6e378bc995fbc76ea762f88c134fc28f6edc5677ae1f0c2ebab7f2ad9",
+    "bytes": {"logits": 36011144192, "dW": 34090914816, "dhidden": 39245122560},
+}
 
 # the three products of the single pass, by the phase that times them
 PRODUCTS = {
