@@ -537,7 +537,7 @@ def cpu_sampler_stress(seed=3):
             "sample": f"{wl.n_draw} draws from {n} records, padded [{wl.n_draw}, {wl.l_max}]"}
 
 
-def run_step_fused(rbp, wl, S, step, out, ex, ev0=None):
+def run_step_fused(rbp, wl, S, step, out, ex, ev0=None, accumulate=True):
     """The same step through policy_fused_fwd_bwd (forward, loss, backward and
     entropy in one call).  ev0: an event recorded at the step start; the
     phase events of the call, if any, are in ex."""
@@ -548,7 +548,7 @@ def run_step_fused(rbp, wl, S, step, out, ex, ev0=None):
     rbp.policy_fused_fwd_bwd(S["hidden"], S["W"], out["tokens"], out["seq_of_token"],
                              out["old_logp"], out["adv"], out["len"], wl.n_draw, S["logp"],
                              S["lse"], S["entropy"], S["loss"], S["dlogp"], S["stats"], S["dh"],
-                             S["dW"], S["ws_fused"], accumulate_dW=True, exec=ex)
+                             S["dW"], S["ws_fused"], accumulate_dW=accumulate, exec=ex)
 
 
 def tokens_of_steps(rbp, wl, S, out, steps):

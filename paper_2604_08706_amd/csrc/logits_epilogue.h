@@ -17,7 +17,10 @@ using rbp::gemm::f32x16;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kGroupLogits = 4;
-constexpr int kGroupGrad = 8;
+constexpr int kGroupGrad = 8;   // dhidden: groups of 8 hidden-unit tiles
+// dW: groups of 14 hidden-unit tiles, all of them at d = 3584, so that an
+// XCD's concurrent tiles read each vocabulary panel of dz^T together
+constexpr int kGroupDw = 14;
 
 // Every product runs on the 8-wave grid (two waves per SIMD).
 using GL = rbp::gemm::Grid8;

@@ -217,7 +217,7 @@ RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
     int32_t tm, tn;
     const int32_t half = split_steps > 0 ? (vid & 1) : 0;
     const int32_t tv = vid_base + (split_steps > 0 ? vid >> 1 : vid);
-    map_tile(tv, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+    map_tile(tv, (int32_t)tiles_m, (int32_t)tiles_n, kGroupDw, tm, tn);
     const int32_t kb = half * split_steps * 64;
     return Tile{tm * 256, (tn + (int32_t)tn_off) * 256, kb,
                 split_steps > 0 ? kb + split_steps * 64 : (int32_t)Tn};
@@ -305,7 +305,7 @@ __global__ void __launch_bounds__(256) part_add_kernel(float* __restrict__ dW,
                                                        int32_t d, int32_t V) {
   const int32_t i = (int32_t)blockIdx.x;
   int32_t tm, tn;
-  map_tile(vid_base + i, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+  map_tile(vid_base + i, (int32_t)tiles_m, (int32_t)tiles_n, kGroupDw, tm, tn);
   const int32_t m0 = tm * 256, v0 = (tn + (int32_t)tn_off) * 256;
   const int32_t vl = (int32_t)blockIdx.y * 16 + (threadIdx.x >> 4);
   const int32_t v = v0 + vl;

@@ -17,8 +17,9 @@ weights and hidden states Gaussian):
                4096; 512 draws, positive mixture p_pos = 0.7; policy age U{0..4} with
                noise sd 0.05 * age; Bern(0.3).
 * ``head7b``   d=3584, V=152064; 1024 records (128 x G=8), LogN(ln 1200, 0.5) cap
-               4096; uniform draws packed into one 16384-token micro-batch; noise
-               N(0, 0.1^2); Bern(0.4).
+               4096; 24 uniform draws, whose stream's first 16384 tokens form the
+               micro-batch (enough draws that it is always full); noise N(0, 0.1^2);
+               Bern(0.4).
 * ``stress``   d=3584, V=152064; 10^6 records, LogN(ln 1200, 1.0) cap 8192; 256 draws,
                positive mixture p_pos = 0.5, padded; age U{0..4}; Bern(0.4).
 
@@ -61,7 +62,7 @@ WORKLOADS = {
                         0.3, 0.1, False, "uniform", 0.0, "packed", 16384, 0),
     "head15b": Workload("head15b", 1536, 151936, 32768, 8, 512, "lognormal", 800, 0.5, 4096,
                         0.3, 0.05, True, "pos_mix", 0.7, "packed", 16384, 0),
-    "head7b": Workload("head7b", 3584, 152064, 1024, 8, 16, "lognormal", 1200, 0.5, 4096,
+    "head7b": Workload("head7b", 3584, 152064, 1024, 8, 24, "lognormal", 1200, 0.5, 4096,
                        0.4, 0.1, False, "uniform", 0.0, "packed", 16384, 0),
     "stress": Workload("stress", 3584, 152064, 1_000_000, 8, 256, "lognormal", 1200, 1.0, 8192,
                        0.4, 0.05, True, "pos_mix", 0.5, "padded", 0, 8192),
