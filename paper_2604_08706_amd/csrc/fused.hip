@@ -51,6 +51,8 @@ using rbp::gemm::map_tile;
 using rbp::gemm::Operand;
 using rbp::gemm::Tile;
 using rbp::gemm::tile_stream;
+using rbp::gemm::kKMajor;
+using rbp::gemm::kKPaired;
 
 // Per token column of this wave's 128 x 64 block: the max over the lane
 // pair's rows (lanes l and l + 32 hold the same column).
@@ -69,49 +71,34 @@ __device__ __forceinline__ void column_max(const f32x16 (&acc)[GL::MI][GL::NI], 
   }
 }
 
-// e = exp(z - M) for four consecutive rows of one token: the fp32 e and e z
-// are added to the column's sums, e f (f = exp(M - ref)) is packed to bf16
-// pairs (rows past the vocabulary hold 0).
-template <bool kFull, bool kEnt>
-__device__ __forceinline__ void q_pack(const f32x16& acc, float ls, float f, int mi, int rg,
-                                       int32_t lim, uint32_t& P0, uint32_t& P1, float& S,
-                                       float& E) {
-  float q[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float z = acc[rg * 4 + i];
-    q[i] = exp2_hw(fmaf(z, kLog2e, -ls));
-    if constexpr (!kFull)
-      q[i] = __uint_as_float(select_below(GL::row_off(mi, rg * 4 + i), lim,
-                                          __float_as_uint(q[i]), 0u));
-    S += q[i];
-    if constexpr (kEnt) E = fmaf(q[i], z, E);
-  }
-  P0 = pack_bf16x2(q[0] * f, q[1] * f);
-  P1 = pack_bf16x2(q[2] * f, q[3] * f);
-}
-
-// dz_rows of the backward with q in place of dz, plus the sums.
+// One 32-row block (mi) of the wave's q tile.  B is loaded with paired rows,
+// so lane l holds tokens 2 (l % 32) and 2 (l % 32) + 1 (tiles ni = 0, 1) of the
+// same 16 vocabulary rows: per row, e = exp(z - M) of both tokens go into
+// their columns' sums (S, and E += e z when kEnt), and e f (f = exp(M - ref))
+// is packed into one bf16 pair and stored as 4 bytes.  Lanes 0..31 then write
+// 128 contiguous bytes of one row of Q^T and lanes 32..63 those of the row 4
+// below: whole cache lines, with no exchange between lanes.  Rows past the
+// vocabulary hold 0.
 template <bool kFull, bool kEnt>
 __device__ __forceinline__ void q_rows(const f32x16 (&acc)[GL::MI][GL::NI], const float (&ls)[2],
                                        const float (&f)[2], int mi, int32_t lim,
-                                       const QuadSel& qs, __amdgpu_buffer_rsrc_t rQ, uint32_t off,
-                                       int64_t ldQ, float (&S)[2], float (&E)[2]) {
-  static_assert(GL::NI == 2, "two column blocks per wave");
+                                       __amdgpu_buffer_rsrc_t rQ, uint32_t off, int64_t ldQ,
+                                       float (&S)[2], float (&E)[2]) {
+  static_assert(GL::NI == 2, "two column tiles per wave");
 #pragma unroll
-  for (int rg = 0; rg < 4; ++rg) {
-    uint32_t X0, X1, Y0, Y1;
-    q_pack<kFull, kEnt>(acc[mi][0], ls[0], f[0], mi, rg, lim, X0, X1, S[0], E[0]);
-    q_pack<kFull, kEnt>(acc[mi][1], ls[1], f[1], mi, rg, lim, Y0, Y1, S[1], E[1]);
-    const auto s0 = __builtin_amdgcn_permlane32_swap(X0, Y0, false, false);
-    const auto s1 = __builtin_amdgcn_permlane32_swap(X1, Y1, false, false);
-    uint32_t w0, w1;
-    const int ro = mi * 32 + rg * 8;
-    quad_transpose(s0[0], s1[0], qs, w0, w1);
-    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rQ, off, (int)(ro * ldQ * 2), kStreamStore);
-    quad_transpose(s0[1], s1[1], qs, w0, w1);
-    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rQ, off, (int)((ro + 4) * ldQ * 2),
-                                          kStreamStore);
+  for (int r = 0; r < 16; ++r) {
+    float q[2];
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      const float z = acc[mi][ni][r];
+      q[ni] = exp2_hw(fmaf(z, kLog2e, -ls[ni]));
+      if constexpr (!kFull)
+        q[ni] = __uint_as_float(select_below(GL::row_off(mi, r), lim, __float_as_uint(q[ni]), 0u));
+      S[ni] += q[ni];
+      if constexpr (kEnt) E[ni] = fmaf(q[ni], z, E[ni]);
+    }
+    __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(q[0] * f[0], q[1] * f[1]), rQ, off,
+                                          (int)(GL::row_off(mi, r) * ldQ * 2), kStreamStore);
   }
 }
 
@@ -170,9 +157,7 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const Operand A{W, d, V, d};
   const Operand B{Hc, d, Tn, d};
-  const QuadSel qs;
   const int lane = threadIdx.x & 63;
-  const int j = threadIdx.x & 3;
   auto tile_of = [&](int32_t vid) {
     int32_t tm, tn;
     map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupLogits, tm, tn);
@@ -184,7 +169,7 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
   auto load_ref = [&](int32_t vid) {
     const Tile tile = tile_of(vid);
 #pragma unroll
-    for (int ni = 0; ni < GL::NI; ++ni) Rr[ni] = Rc[tile.n0 + GL::col(ni)];
+    for (int ni = 0; ni < GL::NI; ++ni) Rr[ni] = Rc[tile.n0 + GL::col_paired(ni)];
   };
   load_ref((int32_t)blockIdx.x);
   const int32_t n_vid = (int32_t)(tiles_m * tiles_n);
@@ -207,15 +192,14 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
     }
     const auto rQ = __builtin_amdgcn_make_buffer_rsrc(
         uniform_ptr(Qt + (int64_t)tile.m0 * ldQ + tile.n0), 0, (int)(256 * ldQ * 2), 0x00020000);
-    const uint32_t off =
-        (uint32_t)((GL::wm() * (256 / GL::WM) + j) * ldQ + GL::wn() * (256 / GL::WN) +
-                   32 * (lane >> 5) + ((lane & 31) - j)) * 2u;
+    // lane l: row GL::row(0, 0), tokens 2 (l % 32) and 2 (l % 32) + 1
+    const uint32_t off = (uint32_t)(GL::row(0, 0) * ldQ + GL::col_paired(0)) * 2u;
 #pragma unroll
     for (int mi = 0; mi < GL::MI; ++mi) {
       if (vlim >= 256)
-        q_rows<true, kEnt>(acc, ls, f, mi, lim, qs, rQ, off, ldQ, S, E);
+        q_rows<true, kEnt>(acc, ls, f, mi, lim, rQ, off, ldQ, S, E);
       else
-        q_rows<false, kEnt>(acc, ls, f, mi, lim, qs, rQ, off, ldQ, S, E);
+        q_rows<false, kEnt>(acc, ls, f, mi, lim, rQ, off, ldQ, S, E);
     }
     // both lane halves hold rows of the same columns; the lower half writes
     // the sums, 128 contiguous bytes per array and column block
@@ -225,7 +209,7 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
       const float s = S[ni] + __shfl_xor(S[ni], 32, 64);
       const float e = kEnt ? E[ni] + __shfl_xor(E[ni], 32, 64) : 0.0f;
       if (lane < 32) {
-        const int64_t o = half * ldp + tile.n0 + GL::col(ni);
+        const int64_t o = half * ldp + tile.n0 + GL::col_paired(ni);
         pM[o] = mx[ni];
         pS[o] = s;
         if (kEnt) pE[o] = e;
@@ -233,7 +217,7 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
     }
     if (vid + (int32_t)gridDim.x < n_vid) load_ref(vid + (int32_t)gridDim.x);
   };
-  tile_stream<GL, false, false>(A, B, n_vid, smem, tile_of, epi);
+  tile_stream<GL, kKMajor, kKPaired>(A, B, n_vid, smem, tile_of, epi);
 }
 
 // (m, s, e) <- merge with the partial (Mi, Si, Ei), rescaling to the larger max.

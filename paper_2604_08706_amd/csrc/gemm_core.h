@@ -4,15 +4,17 @@
 //   logits   A = W  (m = vocabulary), B = H  (n = token), k = hidden unit
 //   dhidden  A = W^T (m = hidden unit), B = dz (n = token), k = vocabulary
 //   dW       A = H^T (m = hidden unit), B = dz^T (n = vocabulary), k = token
-// Every operand is stored k-contiguous ("K-major"), so one mainloop
-// (gemm_dma.h) serves all of them.
+// Each operand is read where it lies, k-contiguous ("K-major") or
+// m/n-contiguous ("MN-major"); one mainloop (gemm_dma.h) serves all of them.
 //
 // Workgroup tile 256 x 256 over a grid of WM x WN waves; each wave owns
 // (256/WM) x (256/WN) outputs as MI x NI v_mfma_f32_32x32x16_bf16 tiles.
 // MFMA 32x32x16 lane layout: lane l supplies A[l % 32][8 (l / 32) .. + 8) and
 // B[l % 32][8 (l / 32) .. + 8); accumulator r of lane l holds
 // C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].  Each lane therefore owns runs of
-// four consecutive m for one n, which the epilogues store as 8/16-byte vectors.
+// four consecutive m for one n (the fp32 epilogues store them as 16-byte
+// vectors); with B loaded with paired rows it owns two adjacent n of the same
+// m, which the bf16 epilogues store as one 4-byte pair.
 //
 // An LDS operand tile is [256 rows][64 k] bf16: 128-byte rows of eight 16-byte
 // chunks, chunk index XOR-swizzled by (row ^ row >> 3) & 7 so that fragment
@@ -71,6 +73,13 @@ struct Grid {
   }
   static __device__ __forceinline__ int col(int ni) {
     return wn() * (256 / WN) + ni * 32 + (threadIdx.x & 31);
+  }
+  // column of tile ni when B is loaded with paired rows (gemm_dma.h,
+  // kKPaired): lane l of tiles 0 and 1 holds columns 2 (l % 32) and
+  // 2 (l % 32) + 1 of the wave's 64
+  static __device__ __forceinline__ int col_paired(int ni) {
+    static_assert(256 / WN == 64 && NI == 2, "paired columns need 64-column waves");
+    return wn() * 64 + 2 * (threadIdx.x & 31) + ni;
   }
 };
 // 8 waves, two per SIMD, 128 x 64 outputs each (128 accumulators per lane):

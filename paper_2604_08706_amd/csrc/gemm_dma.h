@@ -107,12 +107,24 @@ __device__ __forceinline__ void mfma_tiles_interleaved(const bf16x8 (&a)[G::MI],
   }
 }
 
+// Operand layouts (template arguments of tile_stream):
+//   kKMajor   element (mn, k) at ptr[mn * ld + k];
+//   kMNMajor  element (mn, k) at ptr[k * ld + mn];
+//   kKPaired  K-major, with the rows of every 64-row block reordered on their
+//             way into LDS: rows 2 i and 2 i + 1 land in LDS rows i and 32 + i,
+//             so the two 32-row MFMA tiles of a 64-row wave block hold the
+//             block's even and odd rows, and one lane holds the outputs of two
+//             adjacent rows (Grid::col_paired).
+constexpr int kKMajor = 0, kMNMajor = 1, kKPaired = 2;
+
 // ---- K-major operand: LDS tile = 256 rows x 128 bytes (K step 64) ----------
 //
 // Each lane's share of one operand tile's loads.  Load j of a wave moves a
 // 1 KiB block (8 rows x 128 bytes) into LDS; the offsets are relative to the
-// first row of the tile, so they serve every tile of a launch.
-template <class G>
+// first row of the tile, so they serve every tile of a launch.  With kPaired
+// LDS row r holds operand row (r & ~63) | 2 (r & 31) | ((r >> 5) & 1); the
+// swizzle follows the LDS row.
+template <class G, bool kPaired>
 struct KLanes {
   static constexpr int kLoads = 32 / G::kWaves;  // 1 KiB blocks per wave per step
   uint32_t voff[kLoads];
@@ -127,9 +139,10 @@ struct KLanes {
     for (int j = 0; j < kLoads; ++j) {
       const int b = j * G::kWaves + wave;
       const int row = b * 8 + (lane >> 3);
+      const int src = kPaired ? ((row & ~63) | ((row & 31) << 1) | ((row >> 5) & 1)) : row;
       const int c = (lane & 7) ^ (lane >> 3) ^ (b & 7);
       kc[j] = c * 8;
-      voff[j] = (uint32_t)((row * ld + c * 8) * 2);
+      voff[j] = (uint32_t)((src * ld + c * 8) * 2);
     }
   }
 };
@@ -229,8 +242,9 @@ struct MNFrags {
   }
 };
 
-template <bool kMN, int kCount>
-using Frags = typename std::conditional<kMN, MNFrags<kCount>, KFrags<kCount>>::type;
+template <int kLayout, int kCount>
+using Frags =
+    typename std::conditional<kLayout == kMNMajor, MNFrags<kCount>, KFrags<kCount>>::type;
 
 // One output tile: rows m0.. of A, rows n0.. of B, K range [k_begin, k_end)
 // (non-empty).  32-bit fields keep the loop's scalar state small.
@@ -244,12 +258,9 @@ __device__ __forceinline__ int32_t k_steps(const Tile& t) {
 
 // Load side of one operand: per-lane offsets, the per-tile view (`Res`) and
 // the issue of load j of K step `step` of a tile into an LDS tile.
-template <class G, bool kMN>
-struct SideLoad;
-
-template <class G>
-struct SideLoad<G, false> {  // K-major
-  KLanes<G> lanes;
+template <class G, int kLayout>
+struct SideLoad {  // K-major (kKMajor, kKPaired)
+  KLanes<G, kLayout == kKPaired> lanes;
   int32_t k_extent;
   struct Res {
     i32x4 rsrc;  // the tile's (at most 256) rows; range 0 past the end of the stream
@@ -276,7 +287,7 @@ struct SideLoad<G, false> {  // K-major
 };
 
 template <class G>
-struct SideLoad<G, true> {  // MN-major
+struct SideLoad<G, kMNMajor> {
   MNLanes<G> lanes;
   int32_t mn_extent;
   int64_t ld;
@@ -317,10 +328,9 @@ struct SideLoad<G, true> {  // MN-major
 // Persistent tile loop.  This workgroup takes the virtual blocks blockIdx.x,
 // blockIdx.x + gridDim.x, ... below n_vid; tile_of(vid) gives each one's Tile
 // (every tile of a launch has the same number of K steps, nk >= 1) and
-// epi(vid, acc) consumes its finished fp32 accumulators.  kMNA / kMNB select
-// the layout of A / B: K-major (element (mn, k) at ptr[mn * ld + k]) or
-// MN-major (at ptr[k * ld + mn]); K-major needs k_extent % 8 == 0, MN-major
-// mn_extent % 8 == 0.
+// epi(vid, acc) consumes its finished fp32 accumulators.  kLA / kLB select
+// the layouts of A / B (kKMajor, kMNMajor, kKPaired); K-major needs
+// k_extent % 8 == 0, MN-major mn_extent % 8 == 0.
 //
 // The K steps of consecutive tiles form one stream through two 64-KiB LDS
 // stages (stream step g in stage g % 2), so the first steps of the next tile
@@ -337,27 +347,27 @@ struct SideLoad<G, true> {  // MN-major
 //   offsets >= kLdsBytes (the stages are in use) and may contain barriers.
 // The load cursor runs two steps ahead of the MFMAs; it holds its tile's
 // load views (cur) and the following tile's (nxt), refreshed once per tile.
-template <class G, bool kMNA, bool kMNB, class TileFn, class EpiFn>
+template <class G, int kLA, int kLB, class TileFn, class EpiFn>
 __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, int32_t n_vid,
                                             uint8_t* smem, TileFn&& tile_of, EpiFn&& epi) {
   const int32_t stride = (int32_t)gridDim.x;
   const int32_t vid0 = (int32_t)blockIdx.x;
   if (vid0 >= n_vid) return;
   constexpr int L = 32 / G::kWaves;
-  SideLoad<G, kMNA> la;
-  SideLoad<G, kMNB> lb;
+  SideLoad<G, kLA> la;
+  SideLoad<G, kLB> lb;
   la.init(A);
   lb.init(B);
-  Frags<kMNA, G::MI> fa;
-  Frags<kMNB, G::NI> fb;
+  Frags<kLA, G::MI> fa;
+  Frags<kLB, G::NI> fb;
   fa.init(0u, G::wm() * (256 / G::WM));
   fb.init((uint32_t)kTileBytes, G::wn() * (256 / G::WN));
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
   const int32_t nk = k_steps(tile_of(vid0));
 
   struct TileRes {
-    typename SideLoad<G, kMNA>::Res a;
-    typename SideLoad<G, kMNB>::Res b;
+    typename SideLoad<G, kLA>::Res a;
+    typename SideLoad<G, kLB>::Res b;
   };
   auto res_of = [&](int32_t vid) {
     const bool valid = vid < n_vid;

@@ -2,7 +2,7 @@
 // logprob_bwd.hip, fused.hip):
 // the 8-wave tile grid, exponentials, per-column (max, sum exp) reductions of
 // a 256 x 256 logit tile, wave reductions, the target-logit dot product and the
-// transposing bf16 store of a tile into a vocabulary-major [v][t] array.
+// bf16 store of a tile into a vocabulary-major [v][t] array.
 #pragma once
 
 #include <cmath>
@@ -37,9 +37,12 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float((uint32_t)b << 16);
 }
 
+// Two floats rounded to bf16 (nearest even) and packed, lo in the low half:
+// one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const __bf16 a = (__bf16)lo, b = (__bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 // a where off < lim, else b, as (a & mask) | (b & ~mask) with mask = all ones
@@ -137,41 +140,6 @@ __device__ __forceinline__ T* uniform_ptr(T* p) {
   return reinterpret_cast<T*>(((uint64_t)hi << 32) | lo);
 }
 
-// Transposing tile store.  A lane holds four consecutive vocabulary rows
-// v0..v0+3 of one token.  The four lanes of a quad (tokens t0..t0+3) transpose
-// their 4 x 4 block with two lane exchanges (DPP quad permutes; 16-bit halves
-// regrouped with byte permutes), after which lane j of the quad holds row
-// v0 + j for tokens t0..t0+3: one 8-byte store (see dz_rows for the grouping
-// into whole cache lines).  Stores go through a per-tile buffer resource, so
-// every address is a 32-bit offset from the tile's corner.
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ uint32_t quad_xor1(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xf, 0xf, false);  // [1,0,3,2]
-}
-__device__ __forceinline__ uint32_t quad_xor2(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xf, 0xf, false);  // [2,3,0,1]
-}
-// byte permute: selector byte k picks byte k of the result from
-// {hi (bytes 4..7), lo (bytes 0..3)}
-__device__ __forceinline__ uint32_t byte_perm(uint32_t hi, uint32_t lo, uint32_t sel) {
-  return __builtin_amdgcn_perm(hi, lo, sel);
-}
-
-// Selectors of the quad transpose for lane position j = lane % 4.
-struct QuadSel {
-  uint32_t send1, pick, send2, w0, w1;
-  __device__ __forceinline__ QuadSel() {
-    const int j = threadIdx.x & 3;
-    const bool lo2 = j < 2, ev = (j & 1) == 0;
-    send1 = lo2 ? 0x07060504u : 0x03020100u;  // lanes 0, 1 send rows 2, 3
-    pick = lo2 ? 0x03020100u : 0x07060504u;
-    send2 = ev ? 0x07060302u : 0x05040100u;
-    w0 = ev ? 0x05040100u : 0x03020504u;
-    w1 = ev ? 0x07060100u : 0x03020706u;
-  }
-};
-
 // Cache policy of the dz^T stores: non-temporal.  32 tiles per XCD write 4 MB
 // per round -- the whole L2 -- and, cached normally, would evict the operand
 // rows the next tiles share (measured: 1.1 ms of 15.5 at T=16384, V=152064).
@@ -180,67 +148,31 @@ struct QuadSel {
 #endif
 constexpr int kStreamStore = RBP_QSTORE_CPOL;
 
-// -dl p -> bf16 for four consecutive rows of one token, packed in pairs.
-template <bool kFull>
-__device__ __forceinline__ void dz_pack(const f32x16& acc, float ls, float dl, int mi, int rg,
-                                        int32_t lim, uint32_t& P0, uint32_t& P1) {
-  float g[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    g[i] = -dl * exp2_hw(fmaf(acc[rg * 4 + i], kLog2e, -ls));
-    if constexpr (!kFull)  // rows past the vocabulary hold zeros
-      g[i] = __uint_as_float(select_below(GL::row_off(mi, rg * 4 + i), lim,
-                                          __float_as_uint(g[i]), 0u));
-  }
-  P0 = pack_bf16x2(g[0], g[1]);
-  P1 = pack_bf16x2(g[2], g[3]);
-}
-
-// 4 x 4 transpose inside each lane quad: in, lane j holds rows r..r+3 of
-// token t0 + j as (P0 = rows r, r+1; P1 = rows r+2, r+3); out, row r + j of
-// tokens t0..t0+3 as (w0 = tokens 0, 1; w1 = tokens 2, 3).
-__device__ __forceinline__ void quad_transpose(uint32_t P0, uint32_t P1, const QuadSel& qs,
-                                               uint32_t& w0, uint32_t& w1) {
-  // step 1 (partner j ^ 2): lanes 0, 1 keep rows r, r+1 and get their
-  // partner's; lanes 2, 3 keep rows r+2, r+3.  A / B = this row pair for
-  // tokens (j & 1) and (j & 1) + 2.
-  const uint32_t r1 = quad_xor2(byte_perm(P1, P0, qs.send1));
-  const uint32_t Ah = byte_perm(r1, P0, qs.pick);
-  const uint32_t Bh = byte_perm(P1, r1, qs.pick);
-  // step 2 (partner j ^ 1): even lanes collect the first row of the pair,
-  // odd lanes the second
-  const uint32_t r2 = quad_xor1(byte_perm(Bh, Ah, qs.send2));
-  w0 = byte_perm(r2, Ah, qs.w0);
-  w1 = byte_perm(r2, Bh, qs.w1);
-}
-
-// One 32-row block of both 32-token column blocks of a wave (NI == 2).
-// Lanes 0..31 hold rows 0..3 (+8 rg) of their token, lanes 32..63 rows 4..7;
-// a lane-half swap (v_permlane32_swap) first regroups them so that lanes
-// 0..31 hold the first column block and lanes 32..63 the second, for the
-// same four rows: each store then writes 4 rows x 128 contiguous bytes, whole
-// cache lines.
+// One 32-row block (mi) of the wave's tile of dz = -dlogp p, stored into the
+// vocabulary-major array Gt[v][t].  B is loaded with paired rows
+// (gemm_dma.h, kKPaired), so lane l holds tokens 2 (l % 32) and
+// 2 (l % 32) + 1 (tiles ni = 0, 1) of the same 16 vocabulary rows: per row the
+// two values are packed into one bf16 pair and stored as 4 bytes, lanes 0..31
+// writing 128 contiguous bytes of one row and lanes 32..63 those of the row
+// 4 below -- whole cache lines, with no exchange between lanes.  Stores go
+// through a per-tile buffer resource (32-bit offsets from the tile's corner).
+// Rows past the vocabulary hold zeros.
 template <bool kFull>
 __device__ __forceinline__ void dz_rows(const f32x16 (&acc)[GL::MI][GL::NI], const float (&ls)[2],
                                         const float (&dl)[2], int mi, int32_t lim,
-                                        const QuadSel& qs, __amdgpu_buffer_rsrc_t rGt,
-                                        uint32_t off, int64_t ldGt) {
-  static_assert(GL::NI == 2, "two column blocks per wave");
+                                        __amdgpu_buffer_rsrc_t rGt, uint32_t off, int64_t ldGt) {
+  static_assert(GL::NI == 2, "two column tiles per wave");
 #pragma unroll
-  for (int rg = 0; rg < 4; ++rg) {
-    uint32_t X0, X1, Y0, Y1;  // column block 0 / 1, rows (0,1) / (2,3) of the lane's half
-    dz_pack<kFull>(acc[mi][0], ls[0], dl[0], mi, rg, lim, X0, X1);
-    dz_pack<kFull>(acc[mi][1], ls[1], dl[1], mi, rg, lim, Y0, Y1);
-    const auto s0 = __builtin_amdgcn_permlane32_swap(X0, Y0, false, false);
-    const auto s1 = __builtin_amdgcn_permlane32_swap(X1, Y1, false, false);
-    // s0[0], s1[0]: rows 0..3 of the group; s0[1], s1[1]: rows 4..7
-    uint32_t w0, w1;
-    const int ro = mi * 32 + rg * 8;  // first row of the 8-row group within the wave's block
-    quad_transpose(s0[0], s1[0], qs, w0, w1);
-    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rGt, off, (int)(ro * ldGt * 2), kStreamStore);
-    quad_transpose(s0[1], s1[1], qs, w0, w1);
-    __builtin_amdgcn_raw_buffer_store_b64(u32x2{w0, w1}, rGt, off, (int)((ro + 4) * ldGt * 2),
-                                          kStreamStore);
+  for (int r = 0; r < 16; ++r) {
+    float g[2];
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      g[ni] = -dl[ni] * exp2_hw(fmaf(acc[mi][ni][r], kLog2e, -ls[ni]));
+      if constexpr (!kFull)
+        g[ni] = __uint_as_float(select_below(GL::row_off(mi, r), lim, __float_as_uint(g[ni]), 0u));
+    }
+    __builtin_amdgcn_raw_buffer_store_b32(pack_bf16x2(g[0], g[1]), rGt, off,
+                                          (int)(GL::row_off(mi, r) * ldGt * 2), kStreamStore);
   }
 }
 

@@ -26,6 +26,9 @@ using rbp::gemm::Tile;
 using rbp::gemm::tile_stream;
 using rbp::gemm::map_tile;
 using rbp::gemm::Operand;
+using rbp::gemm::kKMajor;
+using rbp::gemm::kMNMajor;
+using rbp::gemm::kKPaired;
 
 // Backward step 1: recompute the tile and write dz = dlogp (onehot - p) as
 // bf16, vocabulary-major (Gt[v][t], the layout both later products read).
@@ -43,8 +46,6 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
   __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
   const Operand A{W, d, V, d};
   const Operand B{Hc, d, Tn, d};
-  const QuadSel qs;
-  const int j = threadIdx.x & 3;
   auto tile_of = [&](int32_t vid) {
     int32_t tm, tn;
     map_tile(vid, (int32_t)tiles_m, (int32_t)tiles_n, kGroupLogits, tm, tn);
@@ -57,7 +58,7 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
     const Tile tile = tile_of(vid);
 #pragma unroll
     for (int ni = 0; ni < GL::NI; ++ni) {
-      const int64_t t = tile.n0 + GL::col(ni);
+      const int64_t t = tile.n0 + GL::col_paired(ni);
       const bool valid = t < Tn && (seq == nullptr || seq[t] >= 0);
       ls[ni] = valid ? lse[t] * kLog2e : INFINITY;
       dl[ni] = valid ? dlogp[t] : 0.0f;
@@ -72,22 +73,18 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
     // the tile's 256 x 256 corner of Gt
     const auto rGt = __builtin_amdgcn_make_buffer_rsrc(Gt + (int64_t)tile.m0 * ldGt + tile.n0, 0,
                                                        (int)(256 * ldGt * 2), 0x00020000);
-    // this lane's store: row (wave's first row) + j, tokens (wave's first
-    // token) + 32 (lane / 32) + 4 (quad) .. + 3
-    const int lane = threadIdx.x & 63;
-    const uint32_t off =
-        (uint32_t)((GL::wm() * (256 / GL::WM) + j) * ldGt + GL::wn() * (256 / GL::WN) +
-                   32 * (lane >> 5) + ((lane & 31) - j)) * 2u;
+    // lane l: row GL::row(0, 0), tokens 2 (l % 32) and 2 (l % 32) + 1
+    const uint32_t off = (uint32_t)(GL::row(0, 0) * ldGt + GL::col_paired(0)) * 2u;
 #pragma unroll
     for (int mi = 0; mi < GL::MI; ++mi) {
       if (vlim >= 256)
-        dz_rows<true>(acc, ls, dl, mi, lim, qs, rGt, off, ldGt);
+        dz_rows<true>(acc, ls, dl, mi, lim, rGt, off, ldGt);
       else
-        dz_rows<false>(acc, ls, dl, mi, lim, qs, rGt, off, ldGt);
+        dz_rows<false>(acc, ls, dl, mi, lim, rGt, off, ldGt);
     }
     if (vid + (int32_t)gridDim.x < n_vid) load_token_terms(vid + (int32_t)gridDim.x);
   };
-  tile_stream<GL, false, false>(A, B, n_vid, smem, tile_of, epi);
+  tile_stream<GL, kKMajor, kKPaired>(A, B, n_vid, smem, tile_of, epi);
 }
 
 // Backward step 1b, after the tile pass: the target entry of each valid
@@ -162,7 +159,7 @@ RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
         }
     }
   };
-  tile_stream<GL, true, true>(A, B, n_vid, smem, tile_of, epi);
+  tile_stream<GL, kMNMajor, kMNMajor>(A, B, n_vid, smem, tile_of, epi);
 }
 
 // dH += part[i] over the tiles vid_base + i of a split dhidden launch; one
@@ -293,7 +290,7 @@ RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
         }
     }
   };
-  tile_stream<GL, true, false>(A, B, n_vid, smem, tile_of, epi);
+  tile_stream<GL, kMNMajor, kKMajor>(A, B, n_vid, smem, tile_of, epi);
 }
 
 // dW += part[i] over the tiles vid_base + i (i < n_tiles) of a split

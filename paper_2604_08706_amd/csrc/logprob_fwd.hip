@@ -22,6 +22,7 @@ using namespace rbp::lp;
 using rbp::gemm::kLdsBytes;
 using rbp::gemm::Tile;
 using rbp::gemm::tile_stream;
+using rbp::gemm::kKMajor;
 using rbp::gemm::map_tile;
 using rbp::gemm::Operand;
 
@@ -58,7 +59,7 @@ RBP_LOGITS_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
         part[half * ld_part + tile.n0 + GL::col(ni)] = make_float2(mx[ni], sum[ni]);
     }
   };
-  tile_stream<GL, false, false>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
+  tile_stream<GL, kKMajor, kKMajor>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
 }
 
 // (m, s) <- merge with the partial (Mi, Si), rescaling to the larger max.
