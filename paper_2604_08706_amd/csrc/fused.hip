@@ -217,7 +217,7 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
     }
     if (vid + (int32_t)gridDim.x < n_vid) load_ref(vid + (int32_t)gridDim.x);
   };
-  tile_stream<GL, kKMajor, kKPaired>(A, B, n_vid, smem, tile_of, epi);
+  tile_stream<GL, kKMajor, kKPaired, kDeepLogits>(A, B, n_vid, smem, tile_of, epi);
 }
 
 // (m, s, e) <- merge with the partial (Mi, Si, Ei), rescaling to the larger max.

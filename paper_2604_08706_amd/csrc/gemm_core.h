@@ -33,7 +33,9 @@ typedef __bf16 bf16x8 __attribute__((__vector_size__(16)));
 typedef float f32x16 __attribute__((__vector_size__(64)));
 
 constexpr int kTileBytes = 256 * 64 * 2;   // one operand tile, 32 KiB
-constexpr int kLdsBytes = 4 * kTileBytes;  // two stages of A + B, 128 KiB
+// five operand tiles -- three buffers of one operand, two of the other --
+// 160 KiB, the whole LDS of a gfx950 compute unit (gemm_dma.h)
+constexpr int kLdsBytes = 5 * kTileBytes;
 
 // Stored operand: element (mn, k) is ptr[mn * ld + k].  Reads outside
 // [0, mn_extent) x [0, k_extent) are replaced by zeros; k_extent % 8 == 0

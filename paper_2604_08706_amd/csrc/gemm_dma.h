@@ -1,5 +1,6 @@
 // The K loop of every bf16 product: operands streamed HBM -> LDS with direct
-// loads (gfx950 buffer_load_dwordx4 ... lds), K step 64, two LDS stages.
+// loads (gfx950 buffer_load_dwordx4 ... lds), K step 64, one operand in three
+// LDS buffers and the other in two (160 KiB, the whole LDS).
 //
 // * Direct loads need no staging registers and no ds_write instructions.  A
 //   load instruction writes 64 lanes x 16 bytes to LDS at M0 + 16 * lane, i.e.
@@ -8,10 +9,14 @@
 //   fetches logical chunk p ^ swz(row).
 // * 128-byte rows make every row segment a whole cache line: measured L2 ->
 //   CU rate ~28 TB/s for 128-byte segments against ~16 TB/s for 64-byte ones.
-// * The loads of step s + 1 are issued right after the barrier that frees
-//   their stage -- one full step ahead -- half during the last K slice of one
-//   step and half during the first slice of the next, spread between MFMAs so
-//   the wave's MFMA issue never waits behind a burst of loads.
+// * Both operands' loads of step s + 2 are issued during step s, spread
+//   between MFMAs so the wave's MFMA issue never waits behind a burst of
+//   loads: the three-buffer ("deep") operand's in the first K slice, the
+//   other's right after the barrier that frees its buffer, in the last.  A
+//   fill therefore has ~1.75 (deep) or ~1 step of MFMAs to land, where two
+//   buffers per operand gave ~1 and ~0.75: operand rows missing the L2 (every
+//   step's first request for a panel row goes to the Infinity Cache or HBM)
+//   arrive before the barrier that needs them.
 // * Fragments are read one K slice (16) ahead of the MFMAs that use them; the
 //   first slice of step s + 1 is read right after the barrier, while the last
 //   slice of step s (already in registers) multiplies.
@@ -35,8 +40,6 @@ namespace rbp {
 namespace gemm {
 
 constexpr int kBK = 64;
-constexpr int kStageBytes = 2 * kTileBytes;  // A + B
-static_assert(2 * kStageBytes <= kLdsBytes, "two stages must fit the LDS allocation");
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
@@ -66,6 +69,13 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
+// vmcnt(N) and lgkmcnt(0) in one wait.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4));
 }
 
 // Workgroup barrier that is also a compiler memory barrier: LDS reads after it
@@ -330,26 +340,33 @@ struct SideLoad<G, kMNMajor> {
 // (every tile of a launch has the same number of K steps, nk >= 1) and
 // epi(vid, acc) consumes its finished fp32 accumulators.  kLA / kLB select
 // the layouts of A / B (kKMajor, kMNMajor, kKPaired); K-major needs
-// k_extent % 8 == 0, MN-major mn_extent % 8 == 0.
+// k_extent % 8 == 0, MN-major mn_extent % 8 == 0.  kDeep names the operand
+// with three buffers (1: A, 2: B); smem holds kLdsBytes: the deep operand's
+// buffers, then the other's two.
 //
-// The K steps of consecutive tiles form one stream through two 64-KiB LDS
-// stages (stream step g in stage g % 2), so the first steps of the next tile
-// load while the current tile's last steps multiply and its epilogue runs.
-// Per step g, with slice 0's fragments already in registers:
-//   slice 0: read slice 1; MFMAs; issue the B loads of step g + 1 (their A
-//            loads went out in step g - 1, or in the prologue);
+// The K steps of consecutive tiles form one stream through the buffers (step
+// g of the stream in deep buffer g % 3 and other buffer g % 2), so the first
+// steps of the next tile load while the current tile's last steps multiply
+// and its epilogue runs.  Per step g, with slice 0's fragments already in
+// registers:
+//   slice 0: read slice 1; MFMAs; issue the deep operand's loads of step
+//            g + 2 into its buffer (g + 2) % 3 (free since the barrier of
+//            step g - 1);
 //   slices 1, 2: read the next slice; MFMAs;
-//   wait for step g + 1's loads and this wave's LDS reads; barrier (step g + 1
-//   visible to all; stage g % 2 no longer read);
-//   slice 3: read step g + 1's slice 0; MFMAs; issue step g + 2's A loads into
-//            stage g % 2;
-//   after the last step of a tile: epi(), which may use LDS only at byte
-//   offsets >= kLdsBytes (the stages are in use) and may contain barriers.
-// The load cursor runs two steps ahead of the MFMAs; it holds its tile's
-// load views (cur) and the following tile's (nxt), refreshed once per tile.
-template <class G, int kLA, int kLB, class TileFn, class EpiFn>
+//   wait until only those loads are outstanding (step g + 1 landed) and for
+//   this wave's LDS reads; barrier (step g + 1 visible to all; step g's
+//   buffers no longer read);
+//   slice 3: read step g + 1's slice 0; MFMAs; issue the other operand's
+//            loads of step g + 2 into its buffer g % 2;
+//   after the last step of a tile: epi(), which may not use LDS (every byte
+//   of it is a buffer) and may contain barriers.
+// The load cursor runs two steps ahead of the MFMAs and recomputes its view
+// whenever it enters a new tile.
+template <class G, int kLA, int kLB, int kDeep, class TileFn, class EpiFn>
 __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, int32_t n_vid,
                                             uint8_t* smem, TileFn&& tile_of, EpiFn&& epi) {
+  static_assert(kDeep == 1 || kDeep == 2, "deep operand: 1 = A, 2 = B");
+  constexpr int nA = kDeep == 1 ? 3 : 2;
   const int32_t stride = (int32_t)gridDim.x;
   const int32_t vid0 = (int32_t)blockIdx.x;
   if (vid0 >= n_vid) return;
@@ -361,8 +378,11 @@ __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, 
   Frags<kLA, G::MI> fa;
   Frags<kLB, G::NI> fb;
   fa.init(0u, G::wm() * (256 / G::WM));
-  fb.init((uint32_t)kTileBytes, G::wn() * (256 / G::WN));
-  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(smem);
+  fb.init(0u, G::wn() * (256 / G::WN));
+  const uint32_t ldsA = (uint32_t)reinterpret_cast<uintptr_t>(smem);
+  const uint32_t ldsB = ldsA + (uint32_t)(nA * kTileBytes);
+  const uint8_t* smA = smem;
+  const uint8_t* smB = smem + nA * kTileBytes;
   const int32_t nk = k_steps(tile_of(vid0));
 
   struct TileRes {
@@ -374,35 +394,44 @@ __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, 
     const Tile t = tile_of(valid ? vid : vid0);
     return TileRes{la.res(A, t.m0, t.k_begin, valid), lb.res(B, t.n0, t.k_begin, valid)};
   };
-  // load cursor: tile qvid (views cur), K step qs; nxt = tile qvid + stride
+  // load cursor: tile qvid (view cur), K step qs
   int32_t qvid = vid0, qs = 0;
-  TileRes cur = res_of(vid0), nxt = res_of(vid0 + stride);
+  TileRes cur = res_of(vid0);
   auto advance = [&]() {
     if (++qs == nk) {
       qs = 0;
       qvid += stride;
-      cur = nxt;
+      cur = res_of(qvid);
     }
   };
-  auto issue_a = [&](uint32_t stage, int j) { la.issue(stage, cur.a, qs, j); };
-  auto issue_b = [&](uint32_t stage, int j) { lb.issue(stage + kTileBytes, cur.b, qs, j); };
-  auto read = [&](const uint8_t* stage, int ks, bf16x8 (&a)[G::MI], bf16x8 (&b)[G::NI]) {
-    fa.read(stage, ks, a);
-    fb.read(stage, ks, b);
+  auto issue_a = [&](uint32_t buf, int j) {
+    la.issue(ldsA + buf * (uint32_t)kTileBytes, cur.a, qs, j);
   };
+  auto issue_b = [&](uint32_t buf, int j) {
+    lb.issue(ldsB + buf * (uint32_t)kTileBytes, cur.b, qs, j);
+  };
+  auto read = [&](uint32_t ba, uint32_t bb, int ks, bf16x8 (&a)[G::MI], bf16x8 (&b)[G::NI]) {
+    fa.read(smA + ba * kTileBytes, ks, a);
+    fb.read(smB + bb * kTileBytes, ks, b);
+  };
+  // buffers of the deep operand for steps g, g + 1, g + 2 (rotating mod 3)
+  // and of the other for step g (its step g + 1 is the other buffer, and its
+  // step g + 2 reuses step g's)
+  uint32_t d0 = 0, d1 = 1, d2 = 2, o0 = 0;
 
-  // prologue: step 0 landed, step 1's A loads in flight (its B loads are
-  // issued in step 0's first slice), cursor at step 1
+  // prologue: steps 0 and 1 issued, step 0 landed, cursor at step 2
 #pragma unroll
-  for (int j = 0; j < L; ++j) issue_a(lds0, j);
+  for (int j = 0; j < L; ++j) issue_a(0u, j);
 #pragma unroll
-  for (int j = 0; j < L; ++j) issue_b(lds0, j);
-  wait_vmcnt<0>();
-  lds_barrier();
+  for (int j = 0; j < L; ++j) issue_b(0u, j);
   advance();
-  if (qs == 0) nxt = res_of(qvid + stride);
 #pragma unroll
-  for (int j = 0; j < L; ++j) issue_a(lds0 + kStageBytes, j);
+  for (int j = 0; j < L; ++j) issue_a(1u, j);
+#pragma unroll
+  for (int j = 0; j < L; ++j) issue_b(1u, j);
+  advance();
+  wait_vmcnt<2 * L>();
+  lds_barrier();
 
   int32_t mvid = vid0, mit = 0;
   f32x16 acc[G::MI][G::NI];
@@ -413,35 +442,49 @@ __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, 
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.0f;
   bf16x8 a0[G::MI], b0[G::NI], a1[G::MI], b1[G::NI];
-  read(smem, 0, a0, b0);
-  for (uint32_t g = 0;; ++g) {
-    const uint8_t* cur_st = smem + (g & 1) * kStageBytes;
-    const uint8_t* nxt_st = smem + ((g + 1) & 1) * kStageBytes;
-    const uint32_t st_next = lds0 + ((g + 1) & 1) * kStageBytes;
-    const uint32_t st_cur = lds0 + (g & 1) * kStageBytes;
-    read(cur_st, 1, a1, b1);
+  read(0u, 0u, 0, a0, b0);
+  for (;;) {
+    const uint32_t ca = kDeep == 1 ? d0 : o0, cb = kDeep == 2 ? d0 : o0;
+    const uint32_t na = kDeep == 1 ? d1 : (o0 ^ 1u), nb = kDeep == 2 ? d1 : (o0 ^ 1u);
+    read(ca, cb, 1, a1, b1);
     RBP_FENCE();
-    mfma_tiles_interleaved<G>(a0, b0, acc, L, [&](int l) { issue_b(st_next, l); });
+    mfma_tiles_interleaved<G>(a0, b0, acc, L, [&](int l) {
+      if constexpr (kDeep == 1)
+        issue_a(d2, l);
+      else
+        issue_b(d2, l);
+    });
     RBP_FENCE();
-    advance();
-    read(cur_st, 2, a0, b0);
+    read(ca, cb, 2, a0, b0);
     RBP_FENCE();
     mfma_tiles<G>(a1, b1, acc);
     RBP_FENCE();
-    read(cur_st, 3, a1, b1);
+    read(ca, cb, 3, a1, b1);
     RBP_FENCE();
     mfma_tiles<G>(a0, b0, acc);
     RBP_FENCE();
-    // step g + 1 landed (only its loads are outstanding); this wave's reads
-    // of stage g % 2 done, so after the barrier the stage may be refilled
-    __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) lgkmcnt(0)
+    // step g + 1 landed (only the deep operand's step g + 2 loads are
+    // outstanding); this wave's reads of step g done
+    wait_vmcnt_lgkm0<L>();
     lds_barrier();
-    // unconditional (after the last step it reads a stale stage): a read under
-    // a branch would make the compiler wait for it before the MFMAs below
-    read(nxt_st, 0, a0, b0);
+    // unconditional (after the last step it reads a stale buffer)
+    read(na, nb, 0, a0, b0);
     RBP_FENCE();
-    mfma_tiles_interleaved<G>(a1, b1, acc, L, [&](int l) { issue_a(st_cur, l); });
+    mfma_tiles_interleaved<G>(a1, b1, acc, L, [&](int l) {
+      if constexpr (kDeep == 1)
+        issue_b(o0, l);
+      else
+        issue_a(o0, l);
+    });
     RBP_FENCE();
+    advance();
+    {
+      const uint32_t t = d0;
+      d0 = d1;
+      d1 = d2;
+      d2 = t;
+      o0 ^= 1u;
+    }
     if (++mit == nk) {
       epi(mvid, acc);
 #pragma unroll
@@ -453,7 +496,6 @@ __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, 
       mvid += stride;
       if (mvid >= n_vid) break;
       mit = 0;
-      nxt = res_of(qvid + stride);
     }
   }
   wait_vmcnt<0>();

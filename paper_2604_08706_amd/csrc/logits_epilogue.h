@@ -28,6 +28,13 @@ using GL = rbp::gemm::Grid8;
   __global__ __attribute__((amdgpu_flat_work_group_size(GL::kThreads, GL::kThreads), \
                             amdgpu_waves_per_eu(GL::kWaves / 4, GL::kWaves / 4)))
 
+// The operand each product keeps in three LDS buffers (gemm_dma.h
+// tile_stream; 1: A, 2: B), measured per product at the 7B head: the logit
+// products W (A), dW the hidden states (A), dhidden dz^T (B).
+constexpr int kDeepLogits = 1;
+constexpr int kDeepDw = 1;
+constexpr int kDeepDh = 2;
+
 // 2^x on the hardware unit (v_exp_f32, ~1 ulp).  Arguments here are
 // (z - max) * log2 e <= 0; below -126 the result flushes toward zero, which
 // only drops terms under 2^-126 of the largest one in a sum.

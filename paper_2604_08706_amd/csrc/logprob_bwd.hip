@@ -84,7 +84,7 @@ RBP_LOGITS_KERNEL void grad_logits_kernel(const uint16_t* __restrict__ W,
     }
     if (vid + (int32_t)gridDim.x < n_vid) load_token_terms(vid + (int32_t)gridDim.x);
   };
-  tile_stream<GL, kKMajor, kKPaired>(A, B, n_vid, smem, tile_of, epi);
+  tile_stream<GL, kKMajor, kKPaired, kDeepLogits>(A, B, n_vid, smem, tile_of, epi);
 }
 
 // Backward step 1b, after the tile pass: the target entry of each valid
@@ -159,7 +159,7 @@ RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
         }
     }
   };
-  tile_stream<GL, kMNMajor, kMNMajor>(A, B, n_vid, smem, tile_of, epi);
+  tile_stream<GL, kMNMajor, kMNMajor, kDeepDh>(A, B, n_vid, smem, tile_of, epi);
 }
 
 // dH += part[i] over the tiles vid_base + i of a split dhidden launch; one
@@ -290,7 +290,7 @@ RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
         }
     }
   };
-  tile_stream<GL, kMNMajor, kKMajor>(A, B, n_vid, smem, tile_of, epi);
+  tile_stream<GL, kMNMajor, kKMajor, kDeepDw>(A, B, n_vid, smem, tile_of, epi);
 }
 
 // dW += part[i] over the tiles vid_base + i (i < n_tiles) of a split

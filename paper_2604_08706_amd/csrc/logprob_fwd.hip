@@ -59,7 +59,8 @@ RBP_LOGITS_KERNEL void logits_lse_partial_kernel(const uint16_t* __restrict__ W,
         part[half * ld_part + tile.n0 + GL::col(ni)] = make_float2(mx[ni], sum[ni]);
     }
   };
-  tile_stream<GL, kKMajor, kKMajor>(A, B, (int32_t)(tiles_m * tiles_n), smem, tile_of, epi);
+  tile_stream<GL, kKMajor, kKMajor, kDeepLogits>(A, B, (int32_t)(tiles_m * tiles_n), smem,
+                                                tile_of, epi);
 }
 
 // (m, s) <- merge with the partial (Mi, Si), rescaling to the larger max.
