@@ -177,42 +177,74 @@ RBP_LOGITS_KERNEL void logits_store_kernel(const uint16_t* __restrict__ W,
     const Tile tile = tile_of(vid);
     const int32_t vlim = V - tile.m0;
     const int32_t lim = vlim - GL::row(0, 0);
-    float mx[GL::NI];
-    if (vlim >= 256)
-      column_max<true>(acc, 0, mx);
-    else
-      column_max<false>(acc, lim, mx);
-    // a half tile past the vocabulary has M = -inf: offset 0 keeps its
-    // (discarded) exponentials finite, and f = exp(-inf) = 0
-    float ls[GL::NI], f[GL::NI], S[GL::NI] = {0.0f, 0.0f}, E[GL::NI] = {0.0f, 0.0f};
-#pragma unroll
-    for (int ni = 0; ni < GL::NI; ++ni) {
-      ls[ni] = mx[ni] == -INFINITY ? 0.0f : mx[ni] * kLog2e;
-      f[ni] = stores_against_ref(mx[ni], Rr[ni]) ? exp2_hw((mx[ni] - Rr[ni]) * kLog2e) : 1.0f;
-    }
     const auto rQ = __builtin_amdgcn_make_buffer_rsrc(
         uniform_ptr(Qt + (int64_t)tile.m0 * ldQ + tile.n0), 0, (int)(256 * ldQ * 2), 0x00020000);
     // lane l: row GL::row(0, 0), tokens 2 (l % 32) and 2 (l % 32) + 1
     const uint32_t off = (uint32_t)(GL::row(0, 0) * ldQ + GL::col_paired(0)) * 2u;
+    // the partial of each of the lane's columns: reference (the exponent
+    // offset of S, E and the stored q), S = sum exp(z - ref), E = sum exp(z - ref) z
+    float ref[GL::NI], s[GL::NI], e[GL::NI];
+    // Direct store against the token's reference: q = exp(z - R_t), no max
+    // pass and no rescaling.  Kept when every column of the wave's half tile
+    // has a sum in [2^-60, 2^28] (q <= 2^28 ~ e^19.4, and the half tile's
+    // largest logit within ~47 of R_t); otherwise (or a NaN reference) the
+    // half tile is redone below against its own maximum, overwriting q.
+    bool direct = false;
+    if (vlim >= 256) {
+      const float ls[GL::NI] = {Rr[0] * kLog2e, Rr[1] * kLog2e};
+      const float one[GL::NI] = {1.0f, 1.0f};
+      float S[GL::NI] = {0.0f, 0.0f}, E[GL::NI] = {0.0f, 0.0f};
 #pragma unroll
-    for (int mi = 0; mi < GL::MI; ++mi) {
+      for (int mi = 0; mi < GL::MI; ++mi)
+        q_rows<true, kEnt>(acc, ls, one, mi, lim, rQ, off, ldQ, S, E);
+      bool ok = true;
+#pragma unroll
+      for (int ni = 0; ni < GL::NI; ++ni) {
+        s[ni] = S[ni] + __shfl_xor(S[ni], 32, 64);
+        e[ni] = kEnt ? E[ni] + __shfl_xor(E[ni], 32, 64) : 0.0f;
+        ref[ni] = Rr[ni];
+        ok = ok && s[ni] >= 0x1p-60f && s[ni] <= 0x1p28f;  // false for NaN
+      }
+      direct = __all(ok);
+    }
+    if (!direct) {
+      float mx[GL::NI];
       if (vlim >= 256)
-        q_rows<true, kEnt>(acc, ls, f, mi, lim, rQ, off, ldQ, S, E);
+        column_max<true>(acc, 0, mx);
       else
-        q_rows<false, kEnt>(acc, ls, f, mi, lim, rQ, off, ldQ, S, E);
+        column_max<false>(acc, lim, mx);
+      // a half tile past the vocabulary has M = -inf: offset 0 keeps its
+      // (discarded) exponentials finite, and f = exp(-inf) = 0
+      float ls[GL::NI], f[GL::NI], S[GL::NI] = {0.0f, 0.0f}, E[GL::NI] = {0.0f, 0.0f};
+#pragma unroll
+      for (int ni = 0; ni < GL::NI; ++ni) {
+        ls[ni] = mx[ni] == -INFINITY ? 0.0f : mx[ni] * kLog2e;
+        f[ni] = stores_against_ref(mx[ni], Rr[ni]) ? exp2_hw((mx[ni] - Rr[ni]) * kLog2e) : 1.0f;
+      }
+#pragma unroll
+      for (int mi = 0; mi < GL::MI; ++mi) {
+        if (vlim >= 256)
+          q_rows<true, kEnt>(acc, ls, f, mi, lim, rQ, off, ldQ, S, E);
+        else
+          q_rows<false, kEnt>(acc, ls, f, mi, lim, rQ, off, ldQ, S, E);
+      }
+#pragma unroll
+      for (int ni = 0; ni < GL::NI; ++ni) {
+        s[ni] = S[ni] + __shfl_xor(S[ni], 32, 64);
+        e[ni] = kEnt ? E[ni] + __shfl_xor(E[ni], 32, 64) : 0.0f;
+        ref[ni] = mx[ni];
+      }
     }
     // both lane halves hold rows of the same columns; the lower half writes
-    // the sums, 128 contiguous bytes per array and column block
+    // the partials, 128 contiguous bytes per array and column block
     const int64_t half = (int64_t)(tile.m0 >> 7) + GL::wm();
 #pragma unroll
     for (int ni = 0; ni < GL::NI; ++ni) {
-      const float s = S[ni] + __shfl_xor(S[ni], 32, 64);
-      const float e = kEnt ? E[ni] + __shfl_xor(E[ni], 32, 64) : 0.0f;
       if (lane < 32) {
         const int64_t o = half * ldp + tile.n0 + GL::col_paired(ni);
-        pM[o] = mx[ni];
-        pS[o] = s;
-        if (kEnt) pE[o] = e;
+        pM[o] = ref[ni];
+        pS[o] = s[ni];
+        if (kEnt) pE[o] = e[ni];
       }
     }
     if (vid + (int32_t)gridDim.x < n_vid) load_ref(vid + (int32_t)gridDim.x);
