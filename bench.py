@@ -5,8 +5,9 @@ One step = the whole trainer-side path over one replay micro-batch:
   rb_sample_gather      (uniform draws from a 1024-record FIFO buffer, packed
                          into a 16384-token micro-batch)
   policy_fused_fwd_bwd  (one pass: logits hidden [16384, 3584] x W [152064,
-                         3584] in bf16 MFMA tiles with the log-sum-exp and
-                         exp(z - M) kept per tile, the clipped GRPO loss with
+                         3584] in bf16 MFMA tiles with the log-sum-exp
+                         partials and q = exp(z - R_t) kept per tile (R_t the
+                         token's reference), the clipped GRPO loss with
                          token ratios and group advantages, and the backward
                          to dhidden and dW, dW accumulated as over
                          micro-batches; 6 d V flop per token)
@@ -50,15 +51,15 @@ TRAFFIC_SOURCES = ("fused.hip", "logprob_bwd.hip", "logits_epilogue.h", "gemm_co
 #   dW      = dweight_kernel (main launch + last-round launch) + part_add_kernel
 #   dhidden = dhidden_kernel (main launch + last-round launch) + part_add_dh_kernel
 TRAFFIC = {
-    "sources_sha256": "ade79da6e378bc995fbc76ea762f88c134fc28f6edc5677ae1f0c2ebab7f2ad9",
-    "bytes": {"logits": 36011144192, "dW": 34090914816, "dhidden": 39245122560},
+    "sources_sha256": "7e55dcba4c5529133368c0f2eda21c0d2f629e95ae56add91cc8ef7a56e0c454",
+    "bytes": {"logits": 34934814720, "dW": 42042163200, "dhidden": 43714963456},
 }
 
 # the three products of the single pass, by the phase that times them
 PRODUCTS = {
-    "logits": "logits_store_kernel (forward product; stores exp(z - M) as bf16)",
+    "logits": "logits_store_kernel (forward product; stores q = exp(z - R_t) as bf16)",
     "dW": "dweight_kernel (dW product)",
-    "dhidden": "dhidden_kernel + add_f32_kernel (dhidden product, split-K 2)",
+    "dhidden": "dhidden_kernel (dhidden product: main launch + last-round K halves)",
 }
 
 
@@ -675,8 +676,8 @@ def main():
     tok_s = tok / (f["ms_total"] / 1e3)
     frac = tok_s * 6 * dV / PEAK_BF16
     ph = f["phase_ms"]
-    # the three products; the dW phase holds its two launches and, beside the
-    # first, the side stream's part of the rescale
+    # the three products; the dW and dhidden phases each hold a main launch,
+    # a launch of the last round's K halves and the small kernel that adds them
     products = {k: ph[k] for k in PRODUCTS}
     dom = max(products, key=products.get)
     dom_ms = products[dom]
