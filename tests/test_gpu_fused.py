@@ -335,16 +335,20 @@ def test_fused_phase_events():
         assert torch.equal(a[key], c[key]), key
 
 
-@pytest.mark.parametrize("shift,adv_sign", [(35.0, 1.0), (-45.0, -1.0), ("mixed", 0.0)])
+@pytest.mark.parametrize("shift,adv_sign", [(35.0, 1.0), (-45.0, -1.0), ("mixed", 0.0),
+                                            (15.0, 1.0), (-30.0, -1.0)])
 def test_fused_tokens_off_their_reference(shift, adv_sign):
     """Tokens whose behaviour log-prob puts the reference R_t far from their
     largest logit take the re-referencing path: old = logp + 35 (ratio e^-35,
     positive advantages, so a tiny but unclipped gradient) or old = logp - 45
     (ratio e^45, negative advantages: an unclipped gradient e^45 times the
     usual).  'mixed': half the sequences shifted by +35, the rest ordinary, so
-    the pass must leave the ordinary tokens' columns alone.  Everything
-    against the oracle at the usual bars; in the mixed case dhidden is also
-    checked on each group's rows alone."""
+    the pass must leave the ordinary tokens' columns alone.  Shifts of +15
+    and -30 keep every half tile's sums inside the range the store pass takes
+    directly against R_t (q up to e^15; c_t of order e^30), so that path is
+    checked far from R_t = lse_t too.  Everything against the oracle at the
+    usual bars; in the mixed case dhidden is also checked on each group's
+    rows alone."""
     rbp = require_gpu()
     T, d, V = 700, 136, 4097
     (hidden, W, tokens, seq, lens, h64, W64, y, want_logp, want_lse, old,
