@@ -51,7 +51,7 @@ TRAFFIC_SOURCES = ("fused.hip", "logprob_bwd.hip", "logits_epilogue.h", "gemm_co
 #   dW      = dweight_kernel (main launch + last-round launch) + part_add_kernel
 #   dhidden = dhidden_kernel (main launch + last-round launch) + part_add_dh_kernel
 TRAFFIC = {
-    "sources_sha256": "7e55dcba4c5529133368c0f2eda21c0d2f629e95ae56add91cc8ef7a56e0c454",
+    "sources_sha256": "8643d9a908cb10d4624f089277e9061c1758e3edea78c40a17649acbf37ffebd",
     "bytes": {"logits": 34934814720, "dW": 42042163200, "dhidden": 43714963456},
 }
 

@@ -384,9 +384,11 @@ typedef struct rbp_exec {
  * behaviour log-prob implies (lse_t - log rho_t), so the stored values are
  * p_{t,v} / rho_t and the backward's dz is one scalar per token times them:
  * the logits never reach memory and no pass over the array rescales it.
- * A token whose R_t lies outside [M_t - 20, M_t + 40] (M_t its largest
- * logit: a ratio below about e^-20 or above e^40, or an invalid old_logp)
- * is re-referenced to M_t by a pass over its column alone.  dz is rounded to
+ * A token whose R_t lies too far from its logits for exp(z - R_t) to stay in
+ * range -- R_t below M_t - 20 or above M_t + 40 to 47 (M_t its largest
+ * logit: a ratio below about e^-20 or above about e^40), or an invalid
+ * old_logp -- is re-referenced to its largest logit by a pass over its
+ * column alone.  dz is rounded to
  * bf16 once (as exp(z - R_t)); the dW product reads h_t scaled by the token's
  * factor, rounded to bf16.
  * exec: NULL, or the caller's rbp_exec of phase events.

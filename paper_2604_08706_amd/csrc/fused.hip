@@ -17,16 +17,20 @@
 //      equal to lse_t - log rho_t (rho_t the importance ratio, close to 1 for
 //      a replayed token);
 //   1. Z^T = W H^T tile by tile.  For each token column and 128-row half tile
-//      i (one wave's rows), the epilogue writes the partial M_i = max z,
-//      S_i = sum exp(z - M_i), E_i = sum exp(z - M_i) z, and stores
-//      q = exp(z - R_t) as bf16 into Q^T [Vp][Tc] (the layout the backward
-//      products read) -- or, where that would exceed exp(20) (M_i > R_t + 20),
-//      q = exp(z - M_i);
+//      i (one wave's rows), the epilogue stores q = exp(z - R_t) as bf16 into
+//      Q^T [Vp][Tc] (the layout the backward products read) and writes the
+//      partial (M_i, S_i, E_i) = (R_t, sum q, sum q z) -- or, for a half tile
+//      whose sums leave [2^-60, 2^28] (R_t too far from its logits) or whose
+//      reference is NaN, M_i = max z, S_i = sum exp(z - M_i), E_i = sum
+//      exp(z - M_i) z and q = exp(z - R_t), or q = exp(z - M_i) where that
+//      would exceed exp(20) (M_i > R_t + 20): M_i is always the reference of
+//      the half tile's sums;
 //   2. merge: lse and entropy from the partials, logp from the target logit;
-//      a token is "referenced" when R_t lies in [M_t - 20, M_t + 40] (M_t its
-//      largest logit); the others -- a ratio below about e^-20 or above e^40,
-//      or an invalid behaviour log-prob -- are listed and take M_t as their
-//      reference instead;
+//      a token is "referenced" when R_t lies in [M_t - 20, M_t + 40], M_t the
+//      largest reference of its partials (its largest logit whenever a half
+//      tile was stored against its own maximum); the others -- a ratio below
+//      about e^-20 or above about e^40, or an invalid behaviour log-prob --
+//      are listed and take M_t as their reference instead;
 //   3. the loss pass writes dlogp (policy_loss_fwd_bwd);
 //   4. the listed tokens' columns of Q^T are re-referenced to M_t in place;
 //      then per token c_t = -dlogp_t exp(ref_t - lse_t), so that
@@ -105,9 +109,9 @@ __device__ __forceinline__ void q_rows(const f32x16 (&acc)[GL::MI][GL::NI], cons
 // A half tile stores against the token's reference R_t unless its largest
 // logit exceeds R_t by more than kRefAbove (q would pass exp(20)); a token
 // keeps R_t as its reference when R_t is within [M_t - kRefAbove,
-// M_t + kRefBelow] of its largest logit M_t (the top entries' q then stay in
-// [exp(-40), exp(20)] and c_t = -dlogp_t rho_t stays finite).  The same fp32
-// comparison is made wherever the decision is needed.
+// M_t + kRefBelow] of the largest reference M_t of its partials (the top
+// entries' q then stay in [exp(-47), exp(20)] and c_t = -dlogp_t rho_t stays
+// finite).  The same fp32 comparison is made wherever the decision is needed.
 constexpr float kRefAbove = 20.0f;
 constexpr float kRefBelow = 40.0f;
 
