@@ -336,7 +336,8 @@ def test_fused_phase_events():
 
 
 @pytest.mark.parametrize("shift,adv_sign", [(35.0, 1.0), (-45.0, -1.0), ("mixed", 0.0),
-                                            (15.0, 1.0), (-30.0, -1.0)])
+                                            (15.0, 1.0), (-30.0, -1.0), (22.0, 1.0),
+                                            (24.0, 1.0), (-37.5, -1.0), (-38.5, -1.0)])
 def test_fused_tokens_off_their_reference(shift, adv_sign):
     """Tokens whose behaviour log-prob puts the reference R_t far from their
     largest logit take the re-referencing path: old = logp + 35 (ratio e^-35,
@@ -346,7 +347,12 @@ def test_fused_tokens_off_their_reference(shift, adv_sign):
     the pass must leave the ordinary tokens' columns alone.  Shifts of +15
     and -30 keep every half tile's sums inside the range the store pass takes
     directly against R_t (q up to e^15; c_t of order e^30), so that path is
-    checked far from R_t = lse_t too.  Everything against the oracle at the
+    checked far from R_t = lse_t too.  The logits here are nearly flat, so a
+    half tile's sum is about e^shift / 32 (R_t = lse_t - shift, 32 half tiles
+    at V = 4097): +22 / +24 put it just under / over the direct range's
+    upper bound 2^28, and -37.5 / -38.5 just over / under its lower bound
+    2^-60, so with the staleness noise and the spread of the logits waves
+    take either form between neighbouring tokens.  Everything against the oracle at the
     usual bars; in the mixed case dhidden is also checked on each group's
     rows alone."""
     rbp = require_gpu()
