@@ -51,8 +51,8 @@ TRAFFIC_SOURCES = ("fused.hip", "logprob_bwd.hip", "logits_epilogue.h", "gemm_co
 #   dW      = dweight_kernel (main launch + last-round launch) + part_add_kernel
 #   dhidden = dhidden_kernel (main launch + last-round launch) + part_add_dh_kernel
 TRAFFIC = {
-    "sources_sha256": "8643d9a908cb10d4624f089277e9061c1758e3edea78c40a17649acbf37ffebd",
-    "bytes": {"logits": 34934814720, "dW": 42042163200, "dhidden": 43714963456},
+    "sources_sha256": "168aab66a530955bf19461601043a038e83b401b8324e2ced642ff4548835daf",
+    "bytes": {"logits": 34395098112, "dW": 42019896320, "dhidden": 40238567424},
 }
 
 # the three products of the single pass, by the phase that times them

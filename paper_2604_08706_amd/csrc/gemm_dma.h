@@ -338,11 +338,14 @@ struct SideLoad<G, kMNMajor> {
 // Persistent tile loop.  This workgroup takes the virtual blocks blockIdx.x,
 // blockIdx.x + gridDim.x, ... below n_vid; tile_of(vid) gives each one's Tile
 // (every tile of a launch has the same number of K steps, nk >= 1) and
-// epi(vid, acc) consumes its finished fp32 accumulators.  kLA / kLB select
-// the layouts of A / B (kKMajor, kMNMajor, kKPaired); K-major needs
-// k_extent % 8 == 0, MN-major mn_extent % 8 == 0.  kDeep names the operand
-// with three buffers (1: A, 2: B); smem holds kLdsBytes: the deep operand's
-// buffers, then the other's two.
+// epi(vid, acc) consumes its finished fp32 accumulators.  An epi that
+// returns bool may return false to keep the accumulators for the
+// workgroup's next virtual block (whose K range then continues the same
+// output tile); one that returns void always starts the next block from
+// zero.  kLA / kLB select the layouts of A / B (kKMajor, kMNMajor,
+// kKPaired); K-major needs k_extent % 8 == 0, MN-major mn_extent % 8 == 0.
+// kDeep names the operand with three buffers (1: A, 2: B); smem holds
+// kLdsBytes: the deep operand's buffers, then the other's two.
 //
 // The K steps of consecutive tiles form one stream through the buffers (step
 // g of the stream in deep buffer g % 3 and other buffer g % 2), so the first
@@ -486,13 +489,19 @@ __device__ __forceinline__ void tile_stream(const Operand& A, const Operand& B, 
       o0 ^= 1u;
     }
     if (++mit == nk) {
-      epi(mvid, acc);
+      bool done = true;
+      if constexpr (std::is_same_v<decltype(epi(mvid, acc)), bool>)
+        done = epi(mvid, acc);
+      else
+        epi(mvid, acc);
+      if (done) {
 #pragma unroll
-      for (int mi = 0; mi < G::MI; ++mi)
+        for (int mi = 0; mi < G::MI; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < G::NI; ++ni)
+          for (int ni = 0; ni < G::NI; ++ni)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.0f;
+            for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.0f;
+      }
       mvid += stride;
       if (mvid >= n_vid) break;
       mit = 0;

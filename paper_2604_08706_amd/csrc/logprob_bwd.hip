@@ -162,6 +162,81 @@ RBP_LOGITS_KERNEL void dhidden_kernel(const uint16_t* __restrict__ W,
   tile_stream<GL, kMNMajor, kMNMajor, kDeepDh>(A, B, n_vid, smem, tile_of, epi);
 }
 
+// The last round of a dhidden launch when it is more than half full: its r
+// tiles (virtual tiles vid_base .. vid_base + r - 1) are cut into s pieces
+// of `steps` K steps each and run by one round of P = gridDim.x workgroups,
+// with s - 1 = ceil(r / (P - r)).  Workgroup c < r runs pieces 0 .. s - 2 of
+// tile c back to back, its accumulators carried from piece to piece, and
+// writes dH; workgroup r + e runs the last piece of tiles e, e + (P - r),
+// e + 2 (P - r), ... below r and writes each into part[i] (256 x 256 fp32,
+// [t][m]), which part_add_dh_kernel adds afterwards.  No workgroup runs more
+// than s - 1 pieces, so the round takes (s - 1) / s of a whole-vocabulary
+// tile instead of leaving P - r compute units idle for all of it.  Virtual
+// block vid = c + j P (j < s - 1) is workgroup c's j-th piece; the s r
+// pieces are exactly the blocks below s r.
+RBP_LOGITS_KERNEL void dhidden_pieces_kernel(const uint16_t* __restrict__ W,
+                                             const uint16_t* __restrict__ Gt, int64_t ldGt,
+                                             int64_t Tn, int32_t d, int32_t V,
+                                             const float* __restrict__ cs,
+                                             float* __restrict__ dH, int64_t tiles_m,
+                                             int64_t tiles_n, int32_t vid_base, int32_t r,
+                                             int32_t s, int32_t steps,
+                                             float* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[kLdsBytes];
+  const int64_t T256 = (Tn + 255) / 256 * 256;
+  const Operand A{W, d, d, V};          // (m = hidden unit, k = vocab): W[v][m]
+  const Operand B{Gt, ldGt, T256, V};   // (n = token, k = vocab): Gt[v][t]
+  const int32_t P = (int32_t)gridDim.x;
+  // tile i (of the round) and piece j of virtual block vid
+  auto piece = [&](int32_t vid, int32_t& i, int32_t& j) {
+    const int32_t c = vid % P, jj = vid / P;
+    if (c < r) {
+      i = c;
+      j = jj;
+    } else {
+      i = jj * (P - r) + (c - r);
+      j = s - 1;
+    }
+  };
+  auto tile_of = [&](int32_t vid) {
+    int32_t i, j, tm, tn;
+    piece(vid, i, j);
+    map_tile(vid_base + i, (int32_t)tiles_m, (int32_t)tiles_n, kGroupGrad, tm, tn);
+    // every piece spans `steps` steps; columns past V read as zero
+    const int32_t kb = j * steps * 64;
+    return Tile{tm * 256, tn * 256, kb, kb + steps * 64};
+  };
+  auto epi = [&](int32_t vid, f32x16 (&acc)[GL::MI][GL::NI]) -> bool {
+    int32_t i, j;
+    piece(vid, i, j);
+    if (j < s - 2) return false;  // the tile's next piece follows on this workgroup
+    // dhidden_kernel's stores: c_t-scaled, the last piece into its block
+    const Tile tile = tile_of(vid);
+    const bool to_part = j == s - 1;
+    float* blk = part + (int64_t)i * 65536;
+#pragma unroll
+    for (int ni = 0; ni < GL::NI; ++ni) {
+      const int64_t t = tile.n0 + GL::col(ni);
+      if (t >= Tn) continue;
+      const float c = cs != nullptr ? cs[t] : 1.0f;
+#pragma unroll
+      for (int mi = 0; mi < GL::MI; ++mi)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const int64_t m = tile.m0 + GL::row(mi, rg * 4);
+          const float4 val = make_float4(c * acc[mi][ni][rg * 4 + 0], c * acc[mi][ni][rg * 4 + 1],
+                                         c * acc[mi][ni][rg * 4 + 2], c * acc[mi][ni][rg * 4 + 3]);
+          if (to_part)
+            *reinterpret_cast<float4*>(blk + GL::col(ni) * 256 + GL::row(mi, rg * 4)) = val;
+          else if (m < d)
+            *reinterpret_cast<float4*>(dH + t * d + m) = val;
+        }
+    }
+    return true;
+  };
+  tile_stream<GL, kMNMajor, kMNMajor, kDeepDh>(A, B, s * r, smem, tile_of, epi);
+}
+
 // dH += part[i] over the tiles vid_base + i of a split dhidden launch; one
 // block per (tile, 16 tokens).
 __global__ void __launch_bounds__(256) part_add_dh_kernel(float* __restrict__ dH,
@@ -417,18 +492,39 @@ void rbp::launch_dhidden(const uint16_t* W, const uint16_t* Gt, int64_t ldGt, in
     return;
   }
   const int64_t r = tiles % G;
-  const int64_t rem = (nk >= 8 && tiles > G && r > 0 && 2 * r <= G &&
-                       r * 65536 <= ldGt * (int64_t)d) ? r : 0;
-  const int64_t n_main = tiles - rem;
-  hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(n_main, n_cu)),
-                     dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, cs, dhidden_c, tiles_d,
-                     tiles_t, 0, (int32_t)n_main, 0, (float*)nullptr, 0);
-  if (rem == 0) return;
-  hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(2 * rem, n_cu)),
-                     dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, cs, dhidden_c, tiles_d,
-                     tiles_t, (int32_t)n_main, (int32_t)(2 * rem), half_steps, dh_half, 0);
-  hipLaunchKernelGGL(part_add_dh_kernel, dim3((unsigned)rem, 16), dim3(256), 0, s, dhidden_c,
-                     dh_half, (int32_t)n_main, tiles_d, tiles_t, d, Tn);
+  const bool fits = r * 65536 <= ldGt * (int64_t)d;  // one scratch block per tile of the round
+  const int64_t rem = (nk >= 8 && tiles > G && r > 0 && 2 * r <= G && fits) ? r : 0;
+  // A last round more than half full: its tiles cut into pieces of the K
+  // range, s - 1 = ceil(r / (G - r)) pieces per workgroup
+  // (dhidden_pieces_kernel), when a piece keeps at least 8 steps and the
+  // last piece is not empty.
+  int64_t pieces = 0, piece_steps = 0;
+  if (2 * r > G && fits) {
+    const int64_t ps = 1 + rbp::ceil_div(r, G - r), st = rbp::ceil_div(nk, ps);
+    if (ps <= 16 && st >= 8 && (ps - 1) * st < nk) {
+      pieces = ps;
+      piece_steps = st;
+    }
+  }
+  const int64_t n_main = tiles - (rem > 0 ? rem : (pieces > 0 ? r : 0));
+  if (n_main > 0)
+    hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(n_main, n_cu)),
+                       dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, cs, dhidden_c, tiles_d,
+                       tiles_t, 0, (int32_t)n_main, 0, (float*)nullptr, 0);
+  if (rem > 0) {
+    hipLaunchKernelGGL(dhidden_kernel, dim3(rbp::gemm::stream_grid(2 * rem, n_cu)),
+                       dim3(GL::kThreads), 0, s, W, Gt, ldGt, Tn, d, V, cs, dhidden_c, tiles_d,
+                       tiles_t, (int32_t)n_main, (int32_t)(2 * rem), half_steps, dh_half, 0);
+    hipLaunchKernelGGL(part_add_dh_kernel, dim3((unsigned)rem, 16), dim3(256), 0, s, dhidden_c,
+                       dh_half, (int32_t)n_main, tiles_d, tiles_t, d, Tn);
+  } else if (pieces > 0) {
+    // grid G exactly: workgroup c's pieces are the virtual blocks c + j G
+    hipLaunchKernelGGL(dhidden_pieces_kernel, dim3((unsigned)G), dim3(GL::kThreads), 0, s, W,
+                       Gt, ldGt, Tn, d, V, cs, dhidden_c, tiles_d, tiles_t, (int32_t)n_main,
+                       (int32_t)r, (int32_t)pieces, (int32_t)piece_steps, dh_half);
+    hipLaunchKernelGGL(part_add_dh_kernel, dim3((unsigned)r, 16), dim3(256), 0, s, dhidden_c,
+                       dh_half, (int32_t)n_main, tiles_d, tiles_t, d, Tn);
+  }
 }
 
 void rbp::launch_grad_products(const uint16_t* Hc, const uint16_t* W, const uint16_t* Gt,

@@ -1,5 +1,8 @@
 """Dense-gradient parity at the benchmark's launch configuration (T = 16384,
-d = 3584, V = 152064, one chunk), for the four-call path and the single pass.
+d = 3584, V = 152064), for the four-call path and the single pass, each in one
+16384-token chunk and with a workspace for 4096-token chunks (four chunks,
+dW accumulated across them; each chunk's dhidden has 224 tiles, a last round
+more than half full, cut into K pieces).
 
 Every token of a ~2048-token block of whole sequences (inside the batch, not
 tile-aligned, spanning nine token tiles) carries the loss's gradient: its
@@ -114,10 +117,11 @@ def _check(out, want, T, V, with_entropy):
     assert np.sqrt(num_nt / den_nt) < RTOL
 
 
-def test_dense_four_call_path(case):
+@pytest.mark.parametrize("ws_tokens", [16384, 4096])
+def test_dense_four_call_path(case, ws_tokens):
     rbp, wl, dev, want = case
     T, d, V = wl.max_tokens, wl.d, wl.V
-    print("[dense] four calls", flush=True)
+    print(f"[dense] four calls, workspace for {ws_tokens} tokens", flush=True)
     out = {"logp": torch.empty(T, device="cuda"), "lse": torch.empty(T, device="cuda"),
            "dlogp": torch.empty(T, device="cuda"), "loss": torch.zeros(1, device="cuda"),
            "stats": torch.zeros(4, device="cuda"), "dh": torch.empty((T, d), device="cuda"),
@@ -129,17 +133,18 @@ def test_dense_four_call_path(case):
                             rbp.workspace(rbp.RBP_OP_LOSS, T))
     rbp.policy_logprob_bwd(dev["hidden"], dev["W"], dev["tokens"], dev["seq"], out["lse"],
                            out["dlogp"], out["dh"], out["dW"],
-                           rbp.workspace(rbp.RBP_OP_LOGPROB_BWD, T, d, V))
+                           rbp.workspace(rbp.RBP_OP_LOGPROB_BWD, ws_tokens, d, V))
     torch.cuda.synchronize()
     _check(out, want, T, V, with_entropy=False)
     del out
     torch.cuda.empty_cache()
 
 
-def test_dense_single_pass(case):
+@pytest.mark.parametrize("ws_tokens", [16384, 4096])
+def test_dense_single_pass(case, ws_tokens):
     rbp, wl, dev, want = case
     T, d, V = wl.max_tokens, wl.d, wl.V
-    print("[dense] single pass", flush=True)
+    print(f"[dense] single pass, workspace for {ws_tokens} tokens", flush=True)
     out = {"logp": torch.empty(T, device="cuda"), "lse": torch.empty(T, device="cuda"),
            "ent": torch.empty(T, device="cuda"),
            "dlogp": torch.empty(T, device="cuda"), "loss": torch.zeros(1, device="cuda"),
@@ -148,7 +153,8 @@ def test_dense_single_pass(case):
     rbp.policy_fused_fwd_bwd(dev["hidden"], dev["W"], dev["tokens"], dev["seq"], dev["old"],
                              dev["adv"], dev["lens"], dev["lens"].numel(), out["logp"],
                              out["lse"], out["ent"], out["loss"], out["dlogp"], out["stats"],
-                             out["dh"], out["dW"], rbp.workspace(rbp.RBP_OP_FUSED, T, d, V))
+                             out["dh"], out["dW"],
+                             rbp.workspace(rbp.RBP_OP_FUSED, ws_tokens, d, V))
     torch.cuda.synchronize()
     _check(out, want, T, V, with_entropy=True)
     del out

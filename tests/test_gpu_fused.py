@@ -99,6 +99,26 @@ def test_fused_small_shapes(T, d, V, w_sd):
     _check(out, h64, W64, y, seq, lens, want_logp, want_lse, old, adv, n_seq)
 
 
+def test_fused_chunks_with_dhidden_in_pieces():
+    """d = 3584 with a workspace for 4096-token chunks (the bounded-workspace
+    chunk at the 7B head's width): T = 8000 runs as chunks of 4096 and 3904
+    tokens, dW accumulated over both.  Each chunk's dhidden has 16 x 14 = 224
+    tiles, a last round more than half full on 256 compute units, cut into K
+    pieces; V = 4000 keeps the full oracle cheap."""
+    rbp = require_gpu()
+    T, d, V = 8000, 3584, 4000
+    print(f"[fused] T={T} d={d} V={V}, 4096-token chunks", flush=True)
+    (hidden, W, tokens, seq, lens, h64, W64, y, want_logp, want_lse, old,
+     adv) = _case(T, d, V, 0.02, 31)
+    n_seq = len(lens)
+    dW0 = wlm.normal((V, d), 1e-3, 32, device="cuda")
+    out = _run(rbp, hidden.cuda(), W.cuda(), tokens.cuda(), torch.from_numpy(seq).cuda(),
+               torch.from_numpy(old).cuda(), torch.from_numpy(adv).cuda(),
+               torch.from_numpy(lens).cuda(), n_seq, ws_tokens=4096, dW0=dW0)
+    _check(out, h64, W64, y, seq, lens, want_logp, want_lse, old, adv, n_seq,
+           dW_extra=to_np(dW0).astype(np.float64))
+
+
 @pytest.mark.parametrize("name,T", [("head05b", 700), ("head15b", 300)])
 def test_fused_real_vocab_chunked_and_accumulating(name, T):
     """Real vocabulary (151936: a V tail), then 256-token chunks with dW

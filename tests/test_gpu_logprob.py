@@ -86,6 +86,53 @@ def test_small_shapes_fwd_bwd(T, d, V, w_sd):
     _check_grads(to_np(dh), to_np(dW), want_dh, want_dW, y, seq)
 
 
+# dhidden launches whose last round, on 256 compute units, is more than half
+# full, so that its tiles are cut into K pieces: (T, d, V)
+PIECE_SHAPES = [
+    (4096, 3584, 4000),   # 224 tiles in one round, 8 pieces of 8 K steps
+    (9316, 1024, 3001),   # 148 tiles, T and V tails: 3 pieces of 16 steps
+    (14500, 2048, 2600),  # 456 tiles: a whole round, then 200 in 5 pieces
+]
+
+
+def _dhidden_pieces(T, d, V, n_cu):
+    """Pieces per tile of the launch's last round (0: not cut), as the
+    library chooses them: a last round of r > G / 2 tiles of a G-workgroup
+    round is cut into s = 1 + ceil(r / (G - r)) <= 16 pieces of >= 8 steps,
+    the last one not empty, when the scratch ([T256][d] fp32) holds r blocks
+    of 256 x 256."""
+    G = max(8, n_cu // 8 * 8)
+    tiles = -(-d // 256) * -(-T // 256)
+    r, nk = tiles % G, -(-V // 64)
+    if 2 * r <= G or r * 65536 > -(-T // 256) * 256 * d:
+        return 0
+    s = 1 + -(-r // (G - r))
+    st = -(-nk // s)
+    return s if s <= 16 and st >= 8 and (s - 1) * st < nk else 0
+
+
+@pytest.mark.parametrize("T,d,V", PIECE_SHAPES)
+def test_dhidden_last_round_in_pieces(T, d, V):
+    rbp = require_gpu()
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    s = _dhidden_pieces(T, d, V, n_cu)
+    print(f"[logprob] T={T} d={d} V={V}: {n_cu} CUs, {s} pieces per tile", flush=True)
+    if n_cu == 256:
+        assert s > 0
+    hidden, W, tokens = wlm.head(T, d, V, seed=T + d, w_sd=0.02)
+    seq = _mask(T, T + 1)
+    h64, W64, y = bf16_to_f64(hidden), bf16_to_f64(W), to_np(tokens)
+    _, want_lse = logprob(h64, W64, y, seq)
+    hc, Wc, tc, sc = hidden.cuda(), W.cuda(), tokens.cuda(), torch.from_numpy(seq).cuda()
+    _, lse = _fwd(rbp, hc, Wc, tc, sc)
+    assert np.abs(to_np(lse) - want_lse).max() < LOGP_ATOL
+    dlogp = wlm.normal(T, 1.0, T + 2).numpy()
+    dlogp[seq < 0] = 0.0
+    want_dh, want_dW = logprob_backward(h64, W64, y, want_lse, dlogp, seq)
+    dh, dW = _bwd(rbp, hc, Wc, tc, sc, lse, torch.from_numpy(dlogp).cuda())
+    _check_grads(to_np(dh), to_np(dW), want_dh, want_dW, y, seq)
+
+
 @pytest.mark.parametrize("name,T", [("head05b", 700), ("head15b", 300)])
 def test_real_vocab_full_oracle(name, T):
     """Real vocabulary (151936 = 593.5 tiles: a V tail), several token tiles."""

@@ -59,6 +59,7 @@ def _kernels(src, fragment):
     ("logprob_fwd.hip", "logits_lse_partial_kernel"),
     ("logprob_bwd.hip", "grad_logits_kernel"),
     ("logprob_bwd.hip", "dhidden_kernel"),
+    ("logprob_bwd.hip", "dhidden_pieces_kernel"),
     ("logprob_bwd.hip", "dweight_kernel"),
     ("fused.hip", "logits_store_kernel"),
     ("fused.hip", "fused_merge_kernel"),
