@@ -51,7 +51,7 @@ TRAFFIC_SOURCES = ("fused.hip", "logprob_bwd.hip", "logits_epilogue.h", "gemm_co
 #   dW      = dweight_kernel (main launch + last-round launch) + part_add_kernel
 #   dhidden = dhidden_kernel (main launch + last-round launch) + part_add_dh_kernel
 TRAFFIC = {
-    "sources_sha256": "168aab66a530955bf19461601043a038e83b401b8324e2ced642ff4548835daf",
+    "sources_sha256": "2825da243df2c1621cbac27110d208ee401acf8a4a769cfa1f4deb269e77941d",
     "bytes": {"logits": 34395098112, "dW": 42019896320, "dhidden": 40238567424},
 }
 

@@ -147,13 +147,11 @@ __device__ __forceinline__ T* uniform_ptr(T* p) {
   return reinterpret_cast<T*>(((uint64_t)hi << 32) | lo);
 }
 
-// Cache policy of the dz^T stores: non-temporal.  32 tiles per XCD write 4 MB
-// per round -- the whole L2 -- and, cached normally, would evict the operand
-// rows the next tiles share (measured: 1.1 ms of 15.5 at T=16384, V=152064).
-#ifndef RBP_QSTORE_CPOL
-#define RBP_QSTORE_CPOL 2
-#endif
-constexpr int kStreamStore = RBP_QSTORE_CPOL;
+// Cache policy of the dz^T stores: non-temporal (cache-policy bits 2).  32
+// tiles per XCD write 4 MB per round -- the whole L2 -- and, cached normally,
+// would evict the operand rows the next tiles share (measured: 1.1 ms of 15.5
+// at T=16384, V=152064).
+constexpr int kStreamStore = 2;
 
 // One 32-row block (mi) of the wave's tile of dz = -dlogp p, stored into the
 // vocabulary-major array Gt[v][t].  B is loaded with paired rows

@@ -312,11 +312,9 @@ RBP_LOGITS_KERNEL void dweight_kernel(const uint16_t* __restrict__ Hc,
     if (accumulate && tile.n0 + 256 <= V && tile.m0 + 256 <= d) {
       // interior tile: the previous values are loaded kDwBatch float4 at a
       // time before any of them is stored back, so the tile waits for memory
-      // a few times rather than once per float4
-#ifndef RBP_DW_BATCH
-#define RBP_DW_BATCH 8
-#endif
-      constexpr int kDwBatch = RBP_DW_BATCH;  // 4, 8 or 16 (float4 per batch)
+      // a few times rather than once per float4 (batches of 4 and 16 time
+      // the same)
+      constexpr int kDwBatch = 8;
 #pragma unroll
       for (int ni = 0; ni < GL::NI; ++ni) {
         float* row = dW + (int64_t)(tile.n0 + GL::col(ni)) * d + tile.m0;
