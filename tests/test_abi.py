@@ -135,3 +135,47 @@ def test_product_path_fails_loudly_without_the_library(tmp_path):
 
     with pytest.raises(ImportError):
         b.load_library(str(tmp_path / "missing.so"))
+
+
+C_CLIENT = r"""
+#include <stdio.h>
+#include <string.h>
+#include "rbpolicy.h"
+
+int main(void) {
+  /* workspace sizes are host arithmetic: dz^T bf16 [Vp][Tc] + fp32 [Tc][d] */
+  const size_t want = (size_t)152064 * 16384 * 2 + (size_t)16384 * 3584 * 4;
+  if (rbp_workspace_bytes(RBP_OP_LOGPROB_BWD, 16384, 3584, 152064) != want) return 1;
+  /* invalid arguments are rejected on the host, before any launch */
+  if (rb_group_advantage(NULL, NULL, 3, 1, 1e-6f, NULL, NULL) != RBP_EINVAL) return 2;
+  if (strlen(rbp_last_error()) == 0) return 3;
+  if (policy_logprob_fwd(NULL, NULL, NULL, NULL, 4, 12, 10, NULL, NULL, NULL, 0, NULL) !=
+      RBP_EUNSUPPORTED) return 4;
+  if (strcmp(rbp_status_string(RBP_OK), "ok") != 0) return 5;
+  printf("c client ok\n");
+  return 0;
+}
+"""
+
+
+def test_header_compiles_as_c99_and_links(tmp_path):
+    """A plain C99 client (gcc, -pedantic -Werror) includes the header, links
+    the library and calls host-side entry points: the boundary needs no C++
+    and no torch."""
+    import shutil
+
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("needs gcc")
+    lib = _lib_path()
+    src = tmp_path / "client.c"
+    src.write_text(C_CLIENT)
+    exe = tmp_path / "client"
+    libdir = os.path.dirname(lib)
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror",
+                    "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe),
+                    "-L", libdir, "-lrbpolicy", "-Wl,-rpath," + libdir],
+                   check=True, capture_output=True, text=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, (r.returncode, r.stdout, r.stderr)
+    assert "c client ok" in r.stdout
