@@ -747,12 +747,15 @@ def main():
             "single_pass": {
                 "workspace_bytes": rbp.rbp_workspace_bytes(rbp.RBP_OP_FUSED, Tc, wl.d, wl.V),
                 "tokens_per_s": round(b_tok, 1), "ms_per_step": round(bf["ms_total"] / K, 3),
-                "mfma_peak_frac_6dV": round(b_tok * 6 * dV / PEAK_BF16, 4)},
+                "mfma_peak_frac_6dV": round(b_tok * 6 * dV / PEAK_BF16, 4),
+                # the phase events of a chunked call are those of its last chunk
+                "phase_ms_last_chunk": {k: round(v, 3) for k, v in bf["phase_ms"].items()}},
             "four_call": {
                 "workspace_bytes": rbp.rbp_workspace_bytes(rbp.RBP_OP_LOGPROB_BWD, Tc, wl.d,
                                                            wl.V),
                 "tokens_per_s": round(g_tok, 1), "ms_per_step": round(bg["ms_total"] / K, 3),
-                "mfma_peak_frac_6dV": round(g_tok * 6 * dV / PEAK_BF16, 4)},
+                "mfma_peak_frac_6dV": round(g_tok * 6 * dV / PEAK_BF16, 4),
+                "phase_ms": {k: round(v, 3) for k, v in bg["phase_ms"].items()}},
         }
     if not args.no_aux:
         rec["memory_bound_steps"] = aux_stress()
