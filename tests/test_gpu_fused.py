@@ -34,7 +34,7 @@ def _sequences(T, seed, masked=0.1, mean_len=40):
 
 
 def _run(rbp, hidden, W, tokens, seq, old, adv, slen, n_seq, ws_tokens=None, dW0=None,
-         want_entropy=True, ex=None, loss0=0.25):
+         want_entropy=True, ex=None, loss0=0.25, eps=(0.2, 0.2)):
     T, d = hidden.shape
     V = W.shape[0]
     out = {k: torch.empty(T, device="cuda") for k in ("logp", "lse", "dlogp")}
@@ -47,7 +47,8 @@ def _run(rbp, hidden, W, tokens, seq, old, adv, slen, n_seq, ws_tokens=None, dW0
     rbp.policy_fused_fwd_bwd(hidden, W, tokens, seq, old, adv, slen, n_seq, out["logp"],
                              out["lse"], out["entropy"], out["loss"], out["dlogp"],
                              out["stats"], out["dh"], out["dW"], ws,
-                             accumulate_dW=dW0 is not None, exec=ex)
+                             accumulate_dW=dW0 is not None, eps_low=eps[0], eps_high=eps[1],
+                             exec=ex)
     torch.cuda.synchronize()
     return out
 
@@ -64,13 +65,13 @@ def _case(T, d, V, w_sd, seed, device="cpu"):
 
 
 def _check(out, h64, W64, y, seq, lens, want_logp, want_lse, old, adv, n_seq, loss0=0.25,
-           dW_extra=None):
+           dW_extra=None, eps=(0.2, 0.2)):
     assert np.abs(to_np(out["logp"]) - want_logp).max() < ATOL
     assert np.abs(to_np(out["lse"]) - want_lse).max() < ATOL
     if out["entropy"] is not None:
         want_H = entropy(h64, W64, seq)
         assert np.abs(to_np(out["entropy"]) - want_H).max() < ATOL
-    loss, dlogp, st = grpo_loss(want_logp, old, seq, adv, lens, n_seq)
+    loss, dlogp, st = grpo_loss(want_logp, old, seq, adv, lens, n_seq, eps[0], eps[1])
     assert abs(to_np(out["loss"])[0] - loss0 - loss) <= RTOL * max(abs(loss), 1e-6)
     assert rel_l2(to_np(out["dlogp"]), dlogp) < RTOL
     assert to_np(out["stats"])[2] == st[2]
