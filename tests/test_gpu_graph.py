@@ -15,9 +15,9 @@ from gpu_util import DeviceRing, require_gpu
 pytestmark = pytest.mark.gpu
 
 
-def _setup(rbp):
+def _setup(rbp, T=2048, d=128, V=5000, n_draw=64):
     rng = np.random.default_rng(21)
-    n, d, V = 300, 128, 5000
+    n = 300
     length = rng.integers(1, 65, n)
     off = np.concatenate([[0], np.cumsum(length)[:-1]])
     total = int(length.sum())
@@ -26,8 +26,7 @@ def _setup(rbp):
                       rng.integers(0, V, total).astype(np.int32),
                       (rng.standard_normal(total) - 8.0).astype(np.float32), head=77,
                       capacity=400)
-    T = 2048
-    cfg = rbp.make_sample_cfg(rbp.RB_UNIFORM, rbp.RB_LAYOUT_PACKED, 5, 3, 64, cur_version=6,
+    cfg = rbp.make_sample_cfg(rbp.RB_UNIFORM, rbp.RB_LAYOUT_PACKED, 5, 3, n_draw, cur_version=6,
                               max_tokens=T)
     bufs = {
         "out": rbp.alloc_batch(cfg),
@@ -111,11 +110,13 @@ def _fused_step(rbp, ring, cfg, b, hidden, W, ex):
                              exec=ex)
 
 
-def test_fused_step_as_a_graph():
+@pytest.mark.parametrize("T,d,V,n_draw", [(2048, 128, 5000, 64), (9316, 1024, 3001, 400)])
+def test_fused_step_as_a_graph(T, d, V, n_draw):
     """The single pass captured in a graph (its listed-token count is cleared
-    by a kernel, not a memset node) replays bit for bit like the eager call."""
+    by a kernel, not a memset node) replays bit for bit like the eager call;
+    the second shape's dhidden (148 tiles) runs its round in K pieces."""
     rbp = require_gpu()
-    ring, cfg, b, hidden, W = _setup(rbp)
+    ring, cfg, b, hidden, W = _setup(rbp, T, d, V, n_draw)
     T, d = hidden.shape
     V = W.shape[0]
     b["ent"] = torch.empty(T, device="cuda")
