@@ -48,7 +48,9 @@ class Guarded:
             assert np.all(h[PAD + nbytes:] == SENTINEL), (what, i, "guard after")
 
 
-SHAPES = [(1, 8, 1), (37, 8, 300), (513, 72, 4097), (300, 136, 2049)]
+# the last two run dhidden's round in K pieces (3 and 15 per tile)
+SHAPES = [(1, 8, 1), (37, 8, 300), (513, 72, 4097), (300, 136, 2049), (9316, 1024, 3001),
+          (4133, 3584, 9000)]
 
 
 def _seq(T, seed):
