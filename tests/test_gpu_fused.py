@@ -407,3 +407,31 @@ def test_fused_tokens_off_their_reference(shift, adv_sign):
     if shift == "mixed":
         for grp in (tok_shift > 0, (tok_shift == 0) & (seq >= 0)):
             assert rel_l2(dh[grp], want_dh[grp]) < RTOL
+
+
+def test_fused_infinite_behaviour_logprobs():
+    """Tokens whose stored behaviour log-prob is -inf or +inf (ratio +inf or
+    0) in sequences with positive advantages: the objective puts them on a
+    zero-gradient branch, so dlogp, dhidden and dW stay finite and equal the
+    oracle's; their references R_t = z_y - old_logp are infinite, so the
+    single pass re-references their columns to their largest logits."""
+    rbp = require_gpu()
+    T, d, V = 300, 72, 1000
+    print(f"[fused] T={T} d={d} V={V} infinite old_logp", flush=True)
+    (hidden, W, tokens, seq, lens, h64, W64, y, want_logp, want_lse, old,
+     adv) = _case(T, d, V, 0.02, 51)
+    adv = np.abs(adv) + 0.1
+    valid = np.flatnonzero(seq >= 0)
+    pick = valid[np.linspace(0, len(valid) - 1, 12).astype(int)]
+    old = old.copy()
+    old[pick[::2]] = -np.inf
+    old[pick[1::2]] = np.inf
+    n_seq = len(lens)
+    out = _run(rbp, hidden.cuda(), W.cuda(), tokens.cuda(), torch.from_numpy(seq).cuda(),
+               torch.from_numpy(old).cuda(), torch.from_numpy(adv).cuda(),
+               torch.from_numpy(lens).cuda(), n_seq)
+    for k in ("logp", "lse", "entropy", "dlogp", "dh", "dW", "loss"):
+        assert np.isfinite(to_np(out[k])).all(), k
+    assert np.all(to_np(out["dlogp"])[pick] == 0)
+    with np.errstate(over="ignore", invalid="ignore"):
+        _check(out, h64, W64, y, seq, lens, want_logp, want_lse, old, adv, n_seq)
