@@ -282,3 +282,22 @@ def test_maximum_draw_count_packed():
     want = ob.gather(idx, r["arena_off"], r["length"], r["adv"], r["version"], r["tok"],
                      r["old"], 10, ob.LAYOUT_PACKED, **lk)
     _compare(got, want)
+
+
+@pytest.mark.parametrize("n_fresh,n_pos_keep", [(0, 0), (0, 5)])
+def test_pos_retain_empty_set_draws_slot_zero(n_fresh, n_pos_keep):
+    """Positive-bias retention with an empty retained set (no fresh slots
+    and no positive record to keep): the documented fallback draws logical
+    slot 0 every time, and the batch is the gather of those draws."""
+    rbp = require_gpu()
+    wl = wlm.WORKLOADS["tiny"]
+    tab, tok, old, adv = _host_table(wl, 3)
+    reward = np.zeros_like(tab.reward)  # no positives
+    ring = DeviceRing(rbp, tab.length, tab.arena_off, reward, adv, tab.version, tok, old,
+                      head=11, capacity=80)
+    kw = dict(n_fresh=n_fresh, n_pos_keep=n_pos_keep, l_max=40)
+    got = _run(rbp, ring, "pos_retain", "padded", 4, 2, 16, **kw)
+    assert np.all(got["idx"] == 0)
+    want = ob.gather([0] * 16, tab.arena_off, tab.length, adv, tab.version, tok, old, 10,
+                     ob.LAYOUT_PADDED, 0, 0, 40)
+    _compare(got, want)
