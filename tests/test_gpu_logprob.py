@@ -221,6 +221,13 @@ def test_bitwise_reproducible_and_bad_args():
     g1 = _bwd(rbp, hidden, W, tokens, None, a[1], dlogp)
     g2 = _bwd(rbp, hidden, W, tokens, None, a[1], dlogp)
     assert torch.equal(g1[0], g2[0]) and torch.equal(g1[1], g2[1])
+    # a NULL seq_of_token means every token is valid: the same bits as an
+    # all-zero one
+    all_valid = torch.zeros(T, dtype=torch.int32, device="cuda")
+    c = _fwd(rbp, hidden, W, tokens, all_valid)
+    assert torch.equal(a[0], c[0]) and torch.equal(a[1], c[1])
+    g3 = _bwd(rbp, hidden, W, tokens, all_valid, a[1], dlogp)
+    assert torch.equal(g1[0], g3[0]) and torch.equal(g1[1], g3[1])
     h12 = torch.zeros((4, 12), dtype=torch.bfloat16, device="cuda")
     W12 = torch.zeros((5, 12), dtype=torch.bfloat16, device="cuda")
     t4 = torch.zeros(4, dtype=torch.int32, device="cuda")
