@@ -106,3 +106,29 @@ def test_zero_advantage_contributes_nothing():
     old = logp + 0.5
     loss, dlogp, _ = grpo_loss(logp, old, seq, adv, lens, len(lens))
     assert loss == 0.0 and np.all(dlogp == 0.0)
+
+
+@pytest.mark.parametrize("A,rho,active,term", [
+    (1.0, 1.3 + 1e-3, False, 1.3),          # above 1 + eps_high, A > 0: clipped
+    (1.0, 1.25, True, 1.25),                 # inside (outside if the bounds were swapped)
+    (1.0, 0.85, True, 0.85),                 # below 1 - eps_low, A > 0: unclipped side
+    (-1.0, 0.9 - 1e-3, False, -0.9),         # below 1 - eps_low, A < 0: clipped
+    (-1.0, 0.75, False, -0.9),               # (inside if the bounds were swapped)
+    (-1.0, 0.95, True, -0.95),               # inside
+    (-1.0, 1.4, True, -1.4),                 # above 1 + eps_high, A < 0: unclipped side
+])
+def test_asymmetric_clip_range(A, rho, active, term):
+    """eps_low = 0.1, eps_high = 0.3: the lower bound is 0.9, the upper 1.3,
+    so a mistake that swaps or merges the two ranges changes these cases."""
+    old = np.array([-2.0])
+    logp = old + np.log(rho)
+    loss, dlogp, st = grpo_loss(logp, old, np.array([0]), np.array([A]), np.array([1]), 1,
+                                eps_low=0.1, eps_high=0.3)
+    r = np.exp(logp[0] - old[0])
+    assert -loss == pytest.approx(term, rel=1e-9)
+    if active:
+        assert dlogp[0] == pytest.approx(-A * r, rel=1e-12)
+        assert st[1] == 0
+    else:
+        assert dlogp[0] == 0.0
+        assert st[1] == 1

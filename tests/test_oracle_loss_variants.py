@@ -129,3 +129,23 @@ def test_seq_ratio_matches_finite_differences_away_from_kinks():
         fd = (grpo_seq_loss(logp + e, old, cu, adv, n_seq)[0]
               - grpo_seq_loss(logp - e, old, cu, adv, n_seq)[0]) / (2 * h)
         assert fd == pytest.approx(dlogp[t], rel=1e-6, abs=1e-10)
+
+
+def test_seq_ratio_asymmetric_clip_range():
+    """eps_low = 0.1, eps_high = 0.3: a sequence ratio of e^0.25 = 1.28 lies
+    inside (it would be clipped with the bounds swapped), one of e^0.3 = 1.35
+    above; e^-0.2 = 0.82 lies below the lower bound 0.9."""
+    logp = np.array([-1.0, -2.0])
+    cu = [0, 2]
+    for shift, A, clipped in ((0.125, 1.0, False), (0.15, 1.0, True), (-0.1, -1.0, True),
+                              (-0.1, 1.0, False)):
+        old = logp - shift
+        rho = np.exp(2 * shift)
+        loss, d, st = grpo_seq_loss(logp, old, cu, [A], 1, eps_low=0.1, eps_high=0.3)
+        if clipped:
+            assert np.all(d == 0) and st[1] == 1
+            bound = 1.3 if A > 0 else 0.9
+            assert -loss == pytest.approx(bound * A, rel=1e-12)
+        else:
+            assert np.allclose(d, -A * rho, rtol=1e-12) and st[1] == 0
+            assert -loss == pytest.approx(rho * A, rel=1e-12)

@@ -1,0 +1,123 @@
+"""The oracle's pins catch plausible mistakes (CPU only).  Each case plants
+one mistake in an oracle function -- a swapped pair of bounds, a dropped
+term, a wrong sign, an index off by one, rows misaligned with their tokens,
+the other variance estimator, a rounding instead of a floor, a window one
+slot too wide -- by wrapping it under the name a pin test calls it by, then
+runs pins of that function and requires at least one of them to fail.  The
+oracle itself is untouched; the mistakes live in this file only."""
+
+import numpy as np
+import pytest
+
+import oracle.buffer as ob_mod
+import oracle.philox as philox_mod
+import test_oracle_advantage as t_adv
+import test_oracle_buffer as t_buf
+import test_oracle_grad as t_grad
+import test_oracle_logprob as t_lp
+import test_oracle_loss as t_loss
+import test_oracle_loss_variants as t_var
+import test_oracle_philox as t_ph
+
+
+def _some_pin_fails(pins):
+    failed = []
+    for pin in pins:
+        try:
+            pin()
+        except AssertionError:
+            failed.append(pin)
+    return failed
+
+
+def _mutations(golden_dir):
+    from oracle.advantage import group_advantage
+    from oracle.grad import logprob_backward
+    from oracle.logprob import entropy, logprob
+    from oracle.loss import grpo_loss, grpo_seq_loss
+
+    def swapped_bounds(*a, eps_low=0.2, eps_high=0.2):
+        return grpo_loss(*a, eps_low=eps_high, eps_high=eps_low)
+
+    def flipped_gradient(*a, **k):
+        loss, d, st = grpo_loss(*a, **k)
+        return loss, -d, st
+
+    def lengths_dropped(logp, old, seq, adv, lens, n_seq, **k):
+        return grpo_loss(logp, old, seq, adv, np.ones_like(np.asarray(lens)), n_seq, **k)
+
+    def target_off_by_one(h, W, y, *a, **k):
+        return logprob(h, W, (np.asarray(y) + 1) % np.asarray(W).shape[0], *a, **k)
+
+    def backward_sign(*a, **k):
+        dh, dW = logprob_backward(*a, **k)
+        return -dh, -dW
+
+    def rows_misaligned(h, *a, **k):
+        return logprob_backward(np.roll(np.asarray(h), 1, axis=0), *a, **k)
+
+    def entropy_sign(h, W, *a, **k):
+        return -entropy(h, W, *a, **k)
+
+    def other_std(rewards, group_off, ddof=1, eps=1e-6):
+        return group_advantage(rewards, group_off, ddof=1 - ddof, eps=eps)
+
+    def seq_bounds_swapped(*a, eps_low=0.2, eps_high=0.2):
+        return grpo_seq_loss(*a, eps_low=eps_high, eps_high=eps_low)
+
+    real_uniform = philox_mod.uniform_index
+
+    def rounded_index(x, n):
+        return min(int(round(int(x) * int(n) / 2**64)), int(n) - 1)
+
+    real_retained = ob_mod.retained_set
+
+    def window_too_wide(rewards, n_fresh, n_pos_keep):
+        return real_retained(rewards, int(n_fresh) + 1, n_pos_keep)
+
+    return [
+        ("token clip bounds swapped", t_loss, "grpo_loss", swapped_bounds,
+         [lambda: t_loss.test_asymmetric_clip_range(1.0, 1.25, True, 1.25),
+          lambda: t_loss.test_asymmetric_clip_range(-1.0, 0.75, False, -0.9)]),
+        ("gradient sign flipped", t_loss, "grpo_loss", flipped_gradient,
+         [t_loss.test_finite_differences_away_from_kinks, t_loss.test_on_policy_identity]),
+        ("per-sequence token mean dropped", t_loss, "grpo_loss", lengths_dropped,
+         [t_loss.test_on_policy_identity]),
+        ("target index off by one", t_lp, "logprob", target_off_by_one,
+         [t_lp.test_pure_python_brute_force_tiny, t_lp.test_against_scipy_logsumexp]),
+        ("backward sign flipped", t_grad, "logprob_backward", backward_sign,
+         [t_grad.test_finite_differences_of_the_whole_path]),
+        ("hidden rows misaligned with their tokens", t_grad, "logprob_backward",
+         rows_misaligned, [t_grad.test_finite_differences_of_the_whole_path]),
+        ("entropy sign flipped", t_lp, "entropy", entropy_sign,
+         [t_lp.test_entropy_of_uniform_logits_is_log_v]),
+        ("population instead of sample spread", t_adv, "group_advantage", other_std,
+         [lambda: t_adv.test_binary_rewards_closed_form(4), t_adv.test_population_std_closed_form]),
+        ("sequence clip bounds swapped", t_var, "grpo_seq_loss", seq_bounds_swapped,
+         [t_var.test_seq_ratio_asymmetric_clip_range]),
+        ("index rounded instead of floored", philox_mod, "uniform_index", rounded_index,
+         [lambda: t_ph.test_uniform_index_is_floor_of_scaled_word(3),
+          lambda: t_ph.test_uniform_index_is_floor_of_scaled_word(1000)]),
+        ("retention window one slot too wide", ob_mod, "retained_set", window_too_wide,
+         [lambda: t_buf.test_paper_worked_example_positive_bias(golden_dir),
+          t_buf.test_retain_brute_force_definition]),
+    ]
+
+
+CASES = ["token clip bounds swapped", "gradient sign flipped", "per-sequence token mean dropped",
+         "target index off by one", "backward sign flipped",
+         "hidden rows misaligned with their tokens", "entropy sign flipped",
+         "population instead of sample spread", "sequence clip bounds swapped",
+         "index rounded instead of floored", "retention window one slot too wide"]
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_pins_catch_a_planted_mistake(name, golden_dir, monkeypatch):
+    muts = {m[0]: m for m in _mutations(golden_dir)}
+    assert set(muts) == set(CASES)
+    _, where, attr, wrong, pins = muts[name]
+    # the pins pass on the oracle as it is ...
+    assert not _some_pin_fails(pins), name
+    # ... and at least one fails with the mistake planted
+    monkeypatch.setattr(where, attr, wrong)
+    assert _some_pin_fails(pins), f"no pin caught: {name}"
