@@ -1,8 +1,9 @@
 """The oracle's pins catch plausible mistakes (CPU only).  Each case plants
 one mistake in an oracle function -- a swapped pair of bounds, a dropped
 term, a wrong sign, an index off by one, rows misaligned with their tokens,
-the other variance estimator, a rounding instead of a floor, a window one
-slot too wide -- by wrapping it under the name a pin test calls it by, then
+the other variance estimator, eps inside the square root, a rounding
+instead of a floor, a window one slot too wide, steps counted one too many,
+a dropped tail bin -- by wrapping it under the name a pin test calls it by, then
 runs pins of that function and requires at least one of them to fail.  The
 oracle itself is untouched; the mistakes live in this file only."""
 
@@ -75,6 +76,31 @@ def _mutations(golden_dir):
     def window_too_wide(rewards, n_fresh, n_pos_keep):
         return real_retained(rewards, int(n_fresh) + 1, n_pos_keep)
 
+    def eps_inside_the_root(rewards, group_off, ddof=1, eps=1e-6):
+        # A = (r - mean) / sqrt(var + eps) instead of / (std + eps)
+        out = []
+        for g in range(len(group_off) - 1):
+            r = [float(x) for x in rewards[group_off[g]:group_off[g + 1]]]
+            base = group_advantage(r, [0, len(r)], ddof=ddof, eps=0.0)
+            n = len(r)
+            if n - ddof <= 0 or all(v == 0.0 for v in base):
+                out += [0.0] * n
+                continue
+            m = sum(r) / n
+            var = sum((v - m) ** 2 for v in r) / (n - ddof)
+            out += [(v - m) / (var + eps) ** 0.5 for v in r]
+        return out
+
+    real_since = ob_mod.steps_since_last_use
+
+    def since_off_by_one(batches):
+        return [[v if v < 0 else v + 1 for v in b] for b in real_since(batches)]
+
+    real_hist = ob_mod.histogram
+
+    def tail_bin_dropped(values, n_bins, lo=0):
+        return real_hist([v for v in values if v - lo < n_bins], n_bins, lo)
+
     return [
         ("token clip bounds swapped", t_loss, "grpo_loss", swapped_bounds,
          [lambda: t_loss.test_asymmetric_clip_range(1.0, 1.25, True, 1.25),
@@ -101,6 +127,13 @@ def _mutations(golden_dir):
         ("retention window one slot too wide", ob_mod, "retained_set", window_too_wide,
          [lambda: t_buf.test_paper_worked_example_positive_bias(golden_dir),
           t_buf.test_retain_brute_force_definition]),
+        ("eps inside the square root", t_adv, "group_advantage", eps_inside_the_root,
+         [lambda: t_adv.test_one_outlier_closed_form(8, 0.1, 3)]),
+        ("steps since last use off by one", ob_mod, "steps_since_last_use", since_off_by_one,
+         [lambda: t_buf.test_steps_since_last_use_paper_example(golden_dir),
+          t_buf.test_steps_since_last_use_brute_force]),
+        ("histogram tail bin dropped", ob_mod, "histogram", tail_bin_dropped,
+         [t_buf.test_histogram_bins_by_hand]),
     ]
 
 
@@ -108,7 +141,9 @@ CASES = ["token clip bounds swapped", "gradient sign flipped", "per-sequence tok
          "target index off by one", "backward sign flipped",
          "hidden rows misaligned with their tokens", "entropy sign flipped",
          "population instead of sample spread", "sequence clip bounds swapped",
-         "index rounded instead of floored", "retention window one slot too wide"]
+         "index rounded instead of floored", "retention window one slot too wide",
+         "eps inside the square root", "steps since last use off by one",
+         "histogram tail bin dropped"]
 
 
 @pytest.mark.parametrize("name", CASES)
