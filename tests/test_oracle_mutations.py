@@ -3,7 +3,8 @@ one mistake in an oracle function -- a swapped pair of bounds, a dropped
 term, a wrong sign, an index off by one, rows misaligned with their tokens,
 the other variance estimator, eps inside the square root, a rounding
 instead of a floor, a window one slot too wide, steps counted one too many,
-a dropped tail bin -- by wrapping it under the name a pin test calls it by, then
+a dropped tail bin, the draw counter's words swapped, a packed window
+shifted by one token -- by wrapping it under the name a pin test calls it by, then
 runs pins of that function and requires at least one of them to fail.  The
 oracle itself is untouched; the mistakes live in this file only."""
 
@@ -98,6 +99,18 @@ def _mutations(golden_dir):
 
     real_hist = ob_mod.histogram
 
+    real_block = philox_mod.draw_block
+
+    def counter_words_swapped(seed, step, j):
+        return real_block(seed, j, step)
+
+    real_gather = ob_mod.gather
+
+    def window_off_by_one(*a, **k):
+        if k.get("layout", a[8] if len(a) > 8 else None) == ob_mod.LAYOUT_PACKED:
+            k = dict(k, token_begin=k.get("token_begin", 0) + 1)
+        return real_gather(*a, **k)
+
     def tail_bin_dropped(values, n_bins, lo=0):
         return real_hist([v for v in values if v - lo < n_bins], n_bins, lo)
 
@@ -134,6 +147,10 @@ def _mutations(golden_dir):
           t_buf.test_steps_since_last_use_brute_force]),
         ("histogram tail bin dropped", ob_mod, "histogram", tail_bin_dropped,
          [t_buf.test_histogram_bins_by_hand]),
+        ("draw counter words swapped", philox_mod, "draw_block", counter_words_swapped,
+         [t_ph.test_draw_block_counter_layout]),
+        ("packed window shifted by one token", ob_mod, "gather", window_off_by_one,
+         [t_buf.test_gather_packed_windows_tile_the_stream]),
     ]
 
 
@@ -143,7 +160,8 @@ CASES = ["token clip bounds swapped", "gradient sign flipped", "per-sequence tok
          "population instead of sample spread", "sequence clip bounds swapped",
          "index rounded instead of floored", "retention window one slot too wide",
          "eps inside the square root", "steps since last use off by one",
-         "histogram tail bin dropped"]
+         "histogram tail bin dropped", "draw counter words swapped",
+         "packed window shifted by one token"]
 
 
 @pytest.mark.parametrize("name", CASES)
