@@ -3,7 +3,8 @@ one mistake in an oracle function -- a swapped pair of bounds, a dropped
 term, a wrong sign, an index off by one, rows misaligned with their tokens,
 the other variance estimator, eps inside the square root, a rounding
 instead of a floor, a window one slot too wide, steps counted one too many,
-a dropped tail bin, the draw counter's words swapped, a packed window
+a dropped tail bin, the AsymRE offset's sign flipped or its loss
+normalised per token instead of per sequence, the draw counter's words swapped, a packed window
 shifted by one token -- by wrapping it under the name a pin test calls it by, then
 runs pins of that function and requires at least one of them to fail.  The
 oracle itself is untouched; the mistakes live in this file only."""
@@ -36,7 +37,7 @@ def _mutations(golden_dir):
     from oracle.advantage import group_advantage
     from oracle.grad import logprob_backward
     from oracle.logprob import entropy, logprob
-    from oracle.loss import grpo_loss, grpo_seq_loss
+    from oracle.loss import asymre_coef, asymre_loss, grpo_loss, grpo_seq_loss
 
     def swapped_bounds(*a, eps_low=0.2, eps_high=0.2):
         return grpo_loss(*a, eps_low=eps_high, eps_high=eps_low)
@@ -99,6 +100,14 @@ def _mutations(golden_dir):
 
     real_hist = ob_mod.histogram
 
+    def offset_sign_flipped(rewards, group_off, delta_v=-0.1):
+        return asymre_coef(rewards, group_off, -delta_v)
+
+    def asymre_normalised_per_token(logp, seq, coef, n_seq):
+        # divides by the number of valid tokens instead of the sequences
+        n_tok = int(np.sum(np.asarray(seq) >= 0))
+        return asymre_loss(logp, seq, coef, max(n_tok, 1))
+
     real_block = philox_mod.draw_block
 
     def counter_words_swapped(seed, step, j):
@@ -147,6 +156,11 @@ def _mutations(golden_dir):
           t_buf.test_steps_since_last_use_brute_force]),
         ("histogram tail bin dropped", ob_mod, "histogram", tail_bin_dropped,
          [t_buf.test_histogram_bins_by_hand]),
+        ("AsymRE offset sign flipped", t_var, "asymre_coef", offset_sign_flipped,
+         [t_var.test_asymre_coef_group_sum_fixes_the_sign_of_delta_v]),
+        ("AsymRE normalised per token", t_var, "asymre_loss", asymre_normalised_per_token,
+         [t_var.test_asymre_gradient_is_constant_per_sequence_and_matches_finite_differences,
+          t_var.test_asymre_shift_identity_and_masking]),
         ("draw counter words swapped", philox_mod, "draw_block", counter_words_swapped,
          [t_ph.test_draw_block_counter_layout]),
         ("packed window shifted by one token", ob_mod, "gather", window_off_by_one,
@@ -160,7 +174,8 @@ CASES = ["token clip bounds swapped", "gradient sign flipped", "per-sequence tok
          "population instead of sample spread", "sequence clip bounds swapped",
          "index rounded instead of floored", "retention window one slot too wide",
          "eps inside the square root", "steps since last use off by one",
-         "histogram tail bin dropped", "draw counter words swapped",
+         "histogram tail bin dropped", "AsymRE offset sign flipped",
+         "AsymRE normalised per token", "draw counter words swapped",
          "packed window shifted by one token"]
 
 
