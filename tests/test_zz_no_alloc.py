@@ -83,3 +83,49 @@ def test_noalloc_rejects_tables_beyond_its_scratch():
     # the largest table it takes
     ok = rbp.rbp_workspace_bytes(rbp.RBP_OP_SAMPLE_GATHER, 1_500_000) <= 32 << 20
     assert ok
+
+
+def _largest_capacity(rbp, limit=32 << 20):
+    lo, hi = 1, 1 << 24
+    while lo < hi:  # largest capacity whose workspace fits the scratch
+        mid = (lo + hi + 1) // 2
+        if rbp.rbp_workspace_bytes(rbp.RBP_OP_SAMPLE_GATHER, mid) <= limit:
+            lo = mid
+        else:
+            hi = mid - 1
+    return lo
+
+
+def test_noalloc_at_the_largest_table_its_scratch_holds():
+    """The largest record table the 32 MiB scratch holds (every slot live, the
+    ring's head inside it) matches the workspace call bit for bit, without
+    and with replacement; one slot more is refused on the host."""
+    rbp = require_gpu()
+    cap = _largest_capacity(rbp)
+    print(f"[noalloc] largest capacity {cap}", flush=True)
+    assert 1_500_000 < cap < 1_700_000
+    rng = np.random.default_rng(77)
+    length = rng.integers(1, 5, cap)
+    off = np.concatenate([[0], np.cumsum(length)[:-1]])
+    total = int(length.sum())
+    ring = DeviceRing(rbp, length, off, (rng.random(cap) < 0.4).astype(np.float32),
+                      rng.standard_normal(cap).astype(np.float32), rng.integers(0, 5, cap),
+                      rng.integers(0, 152064, total).astype(np.int32),
+                      rng.standard_normal(total).astype(np.float32), head=cap // 3,
+                      capacity=cap)
+    for mode, layout, n_draw, extra in (
+            (rbp.RB_NO_REPLACE, rbp.RB_LAYOUT_PADDED, 512, {"l_max": 8}),
+            (rbp.RB_UNIFORM, rbp.RB_LAYOUT_PACKED, 4096, {"max_tokens": 8192})):
+        cfg = rbp.make_sample_cfg(mode, layout, 3, 11, n_draw, cur_version=7, **extra)
+        _compare(rbp, ring.rec, cfg)
+    big = rbp.make_records(cap, cap + 1, 0, torch.cat([ring.t_off, ring.t_off[:1]]),
+                           torch.cat([ring.t_len, ring.t_len[:1]]),
+                           torch.cat([ring.t_rew, ring.t_rew[:1]]),
+                           torch.cat([ring.t_adv, ring.t_adv[:1]]),
+                           torch.cat([ring.t_ver, ring.t_ver[:1]]), ring.t_tok, ring.t_old)
+    cfg = rbp.make_sample_cfg(rbp.RB_UNIFORM, rbp.RB_LAYOUT_PACKED, 1, 0, 4, max_tokens=100)
+    with pytest.raises(rbp.RbpError) as e:
+        rbp.rb_sample_gather_noalloc(big, cfg, rbp.alloc_batch(cfg))
+    assert e.value.status == rbp.RBP_EWORKSPACE
+    del ring, big
+    torch.cuda.empty_cache()
